@@ -1,0 +1,209 @@
+/* adst.h — reverse-mode gradients of time-iterated stencil programs under a
+ * checkpoint-memory budget, on AMD MI355X (gfx950).
+ *
+ * The operation (DaCe AD, arXiv 2509.02197): given an unmodified time loop
+ *     x_t = F(x_{t-1}; K),  t = 1..T,
+ * and one scalar output L(x_T), return the vector-Jacobian products
+ *     dx0 = dL/dx_0   and   dK = dL/dK
+ * (Sec. II: the backward pass computes gradients of one dependent variable
+ * with respect to a set of independent inputs; Sec. III-A limitations: a
+ * single scalar output per gradient). The forward values the reverse sweep
+ * needs are either stored or recomputed from checkpoints so that storage stays
+ * within a caller-given byte budget (Sec. IV: store/recompute trade-off under
+ * a user memory constraint, store-all as the default and a manual choice
+ * available). Recomputation changes where x_{t-1} comes from, never the
+ * gradient: results are bit-identical across every budget and schedule.
+ *
+ * Step kinds (F), arrays row-major [nz][ny][nx] with x fastest, unpadded:
+ *   ADST_JACOBI2D5    2-D, 5-point average on interior points, outer ring held
+ *                     fixed.  x'[c] = w*((((x[c]+x[W])+x[E])+x[S])+x[N]);
+ *                     p[0] = w (0.2).
+ *   ADST_ALLENCAHN3D7 3-D (nz >= 1), every point updated, out-of-grid
+ *                     neighbours read 0.  lap = (((((x[-x]+x[+x])+x[-y])+x[+y])
+ *                     +x[-z])+x[+z]) - 6*x[c];  x' = (x[c] + D*lap) - C*((x[c]*x[c])*x[c]);
+ *                     p[0] = D (0.1), p[1] = C (0.1).
+ *   ADST_VARDIFF2D9   2-D, x' = x[c] + dt*acc with acc the left-to-right sum
+ *                     over the in-grid neighbours n in the order
+ *                     (-1,0),(+1,0),(0,-1),(0,+1),(-1,-1),(+1,-1),(-1,+1),(+1,+1)
+ *                     of (c_n*(K[c]+K[n]))*(x[n]-x[c]); c_n = 1/3 on the axes
+ *                     and 1/12 on the diagonals (rounded to the working
+ *                     precision); edges leaving the grid are dropped (no flux).
+ *                     p[0] = dt (0.1). The per-point field K is the
+ *                     coefficient ("coeff") whose gradient dK may be asked for.
+ * Each forward formula is evaluated in the order written, in the working
+ * precision, without fused multiply-add contraction.
+ *
+ * Conventions for every call:
+ *   - All device memory is caller-owned; adst never allocates or frees device
+ *     memory. Pointers are device addresses on the current HIP device.
+ *   - Inputs (x0, coeff, loss_aux) are read-only; x0 serves as the free base
+ *     checkpoint and must stay untouched until the stream reaches the call.
+ *   - Outputs are overwritten (=, never +=).
+ *   - Calls that take a stream only enqueue work on it and never synchronise,
+ *     except with ADST_TRACE set (see below). Argument errors are detected
+ *     before anything is enqueued.
+ *   - On failure the call returns a non-zero adst_status and
+ *     adst_last_error() holds a thread-local description.
+ */
+#ifndef ADST_H
+#define ADST_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ADST_OK = 0,
+  ADST_ERR_ARG = 1,         /* NULL required pointer, bad shape/steps/enum, overlapping ranges */
+  ADST_ERR_BUDGET = 2,      /* STORE_ALL asked for but the budget cannot hold its slots */
+  ADST_ERR_WORKSPACE = 3,   /* ws_bytes below what the plan needs */
+  ADST_ERR_UNSUPPORTED = 4, /* kind/dtype/dimension combination not built */
+  ADST_ERR_HIP = 5          /* a HIP launch or runtime call failed */
+} adst_status;
+
+typedef enum { ADST_JACOBI2D5 = 0, ADST_ALLENCAHN3D7 = 1, ADST_VARDIFF2D9 = 2 } adst_kind;
+typedef enum { ADST_F64 = 0, ADST_F32 = 1 } adst_dtype;
+
+/* Checkpoint schedules (Sec. IV: store-all default, a manual choice, or an
+ * automatic one within the memory limit).
+ *   STORE_ALL  keep every state the reverse sweep reads; no recomputation.
+ *   UNIFORM    checkpoints every k = ceil(T/c) steps, one-level recompute.
+ *   BINOMIAL   optimal for a single time loop with uniform step cost
+ *              (Revolve, cited in the related work): minimal forward steps
+ *              for the c checkpoints the budget allows.
+ *   AUTO       STORE_ALL if it fits the budget, else BINOMIAL. */
+typedef enum {
+  ADST_SCHED_AUTO = 0,
+  ADST_SCHED_STORE_ALL = 1,
+  ADST_SCHED_UNIFORM = 2,
+  ADST_SCHED_BINOMIAL = 3
+} adst_sched;
+
+/* The scalar output L. Its value is accumulated in double whatever the
+ * working precision; the seed g_T = dL/dx_T is in the working precision.
+ *   HALF_SQ       L = sum 0.5*x_T^2,            g_T = x_T        (aux unused)
+ *   DOT_W         L = sum aux*x_T,              g_T = aux
+ *   HALF_SQ_DIFF  d = x_T - aux, L = sum 0.5*d^2, g_T = d
+ *   SEED          g_T = aux (explicit cotangent), L = sum aux*x_T */
+typedef enum {
+  ADST_LOSS_HALF_SQ = 0,
+  ADST_LOSS_DOT_W = 1,
+  ADST_LOSS_HALF_SQ_DIFF = 2,
+  ADST_LOSS_SEED = 3
+} adst_loss;
+
+/* Problem flags. */
+#define ADST_FORCE_TAPE 0x1u /* treat every step as reading x_{t-1} in its adjoint, even when
+                                the kind is linear, so store/recompute runs at any shape */
+#define ADST_TRACE 0x2u      /* time every launch with HIP events, synchronise the stream at
+                                the end of the call and fill the ms_* fields of adst_plan_info */
+
+typedef struct {
+  int32_t kind;   /* adst_kind */
+  int32_t dtype;  /* adst_dtype */
+  int64_t n[3];   /* n[0] = nx (fastest), n[1] = ny, n[2] = nz (1 for the 2-D kinds);
+                     every n[i] >= 1 and n[0]*n[1]*n[2] < 2^31 */
+  double p[2];    /* step constants, see the kinds above; rounded to the working precision */
+  uint32_t flags; /* ADST_FORCE_TAPE | ADST_TRACE */
+} adst_problem;
+
+/* One action of a reverse-sweep plan. Buffers are named by small integers:
+ * ADST_BUF_X0 the caller's x0, ADST_BUF_W0/W1 two work states, ADST_BUF_XT
+ * the buffer that receives x_T, and ADST_BUF_SLOT0 + k checkpoint slot k.
+ *   ADST_OP_FWD   x_t = F(state in src), written to dst
+ *   ADST_OP_SEED  loss and seed g_T from x_T held in src (t = T)
+ *   ADST_OP_ADJ   g_{t-1} = J_t^T g_t, reading x_{t-1} from src
+ *                 (src = ADST_BUF_NONE when the step's adjoint reads no state) */
+typedef enum { ADST_OP_FWD = 0, ADST_OP_SEED = 1, ADST_OP_ADJ = 2 } adst_op;
+enum {
+  ADST_BUF_NONE = -1,
+  ADST_BUF_X0 = 0,
+  ADST_BUF_W0 = 1,
+  ADST_BUF_W1 = 2,
+  ADST_BUF_XT = 3,
+  ADST_BUF_SLOT0 = 4
+};
+typedef struct {
+  int32_t op;
+  int32_t t;
+  int32_t src;
+  int32_t dst;
+} adst_action;
+
+typedef struct {
+  int32_t steps;            /* T */
+  int32_t sched;            /* schedule actually used (never AUTO) */
+  int32_t slots;            /* checkpoint slots used, x0 excluded (c = slots + 1) */
+  int32_t needs_state;      /* 1 if the adjoint reads x_{t-1} */
+  int64_t fwd_steps_total;  /* forward-step launches: sweep (T) + recompute */
+  int64_t recompute_steps;  /* fwd_steps_total - T */
+  int64_t adj_steps;        /* T */
+  int64_t n_actions;        /* length of the action list */
+  uint64_t state_bytes;     /* bytes of one state */
+  uint64_t budget_bytes;    /* the budget passed in */
+  uint64_t slot_bytes_peak; /* slots * state_bytes: checkpoint storage actually used */
+  uint64_t workspace_bytes; /* ws bytes adst_vjp needs for this plan */
+  uint64_t fwd_workspace_bytes; /* ws bytes adst_forward needs */
+  uint64_t alg_bytes;       /* algorithmic HBM bytes of one adst_vjp call */
+  float ms_fwd_sweep;       /* ADST_TRACE only: summed kernel time of the first T forward steps */
+  float ms_fwd_recompute;   /*   ... of the recomputed forward steps */
+  float ms_adj;             /*   ... of the adjoint steps */
+  float ms_seed;            /*   ... of the loss/seed and its final reduction */
+  float ms_total;           /*   first launch start to last launch end */
+  float reserved;
+} adst_plan_info;
+
+/* Plan a forward+VJP call without touching the GPU (host only).
+ * The budget counts checkpoint-slot storage only: slots = floor(budget /
+ * state_bytes); x0 is the caller's and is the free base checkpoint, so the
+ * schedule has c = slots + 1 checkpoints. want_dcoeff != 0 asks for dK
+ * (VARDIFF2D9 only), which makes its adjoint read x_{t-1}.
+ * Errors: ADST_ERR_ARG (NULL prob/out, steps < 0, bad kind/dtype/sched, bad
+ * shape), ADST_ERR_UNSUPPORTED (shape not valid for the kind, or dK asked for
+ * a kind without a coefficient field), ADST_ERR_BUDGET (STORE_ALL does not fit). */
+adst_status adst_plan(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
+                      int32_t sched, int32_t want_dcoeff, adst_plan_info* out);
+
+/* The same plan as its action list (host only; for tests and inspection).
+ * Writes min(cap, n) actions to out (out may be NULL when cap == 0) and the
+ * full length to *n_out. Same errors as adst_plan. */
+adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
+                              int32_t sched, int32_t want_dcoeff, adst_action* out, int64_t cap,
+                              int64_t* n_out);
+
+/* x_T after `steps` forward steps (the unmodified program). coeff is K for
+ * VARDIFF2D9 and must be NULL-or-ignored otherwise. ws must hold
+ * adst_plan_info.fwd_workspace_bytes (one state when steps >= 2, else 0).
+ * Errors: as adst_plan, plus ADST_ERR_WORKSPACE and ADST_ERR_HIP. */
+adst_status adst_forward(const adst_problem* prob, const void* x0, const void* coeff,
+                         int32_t steps, void* xT, void* ws, uint64_t ws_bytes,
+                         hipStream_t stream);
+
+/* Forward sweep, loss, and reverse sweep under the budget, enqueued on
+ * `stream`. Outputs: dx0 (required), dcoeff (dK, VARDIFF2D9 only, NULL = not
+ * requested), xT (optional), loss_dev (optional device double). ws must hold
+ * adst_plan_info.workspace_bytes and is clobbered. dx0 doubles as one of the
+ * two adjoint buffers. steps = 0 is valid: dx0 = seed, dK = 0.
+ * info (optional, host) receives the plan; with ADST_TRACE it also receives
+ * the per-phase kernel times, and the call synchronises the stream.
+ * Errors: as adst_plan, plus ADST_ERR_ARG for overlapping input/output ranges
+ * or a missing loss_aux, ADST_ERR_WORKSPACE, ADST_ERR_HIP. */
+adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
+                     int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
+                     void* dx0, void* dcoeff, void* xT, double* loss_dev, void* ws,
+                     uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info);
+
+/* Static description of a status code. */
+const char* adst_status_str(adst_status status);
+
+/* Thread-local detail of the last failure on this thread ("" if none). */
+const char* adst_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ADST_H */
