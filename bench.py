@@ -1,0 +1,221 @@
+"""Benchmark: grid-point-steps/s of one forward+VJP call at a fixed memory
+budget on one MI355X, with the dominant kernel's achieved HBM bandwidth
+against the chip's peak and the CPU oracle timed on the host beside it.
+
+One "step" of the benchmark is one adst_vjp call: the forward sweep, the
+loss and seed, every recomputation the schedule needs and the reverse sweep,
+over one synthetic input already resident in HBM. Throughput is
+npoints * T / (wall time of one call).
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--sched S]
+                    [--force-tape] [--no-cpu-baseline]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "grid-point-steps/s for fwd+VJP at fixed memory budget; achieved HBM GB/s"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+SCHED_NAMES = {0: "auto", 1: "store_all", 2: "uniform", 3: "binomial"}
+LOSS_NAMES = {0: "half_sq", 1: "dot_w", 2: "half_sq_diff", 3: "seed"}
+KERNELS = {  # (forward, adjoint) kernel names as rocprofv3 reports them
+    0: ("fwd_jacobi2d5", "adj_jacobi2d5"),
+    1: ("fwd_allencahn3d7", "adj_allencahn3d7"),
+    2: ("fwd_vardiff2d9", "adj_vardiff2d9"),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--sched", default=None, choices=list(SCHED_NAMES.values()))
+    ap.add_argument("--budget-bytes", type=int, default=None)
+    ap.add_argument("--force-tape", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        with open(os.path.join(ROOT, "paper_2509_02197_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(workload, kernel, launches_per_call):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    or None when none exists for this kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    e = table.get(f"{workload}:{kernel}")
+    if not e or e.get("src_sha") != source_sha():
+        return None
+    return e["bytes_per_launch"]
+
+
+def cpu_baseline(w, inp, target_s):
+    """The oracle (single-threaded store-all tape, as it stands) on the same
+    grid for as many leading steps as fit about target_s seconds."""
+    import oracle
+    from paper_2509_02197_amd.workloads import dims_of  # noqa: F401
+    x0, K, aux = inp["x0"], inp["K"], inp["aux"]
+    n = x0.size
+    # warm the pages once, then probe two steps to size the sample
+    oracle.vjp(w.kind, x0, K=K, steps=1, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    t0 = time.perf_counter()
+    oracle.vjp(w.kind, x0, K=K, steps=2, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    one = (time.perf_counter() - t0) / 2
+    Ts = int(max(1, min(w.steps, target_s / max(one, 1e-6))))
+    t0 = time.perf_counter()
+    oracle.vjp(w.kind, x0, K=K, steps=Ts, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    dt = time.perf_counter() - t0
+    return {"value": n * Ts / dt, "unit": "grid-point-steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"full {'x'.join(map(str, x0.shape))} grid, first {Ts} of {w.steps} steps, "
+                      f"store-all tape, single thread, {dt:.1f} s",
+            "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              f"multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2509_02197_amd as adst
+    from paper_2509_02197_amd.workloads import HEADLINE, WORKLOADS, dims_of, make_inputs
+
+    name = args.workload or HEADLINE
+    w = WORKLOADS[name]
+    sched = w.sched
+    if args.sched:
+        sched = {v: k for k, v in SCHED_NAMES.items()}[args.sched]
+    budget = w.budget_bytes if args.budget_bytes is None else args.budget_bytes
+    flags = adst.ADST_FORCE_TAPE if args.force_tape else 0
+
+    print(f"# bench workload={name} sched={SCHED_NAMES[sched]} budget={budget} "
+          f"force_tape={args.force_tape}", file=sys.stderr, flush=True)
+    inp = make_inputs(w)
+    dev = torch.device("cuda:0")
+    x0 = torch.from_numpy(inp["x0"]).to(dev)
+    K = torch.from_numpy(inp["K"]).to(dev) if inp["K"] is not None else None
+    aux = torch.from_numpy(inp["aux"]).to(dev) if inp["aux"] is not None else None
+    prob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params, flags)
+    info = adst.adst_plan(prob, w.steps, budget, sched, w.want_dK)
+    ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=dev)
+    dx0 = torch.empty_like(x0)
+    dK = torch.empty_like(x0) if w.want_dK else None
+    L = torch.empty((), dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def call(p):
+        return adst.adst_vjp(p, x0, K, w.steps, w.loss, aux, budget, sched, dx0, dK, None, L, ws,
+                             ws.numel(), stream)
+
+    for _ in range(args.warmup):
+        call(prob)
+    torch.cuda.synchronize()
+
+    # ---- timed region: K calls, no tracing
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        call(prob)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = e0.elapsed_time(e1)
+    ms_per_step = 1e3 * wall / args.steps
+    pts = w.npoints * w.steps
+    value = pts / (wall / args.steps)
+
+    # ---- roofline leg: the same K calls with per-launch HIP events
+    tprob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params,
+                              flags | adst.ADST_TRACE)
+    acc = {"ms_fwd_sweep": 0.0, "ms_fwd_recompute": 0.0, "ms_adj": 0.0, "ms_seed": 0.0,
+           "ms_total": 0.0}
+    for _ in range(args.steps):
+        ti = call(tprob)
+        for k in acc:
+            acc[k] += getattr(ti, k) / args.steps
+    isz = 8 if w.dtype == adst.ADST_F64 else 4
+    fwd_B = {0: 2, 1: 2, 2: 3}[w.kind] * isz
+    adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3}[w.kind] * isz
+    n_fwd, n_adj = info.fwd_steps_total, info.adj_steps
+    ms_fwd = acc["ms_fwd_sweep"] + acc["ms_fwd_recompute"]
+    fwd_avg = ms_fwd / max(n_fwd, 1)
+    adj_avg = acc["ms_adj"] / max(n_adj, 1)
+    kname = KERNELS[w.kind]
+    if ms_fwd >= acc["ms_adj"]:
+        kernel, avg_ms, per_pt = kname[0], fwd_avg, fwd_B
+    else:
+        kernel, avg_ms, per_pt = kname[1], adj_avg, adj_B
+    alg_bytes = per_pt * w.npoints
+    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    traffic = traffic_for(name, kernel, 1)
+    roofline = {
+        "bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": traffic, "alg_bytes_per_launch": alg_bytes,
+        "avg_launch_ms": round(avg_ms, 5), "launches_per_step": n_fwd if kernel == kname[0] else n_adj,
+        "fwd_avg_ms": round(fwd_avg, 5), "fwd_gbps": round(fwd_B * w.npoints / fwd_avg / 1e6, 1),
+        "adj_avg_ms": round(adj_avg, 5), "adj_gbps": round(adj_B * w.npoints / adj_avg / 1e6, 1),
+    }
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "grid-point-steps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if w.dtype == adst.ADST_F64 else "f32", "data": "synthetic",
+        "config": {
+            "workload": name, "grid": list(w.shape), "T": w.steps, "kind": adst.workloads.KIND_NAMES[w.kind],
+            "loss": LOSS_NAMES[w.loss], "budget_bytes": budget,
+            "schedule": SCHED_NAMES[info.sched] + ("" if info.needs_state else " (tape elided)"),
+            "slots": info.slots, "fwd_steps": info.fwd_steps_total,
+            "recompute_steps": info.recompute_steps, "grads": "dx0,dK" if w.want_dK else "dx0",
+            "force_tape": bool(args.force_tape),
+        },
+        "hbm_gbps_effective": round(info.alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "event_ms_per_step": ev_ms / args.steps,
+        "phase_ms": {k: round(v, 4) for k, v in acc.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,219 @@
+"""adst: reverse-mode gradients of time-iterated stencils under a checkpoint
+memory budget, on AMD MI355X (gfx950).
+
+Thin ctypes binding of ``libadst.so`` (declared in ``include/adst.h``). The
+functions keep the C names and only marshal arguments: tensors become device
+pointers, the stream defaults to torch's current stream. Every step of the
+path runs in the library's HIP kernels; there is no Python or CPU fallback,
+and a missing library is an error.
+"""
+import ctypes
+import os
+
+from . import workloads  # noqa: F401  (seeded inputs; no method arithmetic)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libadst.so")
+
+# enums of adst.h
+ADST_OK, ADST_ERR_ARG, ADST_ERR_BUDGET, ADST_ERR_WORKSPACE, ADST_ERR_UNSUPPORTED, ADST_ERR_HIP = range(6)
+ADST_JACOBI2D5, ADST_ALLENCAHN3D7, ADST_VARDIFF2D9 = 0, 1, 2
+ADST_F64, ADST_F32 = 0, 1
+ADST_SCHED_AUTO, ADST_SCHED_STORE_ALL, ADST_SCHED_UNIFORM, ADST_SCHED_BINOMIAL = 0, 1, 2, 3
+ADST_LOSS_HALF_SQ, ADST_LOSS_DOT_W, ADST_LOSS_HALF_SQ_DIFF, ADST_LOSS_SEED = 0, 1, 2, 3
+ADST_FORCE_TAPE, ADST_TRACE = 0x1, 0x2
+ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ = 0, 1, 2
+ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
+
+EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_status_str",
+            "adst_last_error")
+
+
+class adst_problem(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n", ctypes.c_int64 * 3),
+                ("p", ctypes.c_double * 2), ("flags", ctypes.c_uint32)]
+
+
+class adst_action(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("t", ctypes.c_int32), ("src", ctypes.c_int32),
+                ("dst", ctypes.c_int32)]
+
+
+class adst_plan_info(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int32), ("sched", ctypes.c_int32), ("slots", ctypes.c_int32),
+                ("needs_state", ctypes.c_int32), ("fwd_steps_total", ctypes.c_int64),
+                ("recompute_steps", ctypes.c_int64), ("adj_steps", ctypes.c_int64),
+                ("n_actions", ctypes.c_int64), ("state_bytes", ctypes.c_uint64),
+                ("budget_bytes", ctypes.c_uint64), ("slot_bytes_peak", ctypes.c_uint64),
+                ("workspace_bytes", ctypes.c_uint64), ("fwd_workspace_bytes", ctypes.c_uint64),
+                ("alg_bytes", ctypes.c_uint64), ("ms_fwd_sweep", ctypes.c_float),
+                ("ms_fwd_recompute", ctypes.c_float), ("ms_adj", ctypes.c_float),
+                ("ms_seed", ctypes.c_float), ("ms_total", ctypes.c_float),
+                ("reserved", ctypes.c_float)]
+
+    def as_dict(self):
+        return {f[0]: getattr(self, f[0]) for f in self._fields_ if f[0] != "reserved"}
+
+
+class AdstError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        super().__init__(f"adst status {status}: {detail}")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library. Built in-tree on first use if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        from . import build as _build
+        _build.build()
+    L = ctypes.CDLL(LIB_PATH)
+    vp, u64, i32, i64 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int64
+    P = ctypes.POINTER
+    L.adst_plan.argtypes = [P(adst_problem), i32, u64, i32, i32, P(adst_plan_info)]
+    L.adst_plan_actions.argtypes = [P(adst_problem), i32, u64, i32, i32, P(adst_action), i64,
+                                    P(i64)]
+    L.adst_forward.argtypes = [P(adst_problem), vp, vp, i32, vp, vp, u64, vp]
+    L.adst_vjp.argtypes = [P(adst_problem), vp, vp, i32, i32, vp, u64, i32, vp, vp, vp, vp, vp, u64,
+                           vp, P(adst_plan_info)]
+    for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp"):
+        getattr(L, f).restype = ctypes.c_int
+    L.adst_status_str.argtypes = [ctypes.c_int]
+    L.adst_status_str.restype = ctypes.c_char_p
+    L.adst_last_error.argtypes = []
+    L.adst_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def adst_status_str(status):
+    return lib().adst_status_str(status).decode()
+
+
+def adst_last_error():
+    return lib().adst_last_error().decode()
+
+
+def _check(status):
+    if status != ADST_OK:
+        raise AdstError(status, f"{adst_status_str(status)}: {adst_last_error()}")
+
+
+def make_problem(kind, dtype, dims, params=None, flags=0):
+    """dims = (nx, ny, nz) with nx fastest."""
+    from .workloads import DEFAULT_PARAMS
+    p = adst_problem()
+    p.kind, p.dtype = kind, dtype
+    for i in range(3):
+        p.n[i] = int(dims[i])
+    pp = params if params is not None else DEFAULT_PARAMS[kind]
+    p.p[0], p.p[1] = float(pp[0]), float(pp[1])
+    p.flags = flags
+    return p
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if hasattr(stream, "cuda_stream"):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def adst_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
+    info = adst_plan_info()
+    _check(lib().adst_plan(ctypes.byref(prob), steps, mem_budget_bytes, sched, int(want_dcoeff),
+                           ctypes.byref(info)))
+    return info
+
+
+def adst_plan_actions(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
+    """The plan's action list as a list of (op, t, src, dst) tuples."""
+    n = ctypes.c_int64(0)
+    L = lib()
+    _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
+                               int(want_dcoeff), None, 0, ctypes.byref(n)))
+    buf = (adst_action * max(n.value, 1))()
+    _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
+                               int(want_dcoeff), buf, n.value, ctypes.byref(n)))
+    return [(a.op, a.t, a.src, a.dst) for a in buf[:n.value]]
+
+
+def adst_forward(prob, x0, coeff, steps, xT, ws, ws_bytes, stream=None):
+    _check(lib().adst_forward(ctypes.byref(prob), _ptr(x0), _ptr(coeff), steps, _ptr(xT),
+                              _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def adst_vjp(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0, dcoeff, xT,
+             loss_dev, ws, ws_bytes, stream=None, want_info=True):
+    info = adst_plan_info() if want_info else None
+    _check(lib().adst_vjp(ctypes.byref(prob), _ptr(x0), _ptr(coeff), steps, loss, _ptr(loss_aux),
+                          mem_budget_bytes, sched, _ptr(dx0), _ptr(dcoeff), _ptr(xT),
+                          _ptr(loss_dev), _ptr(ws), ws_bytes, _stream(stream),
+                          ctypes.byref(info) if info is not None else None))
+    return info
+
+
+# ------------------------------------------------------------ conveniences
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float64:
+        return ADST_F64
+    if t.dtype == torch.float32:
+        return ADST_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dims(shape):
+    if len(shape) == 2:
+        return (shape[1], shape[0], 1)
+    if len(shape) == 3:
+        return (shape[2], shape[1], shape[0])
+    raise ValueError(f"expected a 2-D or 3-D array, got {tuple(shape)}")
+
+
+def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
+    """x_T on the device of x0 (torch tensors, row-major)."""
+    import torch
+    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params)
+    xT = torch.empty_like(x0)
+    info = adst_plan(prob, steps, 0, ADST_SCHED_AUTO)
+    ws = torch.empty(max(info.fwd_workspace_bytes, 1), dtype=torch.uint8, device=x0.device)
+    adst_forward(prob, x0, coeff, steps, xT, ws, info.fwd_workspace_bytes, stream)
+    return xT
+
+
+def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_bytes=None,
+        sched=ADST_SCHED_AUTO, want_dcoeff=False, params=None, flags=0, stream=None, ws=None):
+    """Allocate outputs and workspace with torch and run adst_vjp.
+
+    budget_bytes=None means unlimited (store-all). Returns a dict with dx0,
+    dK (or None), xT, loss (0-d device tensor), info and the workspace."""
+    import torch
+    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags)
+    if budget_bytes is None:
+        budget_bytes = (1 << 63)
+    info = adst_plan(prob, steps, budget_bytes, sched, want_dcoeff)
+    if ws is None or ws.numel() < info.workspace_bytes:
+        ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=x0.device)
+    dx0 = torch.empty_like(x0)
+    dK = torch.empty_like(x0) if want_dcoeff else None
+    xT = torch.empty_like(x0)
+    L = torch.empty((), dtype=torch.float64, device=x0.device)
+    info = adst_vjp(prob, x0, coeff, steps, loss, aux, budget_bytes, sched, dx0, dK, xT, L, ws,
+                    ws.numel(), stream)
+    return {"dx0": dx0, "dK": dK, "xT": xT, "loss": L, "info": info, "ws": ws}

@@ -1,0 +1,416 @@
+// C-ABI of adst: argument validation, workspace layout, and the executor that
+// interprets a plan's action list by enqueueing kernels on the caller's
+// stream. All arguments are checked before the first HIP call, so every
+// argument error is reported without touching the GPU.
+
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+#include <vector>
+
+#include "adst.h"
+#include "kernels.h"
+#include "planner.h"
+
+namespace adst {
+namespace {
+
+thread_local std::string g_last_error;
+
+adst_status fail(adst_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+constexpr uint64_t kAlign = 4096;
+constexpr uint64_t kHeaderBytes = 16384;  // loss partials (8 KiB) + loss scalar
+constexpr uint64_t kLossOffset = 8192;
+
+uint64_t align_up(uint64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int itemsize(int32_t dtype) { return dtype == ADST_F64 ? 8 : 4; }
+
+struct Checked {
+  StepShape shape;
+  int64_t npoints = 0;
+  uint64_t state_bytes = 0;
+  bool needs_state = false;
+  bool trace = false;
+};
+
+adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* out) {
+  if (!p) return fail(ADST_ERR_ARG, "problem is NULL");
+  if (p->kind < ADST_JACOBI2D5 || p->kind > ADST_VARDIFF2D9)
+    return fail(ADST_ERR_ARG, "unknown kind " + std::to_string(p->kind));
+  if (p->dtype != ADST_F64 && p->dtype != ADST_F32)
+    return fail(ADST_ERR_ARG, "unknown dtype " + std::to_string(p->dtype));
+  if (p->flags & ~(ADST_FORCE_TAPE | ADST_TRACE))
+    return fail(ADST_ERR_ARG, "unknown flag bits");
+  for (int d = 0; d < 3; ++d)
+    if (p->n[d] < 1) return fail(ADST_ERR_ARG, "every extent n[i] must be >= 1");
+  if (p->n[0] > INT32_MAX || p->n[1] > INT32_MAX || p->n[2] > INT32_MAX)
+    return fail(ADST_ERR_ARG, "extent too large");
+  const int64_t n = p->n[0] * p->n[1] * p->n[2];
+  if (n >= (int64_t(1) << 31)) return fail(ADST_ERR_ARG, "grid must have fewer than 2^31 points");
+  if ((p->kind == ADST_JACOBI2D5 || p->kind == ADST_VARDIFF2D9) && p->n[2] != 1)
+    return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
+  // A dispatch covers whole 64x4 tiles of every plane; its work-item count
+  // must fit the 32-bit dispatch grid.
+  const int64_t tiles = ((p->n[0] + 63) / 64) * ((p->n[1] + 3) / 4) * p->n[2];
+  if (tiles * 256 >= (int64_t(1) << 32))
+    return fail(ADST_ERR_UNSUPPORTED, "grid too thin in x/y for the tile shape");
+  if (want_dcoeff && p->kind != ADST_VARDIFF2D9)
+    return fail(ADST_ERR_UNSUPPORTED, "only the variable-coefficient kind has a coefficient field");
+  out->shape = {p->kind, p->dtype, (int32_t)p->n[0], (int32_t)p->n[1], (int32_t)p->n[2],
+                p->p[0], p->p[1]};
+  out->npoints = n;
+  out->state_bytes = uint64_t(n) * itemsize(p->dtype);
+  const bool kind_reads_state = p->kind == ADST_ALLENCAHN3D7 ||
+                                (p->kind == ADST_VARDIFF2D9 && want_dcoeff);
+  out->needs_state = kind_reads_state || (p->flags & ADST_FORCE_TAPE);
+  out->trace = (p->flags & ADST_TRACE) != 0;
+  return ADST_OK;
+}
+
+struct Layout {
+  uint64_t state_stride = 0;  // aligned bytes per state buffer
+  uint64_t w0 = 0, w1 = 0, g = 0, slot0 = 0, total = 0;
+};
+
+Layout layout_for(const Checked& c, const Plan& plan) {
+  Layout L;
+  L.state_stride = align_up(c.state_bytes);
+  if (plan.steps == 0) {
+    L.total = kHeaderBytes;
+    return L;
+  }
+  L.w0 = kHeaderBytes;
+  L.w1 = L.w0 + L.state_stride;
+  L.g = L.w1 + L.state_stride;
+  L.slot0 = L.g + L.state_stride;
+  L.total = L.slot0 + uint64_t(plan.slots) * L.state_stride;
+  return L;
+}
+
+// Algorithmic HBM bytes per point of one forward / adjoint step and of the
+// seed: what the step must read and write at least once.
+void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd, uint64_t* adj,
+                     uint64_t* adj_first, uint64_t* seed) {
+  const uint64_t s = itemsize(c.shape.dtype);
+  switch (c.shape.kind) {
+    case ADST_JACOBI2D5:
+      *fwd = 2 * s;
+      *adj = *adj_first = 2 * s;
+      break;
+    case ADST_ALLENCAHN3D7:
+      *fwd = 2 * s;
+      *adj = *adj_first = 3 * s;  // g, x, g'
+      break;
+    default:                      // VARDIFF2D9
+      *fwd = 3 * s;               // x, K, x'
+      *adj = want_dk ? 6 * s : 3 * s;  // g, x, K, dK read+write, g'  |  g, K, g'
+      *adj_first = want_dk ? 5 * s : 3 * s;
+      break;
+  }
+  *seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
+}
+
+void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,
+               adst_plan_info* info) {
+  const Layout L = layout_for(c, plan);
+  uint64_t fb, ab, ab1, sb;
+  per_point_bytes(c, want_dk, loss, &fb, &ab, &ab1, &sb);
+  *info = adst_plan_info{};
+  info->steps = plan.steps;
+  info->sched = plan.sched;
+  info->slots = plan.slots;
+  info->needs_state = plan.needs_state ? 1 : 0;
+  info->fwd_steps_total = plan.fwd_total;
+  info->recompute_steps = plan.fwd_total - plan.steps;
+  info->adj_steps = plan.adj_total;
+  info->n_actions = (int64_t)plan.acts.size();
+  info->state_bytes = c.state_bytes;
+  info->budget_bytes = budget;
+  info->slot_bytes_peak = uint64_t(plan.slots) * c.state_bytes;
+  info->workspace_bytes = L.total;
+  info->fwd_workspace_bytes = plan.steps >= 2 ? c.state_bytes : 0;
+  const uint64_t n = uint64_t(c.npoints);
+  uint64_t adj_total = plan.adj_total > 0 ? ab1 + uint64_t(plan.adj_total - 1) * ab : 0;
+  info->alg_bytes = n * (uint64_t(plan.fwd_total) * fb + adj_total + sb);
+}
+
+adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
+                      int32_t want_dcoeff, Checked* c, Plan* plan) {
+  adst_status st = check_problem(prob, want_dcoeff, c);
+  if (st != ADST_OK) return st;
+  if (steps < 0) return fail(ADST_ERR_ARG, "steps must be >= 0");
+  const int64_t slots_avail = (int64_t)std::min<uint64_t>(budget / c->state_bytes, INT32_MAX);
+  std::string err;
+  st = build_plan(steps, slots_avail, sched, c->needs_state, plan, &err);
+  if (st != ADST_OK) return fail(st, err);
+  return ADST_OK;
+}
+
+struct Range {
+  const char* name;
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+bool overlaps(const Range& a, const Range& b) {
+  return a.lo < b.hi && b.lo < a.hi && a.lo != a.hi && b.lo != b.hi;
+}
+
+Range range_of(const char* name, const void* p, uint64_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return {name, lo, p ? lo + bytes : lo};
+}
+
+// Every output range must be disjoint from every other output and from the
+// inputs (inputs may overlap each other: they are only read).
+adst_status check_disjoint(const std::vector<Range>& outs, const std::vector<Range>& ins) {
+  for (size_t a = 0; a < outs.size(); ++a) {
+    for (size_t b = a + 1; b < outs.size(); ++b)
+      if (overlaps(outs[a], outs[b]))
+        return fail(ADST_ERR_ARG, std::string(outs[a].name) + " overlaps " + outs[b].name);
+    for (const Range& r : ins)
+      if (overlaps(outs[a], r))
+        return fail(ADST_ERR_ARG, std::string(outs[a].name) + " overlaps input " + r.name);
+  }
+  return ADST_OK;
+}
+
+// Per-launch HIP event timing for ADST_TRACE.
+class Tracer {
+ public:
+  explicit Tracer(bool on) : on_(on) {}
+  ~Tracer() {
+    for (auto& e : events_) hipEventDestroy(e);
+  }
+  enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, NCAT };
+  hipError_t begin(hipStream_t s) {
+    if (!on_) return hipSuccess;
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    events_.push_back(e);
+    return hipEventRecord(e, s);
+  }
+  hipError_t end(hipStream_t s, Cat cat) {
+    if (!on_) return hipSuccess;
+    hipEvent_t e;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return r;
+    events_.push_back(e);
+    cats_.push_back(cat);
+    return hipEventRecord(e, s);
+  }
+  hipError_t finish(adst_plan_info* info) {
+    if (!on_ || events_.empty()) return hipSuccess;
+    hipError_t r = hipEventSynchronize(events_.back());
+    if (r != hipSuccess) return r;
+    float ms[NCAT] = {0, 0, 0, 0};
+    for (size_t k = 0; k < cats_.size(); ++k) {
+      float dt = 0.f;
+      r = hipEventElapsedTime(&dt, events_[2 * k], events_[2 * k + 1]);
+      if (r != hipSuccess) return r;
+      ms[cats_[k]] += dt;
+    }
+    float total = 0.f;
+    r = hipEventElapsedTime(&total, events_.front(), events_.back());
+    if (r != hipSuccess) return r;
+    if (info) {
+      info->ms_fwd_sweep = ms[SWEEP];
+      info->ms_fwd_recompute = ms[RECOMPUTE];
+      info->ms_adj = ms[ADJ];
+      info->ms_seed = ms[SEED];
+      info->ms_total = total;
+    }
+    return hipSuccess;
+  }
+
+ private:
+  bool on_;
+  std::vector<hipEvent_t> events_;
+  std::vector<Cat> cats_;
+};
+
+adst_status hip_fail(hipError_t e, const char* what) {
+  return fail(ADST_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+}  // namespace adst
+
+using namespace adst;
+
+extern "C" {
+
+adst_status adst_plan(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
+                      int32_t sched, int32_t want_dcoeff, adst_plan_info* out) {
+  if (!out) return fail(ADST_ERR_ARG, "out is NULL");
+  Checked c;
+  Plan plan;
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff, &c, &plan);
+  if (st != ADST_OK) return st;
+  fill_info(c, plan, mem_budget_bytes, want_dcoeff != 0, ADST_LOSS_HALF_SQ, out);
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
+                              int32_t sched, int32_t want_dcoeff, adst_action* out, int64_t cap,
+                              int64_t* n_out) {
+  if (!n_out) return fail(ADST_ERR_ARG, "n_out is NULL");
+  if (cap < 0 || (cap > 0 && !out)) return fail(ADST_ERR_ARG, "bad output capacity");
+  Checked c;
+  Plan plan;
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff, &c, &plan);
+  if (st != ADST_OK) return st;
+  const int64_t n = (int64_t)plan.acts.size();
+  std::copy(plan.acts.begin(), plan.acts.begin() + std::min(n, cap), out);
+  *n_out = n;
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_forward(const adst_problem* prob, const void* x0, const void* coeff,
+                         int32_t steps, void* xT, void* ws, uint64_t ws_bytes,
+                         hipStream_t stream) {
+  Checked c;
+  adst_status st = check_problem(prob, 0, &c);
+  if (st != ADST_OK) return st;
+  if (steps < 0) return fail(ADST_ERR_ARG, "steps must be >= 0");
+  if (!x0 || !xT) return fail(ADST_ERR_ARG, "x0 and xT are required");
+  if (prob->kind == ADST_VARDIFF2D9 && !coeff)
+    return fail(ADST_ERR_ARG, "the variable-coefficient kind needs coeff (K)");
+  const uint64_t S = c.state_bytes;
+  const uint64_t need = steps >= 2 ? S : 0;
+  if (ws_bytes < need || (need && !ws))
+    return fail(ADST_ERR_WORKSPACE, "adst_forward needs " + std::to_string(need) + " workspace bytes");
+  std::vector<Range> outs = {range_of("xT", xT, S)};
+  if (need) outs.push_back(range_of("ws", ws, need));
+  std::vector<Range> ins = {range_of("x0", x0, S)};
+  if (prob->kind == ADST_VARDIFF2D9) ins.push_back(range_of("coeff", coeff, S));
+  st = check_disjoint(outs, ins);
+  if (st != ADST_OK) return st;
+
+  hipError_t e;
+  if (steps == 0) {
+    e = launch_copy(xT, x0, (int64_t)S, stream);
+    if (e != hipSuccess) return hip_fail(e, "copy");
+    g_last_error.clear();
+    return ADST_OK;
+  }
+  // x_t lands in xT when (T - t) is even, so x_T ends in xT.
+  const void* cur = x0;
+  for (int32_t t = 1; t <= steps; ++t) {
+    void* dst = ((steps - t) % 2 == 0) ? xT : ws;
+    e = launch_forward(c.shape, cur, coeff, dst, stream);
+    if (e != hipSuccess) return hip_fail(e, "forward step");
+    cur = dst;
+  }
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
+                     int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
+                     void* dx0, void* dcoeff, void* xT, double* loss_dev, void* ws,
+                     uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
+  const int32_t want_dk = dcoeff != nullptr;
+  Checked c;
+  Plan plan;
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dk, &c, &plan);
+  if (st != ADST_OK) return st;
+  if (!x0 || !dx0) return fail(ADST_ERR_ARG, "x0 and dx0 are required");
+  if (prob->kind == ADST_VARDIFF2D9 && !coeff)
+    return fail(ADST_ERR_ARG, "the variable-coefficient kind needs coeff (K)");
+  if (loss < ADST_LOSS_HALF_SQ || loss > ADST_LOSS_SEED)
+    return fail(ADST_ERR_ARG, "unknown loss " + std::to_string(loss));
+  if (loss != ADST_LOSS_HALF_SQ && !loss_aux)
+    return fail(ADST_ERR_ARG, "this loss needs loss_aux");
+  const Layout L = layout_for(c, plan);
+  if (ws_bytes < L.total || !ws)
+    return fail(ADST_ERR_WORKSPACE, "adst_vjp needs " + std::to_string(L.total) +
+                                        " workspace bytes, got " + std::to_string(ws_bytes));
+  const uint64_t S = c.state_bytes;
+  std::vector<Range> outs = {range_of("dx0", dx0, S), range_of("ws", ws, L.total)};
+  if (dcoeff) outs.push_back(range_of("dcoeff", dcoeff, S));
+  if (xT) outs.push_back(range_of("xT", xT, S));
+  if (loss_dev) outs.push_back(range_of("loss_dev", loss_dev, sizeof(double)));
+  std::vector<Range> ins = {range_of("x0", x0, S)};
+  if (prob->kind == ADST_VARDIFF2D9) ins.push_back(range_of("coeff", coeff, S));
+  if (loss != ADST_LOSS_HALF_SQ) ins.push_back(range_of("loss_aux", loss_aux, S));
+  st = check_disjoint(outs, ins);
+  if (st != ADST_OK) return st;
+  if (info) fill_info(c, plan, mem_budget_bytes, want_dk != 0, loss, info);
+
+  // ---- interpret the plan
+  char* wsb = static_cast<char*>(ws);
+  double* partials = reinterpret_cast<double*>(wsb);
+  double* loss_out = loss_dev ? loss_dev : reinterpret_cast<double*>(wsb + kLossOffset);
+  void* gbuf_odd = wsb + L.g;
+  auto gbuf = [&](int32_t t) -> void* { return (t % 2 == 0) ? dx0 : gbuf_odd; };
+  auto buffer = [&](int32_t id) -> void* {
+    switch (id) {
+      case ADST_BUF_X0: return const_cast<void*>(x0);
+      case ADST_BUF_W0: return wsb + L.w0;
+      case ADST_BUF_W1: return wsb + L.w1;
+      case ADST_BUF_XT: return xT ? xT : gbuf(steps);
+      default: return wsb + L.slot0 + uint64_t(id - ADST_BUF_SLOT0) * L.state_stride;
+    }
+  };
+
+  Tracer tr(c.trace);
+  bool seeded = false;
+  hipError_t e = hipSuccess;
+  for (const adst_action& a : plan.acts) {
+    if ((e = tr.begin(stream)) != hipSuccess) return hip_fail(e, "trace event");
+    Tracer::Cat cat;
+    if (a.op == ADST_OP_FWD) {
+      e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+      cat = seeded ? Tracer::RECOMPUTE : Tracer::SWEEP;
+    } else if (a.op == ADST_OP_SEED) {
+      const void* xsrc = buffer(a.src);
+      void* xcopy = (steps == 0 && xT) ? xT : nullptr;
+      e = launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, gbuf(steps), xcopy,
+                      partials, stream);
+      if (e == hipSuccess)
+        e = launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
+      if (e == hipSuccess && steps == 0 && dcoeff)
+        e = launch_fill_zero(dcoeff, (int64_t)S, stream);
+      seeded = true;
+      cat = Tracer::SEED;
+    } else {
+      const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
+      e = launch_adjoint(c.shape, xs, coeff, gbuf(a.t), gbuf(a.t - 1), dcoeff, a.t == steps,
+                         stream);
+      cat = Tracer::ADJ;
+    }
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    if ((e = tr.end(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
+  }
+  if ((e = tr.finish(info)) != hipSuccess) return hip_fail(e, "trace");
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+const char* adst_status_str(adst_status s) {
+  switch (s) {
+    case ADST_OK: return "ok";
+    case ADST_ERR_ARG: return "invalid argument";
+    case ADST_ERR_BUDGET: return "memory budget too small for the requested schedule";
+    case ADST_ERR_WORKSPACE: return "workspace too small";
+    case ADST_ERR_UNSUPPORTED: return "unsupported problem";
+    case ADST_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* adst_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

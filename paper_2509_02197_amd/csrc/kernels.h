@@ -1,0 +1,45 @@
+// Launchers of the gfx950 kernels. Plain host signatures: device pointers,
+// sizes, the caller's stream. Every launcher only enqueues and returns the
+// launch status (hipGetLastError after the launch).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace adst {
+
+struct StepShape {
+  int32_t kind;   // adst_kind
+  int32_t dtype;  // adst_dtype
+  int32_t nx, ny, nz;
+  double p0, p1;
+};
+
+// x_t = F(x_{t-1}; K): x -> y. K only for the variable-coefficient kind.
+hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void* y,
+                          hipStream_t stream);
+
+// g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
+// reads no state and dK is not asked for). dK (nullable) is accumulated:
+// dK = (dk_first ? 0 : dK) + contribution of step t.
+hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
+                          void* g_prev, void* dK, bool dk_first, hipStream_t stream);
+
+// Number of per-block loss partials launch_seed writes for n points.
+int32_t seed_partials(int64_t n);
+constexpr int32_t kMaxSeedPartials = 1024;
+
+// Loss partials and seed g from x_T (x and g may be the same buffer: the
+// kernel reads each point before writing it). xcopy (nullable) receives x.
+hipError_t launch_seed(int32_t dtype, int32_t loss, int64_t n, const void* x, const void* aux,
+                       void* g, void* xcopy, double* partials, hipStream_t stream);
+
+// Sum the partials in a fixed order into *loss (one block).
+hipError_t launch_finalize(const double* partials, int32_t nparts, double* loss,
+                           hipStream_t stream);
+
+hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t stream);
+hipError_t launch_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream);
+
+}  // namespace adst

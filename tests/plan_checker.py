@@ -1,0 +1,58 @@
+"""Replays a plan's action list on integer "states" (test helper).
+
+Each buffer holds the index t of the state x_t it contains. The replay
+checks what makes a plan correct, independently of how it was built:
+  * a forward step t reads a buffer holding x_{t-1} and writes a buffer
+    other than the caller's x0 and its own source;
+  * the seed comes exactly once, after x_T was written, before any adjoint;
+  * adjoint steps run T, T-1, ..., 1, each reading a buffer that holds
+    x_{t-1} at that moment when the step's adjoint needs state;
+  * the x_T buffer is not read again after the seed (it may alias g_T);
+  * checkpoint slots used stay within the allowed count.
+Returns the forward-step count and the set of slots touched.
+"""
+X0, W0, W1, XT, SLOT0 = 0, 1, 2, 3, 4
+FWD, SEED, ADJ = 0, 1, 2
+NONE = -1
+
+
+def replay(actions, T, needs_state, max_slots):
+    holds = {X0: 0}
+    seeded = False
+    next_adj = T
+    nfwd = 0
+    slots = set()
+    for k, (op, t, src, dst) in enumerate(actions):
+        if op == FWD:
+            assert not (seeded and src == XT), f"action {k}: reads x_T buffer after the seed"
+            assert holds.get(src) == t - 1, f"action {k}: FWD {t} reads buffer {src} holding {holds.get(src)}"
+            assert dst not in (X0, src, NONE), f"action {k}: bad destination {dst}"
+            assert 1 <= t <= T
+            if dst == XT:
+                assert t == T, f"action {k}: only x_T goes to the x_T buffer"
+            if dst >= SLOT0:
+                slots.add(dst)
+            holds[dst] = t
+            nfwd += 1
+        elif op == SEED:
+            assert not seeded, "seeded twice"
+            assert holds.get(src) == T, f"seed reads buffer {src} holding {holds.get(src)}"
+            seeded = True
+            if T > 0:
+                assert src == XT
+                holds[XT] = None  # now holds g_T
+        elif op == ADJ:
+            assert seeded, "adjoint before seed"
+            assert t == next_adj, f"adjoint {t} out of order (expected {next_adj})"
+            if needs_state:
+                assert holds.get(src) == t - 1, f"ADJ {t} reads buffer {src} holding {holds.get(src)}"
+            else:
+                assert src == NONE
+            next_adj -= 1
+        else:
+            raise AssertionError(f"unknown op {op}")
+    assert seeded
+    assert next_adj == 0, f"adjoints missing below {next_adj + 1}"
+    assert len(slots) <= max_slots, f"{len(slots)} slots used, {max_slots} allowed"
+    assert all(SLOT0 <= s < SLOT0 + max(max_slots, 0) for s in slots)
+    return nfwd, slots

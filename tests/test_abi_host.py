@@ -1,0 +1,158 @@
+"""The C-ABI library on a host without a GPU: it loads, exports every
+function include/adst.h declares, and rejects every bad argument before
+enqueueing anything (so these calls never reach the GPU; the pointers below
+are never dereferenced).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2509_02197_amd as adst
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+# The fake pointers below must never reach a kernel: run only where no GPU
+# is visible, so that a validation gap can only ever fail on the host.
+pytestmark = pytest.mark.skipif(_gpu_visible(), reason="host-only argument checks")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "adst.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(adst_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(adst.EXPORTED)
+
+
+def test_library_exports_every_declared_function():
+    lib = ctypes.CDLL(adst.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for s in range(6):
+        assert adst.adst_status_str(s)
+    assert adst.adst_status_str(99) == "unknown status"
+
+
+def test_struct_layouts_match_header():
+    # int32 x2, int64 x3, double x2, uint32 (+pad) = 56 bytes
+    assert ctypes.sizeof(adst.adst_problem) == 56
+    assert ctypes.sizeof(adst.adst_action) == 16
+    assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 4 * 8 + 6 * 8 + 6 * 4
+
+
+def _p(kind=adst.ADST_ALLENCAHN3D7, dims=(8, 8, 8), dtype=adst.ADST_F64, flags=0):
+    return adst.make_problem(kind, dtype, dims, flags=flags)
+
+
+def _status(fn, *a):
+    try:
+        fn(*a)
+    except adst.AdstError as e:
+        return e.status
+    return adst.ADST_OK
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda p: setattr(p, "kind", 7), adst.ADST_ERR_ARG),
+    (lambda p: setattr(p, "dtype", 3), adst.ADST_ERR_ARG),
+    (lambda p: p.n.__setitem__(1, 0), adst.ADST_ERR_ARG),
+    (lambda p: setattr(p, "flags", 0x80), adst.ADST_ERR_ARG),
+    (lambda p: [p.n.__setitem__(i, 2000) for i in range(3)], adst.ADST_ERR_ARG),
+])
+def test_plan_rejects_bad_problems(mutate, status):
+    p = _p()
+    mutate(p)
+    assert _status(adst.adst_plan, p, 10, 0, 0) == status
+    assert adst.adst_last_error()
+
+
+def test_plan_rejects_bad_scalars():
+    assert _status(adst.adst_plan, _p(), -1, 0, 0) == adst.ADST_ERR_ARG
+    assert _status(adst.adst_plan, _p(), 10, 0, 9) == adst.ADST_ERR_ARG
+    info = adst.adst_plan_info()
+    assert adst.lib().adst_plan(None, 3, 0, 0, 0, ctypes.byref(info)) == adst.ADST_ERR_ARG
+    assert adst.lib().adst_plan(ctypes.byref(_p()), 3, 0, 0, 0, None) == adst.ADST_ERR_ARG
+
+
+def test_plan_rejects_unsupported_combinations():
+    # 2-D kinds with nz > 1
+    assert _status(adst.adst_plan, _p(adst.ADST_JACOBI2D5, (8, 8, 2)), 5, 0, 0) == \
+        adst.ADST_ERR_UNSUPPORTED
+    assert _status(adst.adst_plan, _p(adst.ADST_VARDIFF2D9, (8, 8, 3)), 5, 0, 0) == \
+        adst.ADST_ERR_UNSUPPORTED
+    # a coefficient gradient for a kind without a coefficient field
+    assert _status(adst.adst_plan, _p(), 5, 0, 0, True) == adst.ADST_ERR_UNSUPPORTED
+
+
+# Fake, never-dereferenced device addresses: far apart unless a test wants overlap.
+X0, K, AUX, DX0, DK, XT, LOSS, WS = (0x10000000 * (i + 1) for i in range(8))
+BIG = 1 << 40
+
+
+def _vjp(p, **kw):
+    a = dict(x0=X0, coeff=None, steps=5, loss=adst.ADST_LOSS_HALF_SQ, loss_aux=None,
+             budget=BIG, sched=0, dx0=DX0, dcoeff=None, xT=None, loss_dev=None, ws=WS,
+             ws_bytes=BIG)
+    a.update(kw)
+    return _status(adst.adst_vjp, p, a["x0"], a["coeff"], a["steps"], a["loss"], a["loss_aux"],
+                   a["budget"], a["sched"], a["dx0"], a["dcoeff"], a["xT"], a["loss_dev"], a["ws"],
+                   a["ws_bytes"], 0)
+
+
+def test_vjp_argument_errors():
+    p = _p()
+    E = adst.ADST_ERR_ARG
+    assert _vjp(p, dx0=None) == E
+    assert _vjp(p, x0=None) == E
+    assert _vjp(p, steps=-2) == E
+    assert _vjp(p, loss=7) == E
+    assert _vjp(p, loss=adst.ADST_LOSS_DOT_W) == E             # needs loss_aux
+    assert _vjp(p, loss=adst.ADST_LOSS_HALF_SQ_DIFF) == E      # needs loss_aux
+    assert _vjp(p, dx0=X0 + 8) == E                            # dx0 overlaps x0
+    assert _vjp(p, xT=DX0 + 8) == E                            # xT overlaps dx0
+    assert _vjp(p, loss_dev=WS + 64) == E                      # loss overlaps ws
+    assert _vjp(p, loss=adst.ADST_LOSS_SEED, loss_aux=DX0) == E  # output overlaps input
+    pv = _p(adst.ADST_VARDIFF2D9, (8, 8, 1))
+    assert _vjp(pv) == E                                       # K missing
+    assert _vjp(pv, coeff=K, dcoeff=K) == E                    # dK overlaps K
+
+
+def test_vjp_budget_and_workspace_errors():
+    p = _p()
+    assert _vjp(p, budget=0, sched=adst.ADST_SCHED_STORE_ALL) == adst.ADST_ERR_BUDGET
+    need = adst.adst_plan(p, 5, BIG, 0).workspace_bytes
+    assert _vjp(p, ws_bytes=need - 1) == adst.ADST_ERR_WORKSPACE
+    assert _vjp(p, ws=None) == adst.ADST_ERR_WORKSPACE
+    assert _vjp(_p(adst.ADST_JACOBI2D5, (8, 8, 1)), dcoeff=DK) == adst.ADST_ERR_UNSUPPORTED
+
+
+def test_forward_argument_errors():
+    p = _p()
+
+    def fwd(**kw):
+        a = dict(x0=X0, coeff=None, steps=4, xT=XT, ws=WS, ws_bytes=BIG)
+        a.update(kw)
+        return _status(adst.adst_forward, p if "p" not in kw else kw["p"], a["x0"], a["coeff"],
+                       a["steps"], a["xT"], a["ws"], a["ws_bytes"], 0)
+
+    assert fwd(xT=None) == adst.ADST_ERR_ARG
+    assert fwd(steps=-1) == adst.ADST_ERR_ARG
+    assert fwd(xT=X0) == adst.ADST_ERR_ARG
+    assert fwd(ws_bytes=10) == adst.ADST_ERR_WORKSPACE
+    assert fwd(ws=XT + 16) == adst.ADST_ERR_ARG

@@ -1,0 +1,152 @@
+"""Checkpoint planner of the product library, through the C-ABI (CPU only).
+
+adst_plan / adst_plan_actions never touch the GPU. Every action list is
+replayed by tests/plan_checker.py, and its forward-step count is compared
+with the oracle's schedule definitions (oracle/checkpoint.py).
+"""
+import pytest
+
+import paper_2509_02197_amd as adst
+from oracle import checkpoint as cp
+from tests.plan_checker import replay
+
+AC = adst.ADST_ALLENCAHN3D7
+F64 = adst.ADST_F64
+
+
+def prob(kind=AC, dims=(4, 3, 2), dtype=F64, flags=0):
+    return adst.make_problem(kind, dtype, dims, flags=flags)
+
+
+def budget_for(slots, p=None):
+    p = p or prob()
+    S = p.n[0] * p.n[1] * p.n[2] * (8 if p.dtype == F64 else 4)
+    return slots * S
+
+
+@pytest.mark.parametrize("sched", [adst.ADST_SCHED_BINOMIAL, adst.ADST_SCHED_UNIFORM])
+def test_schedules_replay_and_match_definitions(sched):
+    p = prob()
+    for T in range(0, 41):
+        for slots in list(range(0, 9)) + [T, T + 5]:
+            acts = adst.adst_plan_actions(p, T, budget_for(slots), sched)
+            info = adst.adst_plan(p, T, budget_for(slots), sched)
+            c = min(slots, cp.store_all_slots(T)) + 1
+            nfwd, used = replay(acts, T, True, min(slots, cp.store_all_slots(T)))
+            if sched == adst.ADST_SCHED_BINOMIAL:
+                expect = cp.forward_steps_binomial(T, c)
+            else:
+                expect = cp.forward_steps_uniform(T, c)
+            assert nfwd == expect, (T, slots, nfwd, expect)
+            assert info.fwd_steps_total == nfwd
+            assert info.recompute_steps == nfwd - T
+            assert info.slots == len(used)
+            assert info.n_actions == len(acts)
+
+
+@pytest.mark.parametrize("T,slots", [(100, 10), (50, 8), (200, 16), (200, 7), (300, 3), (500, 40)])
+def test_binomial_large(T, slots):
+    p = prob()
+    acts = adst.adst_plan_actions(p, T, budget_for(slots), adst.ADST_SCHED_BINOMIAL)
+    nfwd, used = replay(acts, T, True, slots)
+    assert nfwd == cp.forward_steps_binomial(T, slots + 1)
+    assert len(used) <= slots
+
+
+def test_binomial_counts_of_the_named_workloads():
+    """Forward-step totals at the budgets of the four large workloads."""
+    W = adst.workloads.WORKLOADS
+    cases = {
+        "allencahn3d7_f64_512cube_T50": 90,
+        "vardiff2d9_f32_8192x8192_T200": 411,
+        "allencahn3d7_f64_1024cube_T200": 581,
+    }
+    for name, fwd in cases.items():
+        w = W[name]
+        p = adst.make_problem(w.kind, w.dtype, adst.workloads.dims_of(w.shape))
+        info = adst.adst_plan(p, w.steps, w.budget_bytes, adst.ADST_SCHED_BINOMIAL, w.want_dK)
+        assert info.fwd_steps_total == fwd, name
+    # Jacobi at the 10-snapshot budget with the tape forced: c = 11
+    w = W["jacobi2d5_f64_4096x4096_T100"]
+    p = adst.make_problem(w.kind, w.dtype, adst.workloads.dims_of(w.shape),
+                          flags=adst.ADST_FORCE_TAPE)
+    info = adst.adst_plan(p, w.steps, w.budget_bytes, adst.ADST_SCHED_BINOMIAL)
+    assert info.slots <= 10 and info.fwd_steps_total == 210
+    info = adst.adst_plan(p, w.steps, w.budget_bytes, adst.ADST_SCHED_UNIFORM)
+    assert info.fwd_steps_total == 541
+    # 64 GB (decimal) over 8 GiB states leaves 7 slots
+    w = W["allencahn3d7_f64_1024cube_T200"]
+    p = adst.make_problem(w.kind, w.dtype, adst.workloads.dims_of(w.shape))
+    info = adst.adst_plan(p, w.steps, w.budget_bytes, adst.ADST_SCHED_BINOMIAL)
+    assert info.slots == 7 and info.slot_bytes_peak <= w.budget_bytes
+
+
+def test_store_all():
+    p = prob()
+    for T in range(0, 30):
+        acts = adst.adst_plan_actions(p, T, budget_for(T), adst.ADST_SCHED_STORE_ALL)
+        nfwd, used = replay(acts, T, True, cp.store_all_slots(T))
+        assert nfwd == T and len(used) == cp.store_all_slots(T)
+
+
+def test_linear_kind_elides_the_tape():
+    """A step whose adjoint reads no state needs nothing stored at any budget."""
+    p = prob(adst.ADST_JACOBI2D5, (6, 5, 1))
+    for sched in range(4):
+        for slots in (0, 3, 100):
+            acts = adst.adst_plan_actions(p, 37, budget_for(slots, p), sched)
+            nfwd, used = replay(acts, 37, False, 0)
+            assert nfwd == 37 and not used
+    # the coefficient field's gradient makes the variable-coefficient kind read state
+    p = prob(adst.ADST_VARDIFF2D9, (6, 5, 1))
+    assert adst.adst_plan(p, 10, 0, 0, want_dcoeff=False).needs_state == 0
+    assert adst.adst_plan(p, 10, 0, 0, want_dcoeff=True).needs_state == 1
+    # forcing the tape makes a linear kind use the schedule
+    p = prob(adst.ADST_JACOBI2D5, (6, 5, 1), flags=adst.ADST_FORCE_TAPE)
+    acts = adst.adst_plan_actions(p, 37, budget_for(3, p), adst.ADST_SCHED_BINOMIAL)
+    nfwd, _ = replay(acts, 37, True, 3)
+    assert nfwd == cp.forward_steps_binomial(37, 4)
+
+
+def test_auto_picks_store_all_when_it_fits():
+    p = prob()
+    info = adst.adst_plan(p, 20, budget_for(18), adst.ADST_SCHED_AUTO)
+    assert info.sched == adst.ADST_SCHED_STORE_ALL and info.recompute_steps == 0
+    info = adst.adst_plan(p, 20, budget_for(17), adst.ADST_SCHED_AUTO)
+    assert info.sched == adst.ADST_SCHED_BINOMIAL and info.recompute_steps > 0
+    info = adst.adst_plan(p, 20, 0, adst.ADST_SCHED_AUTO)  # never fails on budget
+    assert info.slots == 0 and info.fwd_steps_total == cp.forward_steps_binomial(20, 1)
+
+
+def test_store_all_over_budget_is_an_error():
+    p = prob()
+    with pytest.raises(adst.AdstError) as e:
+        adst.adst_plan(p, 20, budget_for(17), adst.ADST_SCHED_STORE_ALL)
+    assert e.value.status == adst.ADST_ERR_BUDGET
+    assert "store-all" in adst.adst_last_error()
+
+
+def test_budget_counts_whole_slots_only():
+    p = prob()
+    S = budget_for(1)
+    assert adst.adst_plan(p, 50, 3 * S - 1, adst.ADST_SCHED_BINOMIAL).slots <= 2
+    assert adst.adst_plan(p, 50, 3 * S, adst.ADST_SCHED_BINOMIAL).slots == 3
+
+
+def test_workspace_and_bytes():
+    p = prob(dims=(100, 30, 7))
+    S = 100 * 30 * 7 * 8
+    stride = -(-S // 4096) * 4096
+    info = adst.adst_plan(p, 12, 4 * S, adst.ADST_SCHED_BINOMIAL)
+    assert info.state_bytes == S
+    assert info.workspace_bytes == 16384 + (3 + info.slots) * stride
+    assert info.fwd_workspace_bytes == S
+    # Allen-Cahn: 16 B per point per forward step, 24 per adjoint, 16 for the seed
+    n = 100 * 30 * 7
+    assert info.alg_bytes == n * (16 * info.fwd_steps_total + 24 * 12 + 16)
+    assert adst.adst_plan(p, 0, 0, 0).workspace_bytes == 16384
+
+
+def test_zero_steps_plan():
+    acts = adst.adst_plan_actions(prob(), 0, 0, adst.ADST_SCHED_AUTO)
+    assert acts == [(adst.ADST_OP_SEED, 0, adst.ADST_BUF_X0, adst.ADST_BUF_NONE)]
