@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the benchmark, copy a buffer of this size three times (a plain "
+                         "copy kernel of known size, to scale hardware byte counters)")
     return ap.parse_args()
 
 
@@ -211,6 +214,14 @@ def main():
         "phase_ms": {k: round(v, 4) for k, v in acc.items()},
         "roofline": roofline,
     }
+    if args.copy_probe_mib:
+        del ws
+        a = torch.empty(args.copy_probe_mib << 17, dtype=torch.float64, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        res["copy_probe_bytes"] = a.numel() * 8
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)

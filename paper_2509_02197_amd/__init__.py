@@ -191,7 +191,7 @@ def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
     import torch
     prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params)
     xT = torch.empty_like(x0)
-    info = adst_plan(prob, steps, 0, ADST_SCHED_AUTO)
+    info = adst_plan(prob, steps, 1 << 62, ADST_SCHED_STORE_ALL)
     ws = torch.empty(max(info.fwd_workspace_bytes, 1), dtype=torch.uint8, device=x0.device)
     adst_forward(prob, x0, coeff, steps, xT, ws, info.fwd_workspace_bytes, stream)
     return xT

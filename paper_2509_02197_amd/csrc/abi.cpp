@@ -183,45 +183,53 @@ adst_status check_disjoint(const std::vector<Range>& outs, const std::vector<Ran
   return ADST_OK;
 }
 
-// Per-launch HIP event timing for ADST_TRACE.
+// HIP event timing for ADST_TRACE. Events bracket maximal runs of launches
+// of one category (forward sweep, recomputation, seed, adjoint), so the
+// markers themselves add no gap between back-to-back kernels of a run.
 class Tracer {
  public:
+  enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, NCAT };
   explicit Tracer(bool on) : on_(on) {}
   ~Tracer() {
-    for (auto& e : events_) hipEventDestroy(e);
+    for (auto& g : segs_) {
+      if (g.start) hipEventDestroy(g.start);
+      if (g.stop) hipEventDestroy(g.stop);
+    }
   }
-  enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, NCAT };
-  hipError_t begin(hipStream_t s) {
+  // Call before enqueueing a launch of category cat.
+  hipError_t before(hipStream_t s, Cat cat) {
+    if (!on_ || (open_ && cat == cur_)) return hipSuccess;
+    hipError_t r = close(s);
+    if (r != hipSuccess) return r;
+    Seg g{nullptr, nullptr, cat};
+    if ((r = hipEventCreate(&g.start)) != hipSuccess) return r;
+    segs_.push_back(g);
+    open_ = true;
+    cur_ = cat;
+    return hipEventRecord(segs_.back().start, s);
+  }
+  hipError_t close(hipStream_t s) {
+    if (!on_ || !open_) return hipSuccess;
+    open_ = false;
+    hipError_t r = hipEventCreate(&segs_.back().stop);
+    if (r != hipSuccess) return r;
+    return hipEventRecord(segs_.back().stop, s);
+  }
+  // Waits for the last marker and fills the ms_* fields.
+  hipError_t finish(hipStream_t s, adst_plan_info* info) {
     if (!on_) return hipSuccess;
-    hipEvent_t e;
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-    events_.push_back(e);
-    return hipEventRecord(e, s);
-  }
-  hipError_t end(hipStream_t s, Cat cat) {
-    if (!on_) return hipSuccess;
-    hipEvent_t e;
-    hipError_t r = hipEventCreate(&e);
-    if (r != hipSuccess) return r;
-    events_.push_back(e);
-    cats_.push_back(cat);
-    return hipEventRecord(e, s);
-  }
-  hipError_t finish(adst_plan_info* info) {
-    if (!on_ || events_.empty()) return hipSuccess;
-    hipError_t r = hipEventSynchronize(events_.back());
-    if (r != hipSuccess) return r;
+    hipError_t r = close(s);
+    if (r != hipSuccess || segs_.empty()) return r;
+    if ((r = hipEventSynchronize(segs_.back().stop)) != hipSuccess) return r;
     float ms[NCAT] = {0, 0, 0, 0};
-    for (size_t k = 0; k < cats_.size(); ++k) {
+    for (const Seg& g : segs_) {
       float dt = 0.f;
-      r = hipEventElapsedTime(&dt, events_[2 * k], events_[2 * k + 1]);
-      if (r != hipSuccess) return r;
-      ms[cats_[k]] += dt;
+      if ((r = hipEventElapsedTime(&dt, g.start, g.stop)) != hipSuccess) return r;
+      ms[g.cat] += dt;
     }
     float total = 0.f;
-    r = hipEventElapsedTime(&total, events_.front(), events_.back());
-    if (r != hipSuccess) return r;
+    if ((r = hipEventElapsedTime(&total, segs_.front().start, segs_.back().stop)) != hipSuccess)
+      return r;
     if (info) {
       info->ms_fwd_sweep = ms[SWEEP];
       info->ms_fwd_recompute = ms[RECOMPUTE];
@@ -233,9 +241,14 @@ class Tracer {
   }
 
  private:
+  struct Seg {
+    hipEvent_t start, stop;
+    Cat cat;
+  };
   bool on_;
-  std::vector<hipEvent_t> events_;
-  std::vector<Cat> cats_;
+  bool open_ = false;
+  Cat cur_ = SWEEP;
+  std::vector<Seg> segs_;
 };
 
 adst_status hip_fail(hipError_t e, const char* what) {
@@ -369,11 +382,12 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   bool seeded = false;
   hipError_t e = hipSuccess;
   for (const adst_action& a : plan.acts) {
-    if ((e = tr.begin(stream)) != hipSuccess) return hip_fail(e, "trace event");
-    Tracer::Cat cat;
+    const Tracer::Cat cat = a.op == ADST_OP_FWD    ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
+                            : a.op == ADST_OP_SEED ? Tracer::SEED
+                                                   : Tracer::ADJ;
+    if ((e = tr.before(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
     if (a.op == ADST_OP_FWD) {
       e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
-      cat = seeded ? Tracer::RECOMPUTE : Tracer::SWEEP;
     } else if (a.op == ADST_OP_SEED) {
       const void* xsrc = buffer(a.src);
       void* xcopy = (steps == 0 && xT) ? xT : nullptr;
@@ -384,17 +398,14 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
       if (e == hipSuccess && steps == 0 && dcoeff)
         e = launch_fill_zero(dcoeff, (int64_t)S, stream);
       seeded = true;
-      cat = Tracer::SEED;
     } else {
       const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
       e = launch_adjoint(c.shape, xs, coeff, gbuf(a.t), gbuf(a.t - 1), dcoeff, a.t == steps,
                          stream);
-      cat = Tracer::ADJ;
     }
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
-    if ((e = tr.end(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
   }
-  if ((e = tr.finish(info)) != hipSuccess) return hip_fail(e, "trace");
+  if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");
   g_last_error.clear();
   return ADST_OK;
 }
