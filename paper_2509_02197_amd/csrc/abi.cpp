@@ -58,10 +58,14 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
   if (n >= (int64_t(1) << 31)) return fail(ADST_ERR_ARG, "grid must have fewer than 2^31 points");
   if ((p->kind == ADST_JACOBI2D5 || p->kind == ADST_VARDIFF2D9) && p->n[2] != 1)
     return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
-  // A dispatch covers whole 64x4 tiles of every plane; its work-item count
-  // must fit the 32-bit dispatch grid.
-  const int64_t tiles = ((p->n[0] + 63) / 64) * ((p->n[1] + 3) / 4) * p->n[2];
-  if (tiles * 256 >= (int64_t(1) << 32))
+  // Every launch covers the grid with workgroups of 256 work-items: 256 x 4
+  // (or x 8) tiles for the 2-D kinds, 64 x 8 x 32 columns for the 3-D kind.
+  // The work-item count must fit the 32-bit dispatch grid.
+  const int64_t tiles =
+      p->kind == ADST_ALLENCAHN3D7
+          ? ((p->n[0] + 63) / 64) * ((p->n[1] + 7) / 8) * ((p->n[2] + 31) / 32)
+          : ((p->n[0] + 255) / 256) * ((p->n[1] + 3) / 4);
+  if ((tiles + 8) * 256 >= (int64_t(1) << 32))
     return fail(ADST_ERR_UNSUPPORTED, "grid too thin in x/y for the tile shape");
   if (want_dcoeff && p->kind != ADST_VARDIFF2D9)
     return fail(ADST_ERR_UNSUPPORTED, "only the variable-coefficient kind has a coefficient field");

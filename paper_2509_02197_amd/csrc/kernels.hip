@@ -27,46 +27,97 @@ constexpr int kBX = 64;  // one wavefront along x
 constexpr int kBY = 4;   // four wavefronts per block
 constexpr int kThreads = kBX * kBY;
 
-struct Tile2 {
-  int i, j;
-};
-
-__device__ inline Tile2 tile2(int tiles_x) {
-  const int b = blockIdx.x;
-  return {(b % tiles_x) * kBX + (int)threadIdx.x, (b / tiles_x) * kBY + (int)threadIdx.y};
+// Launches cover their tiles in an XCD-aware order. Consecutive workgroup
+// ids go to the 8 XCDs in turn, and each XCD has its own L2; renumbering so
+// that XCD k works on the k-th contiguous eighth of the tiles keeps a tile's
+// x- and y-neighbours (whose cache lines its halo shares) in the same L2.
+// The grid is rounded up to a multiple of 8; surplus workgroups exit at once.
+__device__ inline int xcd_tile(int ntiles) {
+  const int per = (ntiles + 7) / 8;
+  return (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
 }
 
-struct Tile3 {
-  int i, j, k;
+inline unsigned xcd_grid(int64_t ntiles) { return (unsigned)(8 * ((ntiles + 7) / 8)); }
+
+// ------------------------------------------------------- 2-D LDS tiles
+// A workgroup of TW threads owns a TW x TR tile of the output; one thread per
+// column, TR rows each. It first stages rows j0-1 .. j0+TR of every input
+// array, columns i0-V .. i0+TW+V-1 (V elements = 16 bytes), in LDS with all
+// loads in flight at once (16-byte vector loads when rows are 16-byte
+// aligned), then computes from LDS. Cells outside the grid read 0 and are
+// never used by a formula that drops them.
+template <class R, int TW, int TR>
+struct Tile2 {
+  static constexpr int V = 16 / sizeof(R);
+  static constexpr int LW = TW + 2 * V;  // LDS row length
+  static constexpr int LR = TR + 2;      // LDS rows
+  static constexpr int CH = LW / V;      // 16-byte chunks per LDS row
 };
 
-__device__ inline Tile3 tile3(int tiles_x, int tiles_y) {
-  int b = blockIdx.x;
-  const int bx = b % tiles_x;
-  b /= tiles_x;
-  const int by = b % tiles_y;
-  const int bz = b / tiles_y;
-  return {bx * kBX + (int)threadIdx.x, by * kBY + (int)threadIdx.y, bz};
+template <class R, int TW, int TR>
+__device__ inline void stage_tile(R* lds, const R* __restrict__ a, int i0, int j0, int nx, int ny,
+                                  bool vec) {
+  using G = Tile2<R, TW, TR>;
+  constexpr int V = G::V;
+  typedef R vec_t __attribute__((ext_vector_type(V)));
+  for (int q = threadIdx.x; q < G::LR * G::CH; q += TW) {
+    const int rr = q / G::CH, ch = q - rr * G::CH;
+    const int jj = j0 - 1 + rr;
+    const int ii = i0 - V + ch * V;
+    R* dst = lds + rr * G::LW + ch * V;
+    if (jj < 0 || jj >= ny) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) dst[e] = R(0);
+    } else if (vec && ii >= 0 && ii + V <= nx) {
+      const vec_t v = *reinterpret_cast<const vec_t*>(a + jj * nx + ii);
+#pragma unroll
+      for (int e = 0; e < V; ++e) dst[e] = v[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const int c = ii + e;
+        dst[e] = (c >= 0 && c < nx) ? a[jj * nx + c] : R(0);
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------- Jacobi 2-D
+constexpr int kJacTW = 256, kJacTR = 8;
+
 // Forward: interior x'[c] = w*((((x[c]+x[W])+x[E])+x[S])+x[N]); ring copied.
 template <class R>
-__global__ __launch_bounds__(kThreads) void fwd_jacobi2d5(const R* __restrict__ x,
-                                                          R* __restrict__ y, int nx, int ny,
-                                                          int tiles_x, R w) {
-  const Tile2 t = tile2(tiles_x);
-  if (t.i >= nx || t.j >= ny) return;
-  const int c = t.j * nx + t.i;
-  if (t.i > 0 && t.i < nx - 1 && t.j > 0 && t.j < ny - 1) {
-    R s = x[c];
-    s += x[c - 1];
-    s += x[c + 1];
-    s += x[c - nx];
-    s += x[c + nx];
-    y[c] = w * s;
-  } else {
-    y[c] = x[c];
+__global__ __launch_bounds__(kJacTW) void fwd_jacobi2d5(const R* __restrict__ x,
+                                                        R* __restrict__ y, int nx, int ny,
+                                                        int tiles_x, int ntiles, int vec, R w) {
+  using G = Tile2<R, kJacTW, kJacTR>;
+  __shared__ R s[G::LR][G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacTR;
+  stage_tile<R, kJacTW, kJacTR>(&s[0][0], x, i0, j0, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  if (i >= nx) return;
+  const int cx = G::V + (int)threadIdx.x;
+  const bool xin = i > 0 && i < nx - 1;
+#pragma unroll
+  for (int r = 0; r < kJacTR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const R c = s[r + 1][cx];
+    R out;
+    if (xin && j > 0 && j < ny - 1) {
+      R sum = c;
+      sum += s[r + 1][cx - 1];
+      sum += s[r + 1][cx + 1];
+      sum += s[r][cx];
+      sum += s[r + 2][cx];
+      out = w * sum;
+    } else {
+      out = c;
+    }
+    y[j * nx + i] = out;
   }
 }
 
@@ -75,34 +126,95 @@ __global__ __launch_bounds__(kThreads) void fwd_jacobi2d5(const R* __restrict__ 
 //   ring m:     g'[m] = g[m] + w * sum_{q in nbr(m)} gi(q)
 // Points two or more cells from the edge see only interior neighbours.
 template <class R>
-__global__ __launch_bounds__(kThreads) void adj_jacobi2d5(const R* __restrict__ g,
-                                                          R* __restrict__ gp, int nx, int ny,
-                                                          int tiles_x, R w) {
-  const Tile2 t = tile2(tiles_x);
-  if (t.i >= nx || t.j >= ny) return;
-  const int i = t.i, j = t.j;
-  const int c = j * nx + i;
-  if (i >= 2 && i <= nx - 3 && j >= 2 && j <= ny - 3) {
-    R s = g[c];
-    s += g[c - 1];
-    s += g[c + 1];
-    s += g[c - nx];
-    s += g[c + nx];
-    gp[c] = w * s;
-    return;
+__global__ __launch_bounds__(kJacTW) void adj_jacobi2d5(const R* __restrict__ g,
+                                                        R* __restrict__ gp, int nx, int ny,
+                                                        int tiles_x, int ntiles, int vec, R w) {
+  using G = Tile2<R, kJacTW, kJacTR>;
+  __shared__ R s[G::LR][G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacTR;
+  stage_tile<R, kJacTW, kJacTR>(&s[0][0], g, i0, j0, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  if (i >= nx) return;
+  const int cx = G::V + (int)threadIdx.x;
+  const bool deep_cols = i >= 2 && i <= nx - 3;
+  auto interior = [&](int a, int bb) { return a > 0 && a < nx - 1 && bb > 0 && bb < ny - 1; };
+#pragma unroll
+  for (int r = 0; r < kJacTR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const R c = s[r + 1][cx];
+    R out;
+    if (deep_cols && j >= 2 && j <= ny - 3) {
+      R sum = c;
+      sum += s[r + 1][cx - 1];
+      sum += s[r + 1][cx + 1];
+      sum += s[r][cx];
+      sum += s[r + 2][cx];
+      out = w * sum;
+    } else {
+      R sum = interior(i - 1, j) ? s[r + 1][cx - 1] : R(0);
+      sum += interior(i + 1, j) ? s[r + 1][cx + 1] : R(0);
+      sum += interior(i, j - 1) ? s[r][cx] : R(0);
+      sum += interior(i, j + 1) ? s[r + 2][cx] : R(0);
+      out = interior(i, j) ? w * (c + sum) : c + w * sum;
+    }
+    gp[j * nx + i] = out;
   }
-  auto gi = [&](int a, int b) -> R {
-    return (a > 0 && a < nx - 1 && b > 0 && b < ny - 1) ? g[b * nx + a] : R(0);
-  };
-  R s = gi(i - 1, j);
-  s += gi(i + 1, j);
-  s += gi(i, j - 1);
-  s += gi(i, j + 1);
-  const bool interior = i > 0 && i < nx - 1 && j > 0 && j < ny - 1;
-  gp[c] = interior ? w * (g[c] + s) : g[c] + w * s;
 }
 
 // ------------------------------------------------------- Allen-Cahn 3-D
+// 2.5-D blocking: a workgroup of 64 x 4 threads owns a 64 x 8 column of the
+// grid over kAcZC planes (two rows per thread) and marches in z. The plane
+// being updated is staged in LDS with a one-cell xy halo; the planes below
+// and above live in registers, so every input plane is read from HBM once
+// per tile.
+constexpr int kAcTX = 64, kAcTY = 8, kAcZC = 32;
+
+struct AcTile {
+  int i, ja, jb, by, bx, z0, z1;
+};
+
+__device__ inline bool ac_tile(int nx, int ny, int nz, int tiles_x, int tiles_y, int ntiles,
+                               AcTile* t) {
+  int b = xcd_tile(ntiles);
+  if (b >= ntiles) return false;
+  t->bx = b % tiles_x;
+  b /= tiles_x;
+  t->by = b % tiles_y;
+  const int bz = b / tiles_y;
+  t->i = t->bx * kAcTX + (int)threadIdx.x;
+  t->ja = t->by * kAcTY + (int)threadIdx.y;
+  t->jb = t->ja + 4;
+  t->z0 = bz * kAcZC;
+  t->z1 = min(t->z0 + kAcZC, nz);
+  return true;
+}
+
+// Halo cell this thread stages (at most one; 2*64 + 2*8 = 144 < 256).
+__device__ inline void ac_halo_cell(int tid, int* ly, int* lx) {
+  constexpr int LY = kAcTY + 2, LX = kAcTX + 2;
+  const int h = tid;
+  if (h < kAcTX) {
+    *ly = 0;
+    *lx = h + 1;
+  } else if (h < 2 * kAcTX) {
+    *ly = LY - 1;
+    *lx = h - kAcTX + 1;
+  } else if (h < 2 * kAcTX + kAcTY) {
+    *ly = h - 2 * kAcTX + 1;
+    *lx = 0;
+  } else if (h < 2 * kAcTX + 2 * kAcTY) {
+    *ly = h - 2 * kAcTX - kAcTY + 1;
+    *lx = LX - 1;
+  } else {
+    *ly = -1;
+    *lx = 0;
+  }
+}
+
 // Forward, zero ghost values:
 //   lap = (((((x[-x]+x[+x])+x[-y])+x[+y])+x[-z])+x[+z]) - 6*a
 //   x'  = (a + D*lap) - C*((a*a)*a)
@@ -110,25 +222,55 @@ template <class R>
 __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict__ x,
                                                              R* __restrict__ y, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
-                                                             R D, R C) {
-  const Tile3 t = tile3(tiles_x, tiles_y);
-  if (t.i >= nx || t.j >= ny) return;
+                                                             int ntiles, R D, R C) {
+  __shared__ R tile[kAcTY + 2][kAcTX + 2];
+  AcTile t;
+  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;
   const int plane = nx * ny;
-  const int c = t.k * plane + t.j * nx + t.i;
-  const R a = x[c];
-  const R xm = t.i > 0 ? x[c - 1] : R(0);
-  const R xp = t.i < nx - 1 ? x[c + 1] : R(0);
-  const R ym = t.j > 0 ? x[c - nx] : R(0);
-  const R yp = t.j < ny - 1 ? x[c + nx] : R(0);
-  const R zm = t.k > 0 ? x[c - plane] : R(0);
-  const R zp = t.k < nz - 1 ? x[c + plane] : R(0);
-  R lap = xm + xp;
-  lap += ym;
-  lap += yp;
-  lap += zm;
-  lap += zp;
-  lap = lap - R(6) * a;
-  y[c] = (a + D * lap) - C * ((a * a) * a);
+  auto ld = [&](int k, int j, int i) -> R {
+    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? x[k * plane + j * nx + i]
+                                                                      : R(0);
+  };
+  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
+  int hly, hlx;
+  ac_halo_cell(tid, &hly, &hlx);
+  const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
+  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
+  R belowA = ld(t.z0 - 1, t.ja, t.i), belowB = ld(t.z0 - 1, t.jb, t.i);
+  R curA = ld(t.z0, t.ja, t.i), curB = ld(t.z0, t.jb, t.i);
+  for (int k = t.z0; k < t.z1; ++k) {
+    const R aboveA = ld(k + 1, t.ja, t.i), aboveB = ld(k + 1, t.jb, t.i);
+    const R halo = hly >= 0 ? ld(k, hj, hi) : R(0);
+    __syncthreads();
+    tile[ty + 1][tx + 1] = curA;
+    tile[ty + 5][tx + 1] = curB;
+    if (hly >= 0) tile[hly][hlx] = halo;
+    __syncthreads();
+    if (va) {
+      const R a = curA;
+      R lap = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
+      lap += tile[ty][tx + 1];
+      lap += tile[ty + 2][tx + 1];
+      lap += belowA;
+      lap += aboveA;
+      lap = lap - R(6) * a;
+      y[k * plane + t.ja * nx + t.i] = (a + D * lap) - C * ((a * a) * a);
+    }
+    if (vb) {
+      const R a = curB;
+      R lap = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
+      lap += tile[ty + 4][tx + 1];
+      lap += tile[ty + 6][tx + 1];
+      lap += belowB;
+      lap += aboveB;
+      lap = lap - R(6) * a;
+      y[k * plane + t.jb * nx + t.i] = (a + D * lap) - C * ((a * a) * a);
+    }
+    belowA = curA;
+    belowB = curB;
+    curA = aboveA;
+    curB = aboveB;
+  }
 }
 
 // Adjoint: dx'[m]/dx[m] = (1 - 6D) - 3C x[m]^2 (the nonlinear term's adjoint,
@@ -140,96 +282,157 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
                                                              const R* __restrict__ g,
                                                              R* __restrict__ gp, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
-                                                             R D, R k0, R k1) {
-  const Tile3 t = tile3(tiles_x, tiles_y);
-  if (t.i >= nx || t.j >= ny) return;
+                                                             int ntiles, R D, R k0, R k1) {
+  __shared__ R tile[kAcTY + 2][kAcTX + 2];
+  AcTile t;
+  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;
   const int plane = nx * ny;
-  const int c = t.k * plane + t.j * nx + t.i;
-  const R gm = t.i > 0 ? g[c - 1] : R(0);
-  const R gpx = t.i < nx - 1 ? g[c + 1] : R(0);
-  const R gym = t.j > 0 ? g[c - nx] : R(0);
-  const R gyp = t.j < ny - 1 ? g[c + nx] : R(0);
-  const R gzm = t.k > 0 ? g[c - plane] : R(0);
-  const R gzp = t.k < nz - 1 ? g[c + plane] : R(0);
-  R s = gm + gpx;
-  s += gym;
-  s += gyp;
-  s += gzm;
-  s += gzp;
-  const R a = x[c];
-  gp[c] = (k0 - k1 * (a * a)) * g[c] + D * s;
+  auto ld = [&](int k, int j, int i) -> R {
+    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? g[k * plane + j * nx + i]
+                                                                      : R(0);
+  };
+  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
+  int hly, hlx;
+  ac_halo_cell(tid, &hly, &hlx);
+  const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
+  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
+  R belowA = ld(t.z0 - 1, t.ja, t.i), belowB = ld(t.z0 - 1, t.jb, t.i);
+  R curA = ld(t.z0, t.ja, t.i), curB = ld(t.z0, t.jb, t.i);
+  for (int k = t.z0; k < t.z1; ++k) {
+    const R aboveA = ld(k + 1, t.ja, t.i), aboveB = ld(k + 1, t.jb, t.i);
+    const R halo = hly >= 0 ? ld(k, hj, hi) : R(0);
+    const R xa = va ? x[k * plane + t.ja * nx + t.i] : R(0);
+    const R xb = vb ? x[k * plane + t.jb * nx + t.i] : R(0);
+    __syncthreads();
+    tile[ty + 1][tx + 1] = curA;
+    tile[ty + 5][tx + 1] = curB;
+    if (hly >= 0) tile[hly][hlx] = halo;
+    __syncthreads();
+    if (va) {
+      R s = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
+      s += tile[ty][tx + 1];
+      s += tile[ty + 2][tx + 1];
+      s += belowA;
+      s += aboveA;
+      gp[k * plane + t.ja * nx + t.i] = (k0 - k1 * (xa * xa)) * curA + D * s;
+    }
+    if (vb) {
+      R s = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
+      s += tile[ty + 4][tx + 1];
+      s += tile[ty + 6][tx + 1];
+      s += belowB;
+      s += aboveB;
+      gp[k * plane + t.jb * nx + t.i] = (k0 - k1 * (xb * xb)) * curB + D * s;
+    }
+    belowA = curA;
+    belowB = curB;
+    curA = aboveA;
+    curB = aboveB;
+  }
 }
 
 // ------------------------------------------ variable-coefficient diffusion 2-D
 // Neighbour order (-1,0),(+1,0),(0,-1),(0,+1),(-1,-1),(+1,-1),(-1,+1),(+1,+1);
 // the first four carry weight ca (1/3), the last four cd (1/12).
-__constant__ int kNbrDx[8] = {-1, 1, 0, 0, -1, 1, -1, 1};
-__constant__ int kNbrDy[8] = {0, 0, -1, 1, -1, -1, 1, 1};
+constexpr int kNbrDx[8] = {-1, 1, 0, 0, -1, 1, -1, 1};
+constexpr int kNbrDy[8] = {0, 0, -1, 1, -1, -1, 1, 1};
+constexpr int kVdTW = 256, kVdTR = 8, kVdAdjTR = 4;
 
 // Forward: acc = sum over in-grid n of (c_n*(K[c]+K[n]))*(x[n]-x[c]),
 // x' = x[c] + dt*acc.
 template <class R>
-__global__ __launch_bounds__(kThreads) void fwd_vardiff2d9(const R* __restrict__ x,
-                                                           const R* __restrict__ K,
-                                                           R* __restrict__ y, int nx, int ny,
-                                                           int tiles_x, R dt, R ca, R cd) {
-  const Tile2 t = tile2(tiles_x);
-  if (t.i >= nx || t.j >= ny) return;
-  const int i = t.i, j = t.j;
-  const int c = j * nx + i;
-  const R xc = x[c], Kc = K[c];
-  R acc = R(0);
-  if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
+__global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
+                                                        const R* __restrict__ K,
+                                                        R* __restrict__ y, int nx, int ny,
+                                                        int tiles_x, int ntiles, int vec, R dt,
+                                                        R ca, R cd) {
+  using G = Tile2<R, kVdTW, kVdTR>;
+  __shared__ R sx[G::LR][G::LW];
+  __shared__ R sk[G::LR][G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * kVdTR;
+  stage_tile<R, kVdTW, kVdTR>(&sx[0][0], x, i0, j0, nx, ny, vec);
+  stage_tile<R, kVdTW, kVdTR>(&sk[0][0], K, i0, j0, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  if (i >= nx) return;
+  const int cx = G::V + (int)threadIdx.x;
+  const bool xin = i > 0 && i < nx - 1;
+#pragma unroll 4
+  for (int r = 0; r < kVdTR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const R xc = sx[r + 1][cx], Kc = sk[r + 1][cx];
+    R acc = R(0);
+    if (xin && j > 0 && j < ny - 1) {
 #pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      const int m = c + kNbrDy[n] * nx + kNbrDx[n];
-      const R cn = n < 4 ? ca : cd;
-      acc += (cn * (Kc + K[m])) * (x[m] - xc);
-    }
-  } else {
+      for (int n = 0; n < 8; ++n) {
+        const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
+        acc += ((n < 4 ? ca : cd) * (Kc + sk[rr][cc])) * (sx[rr][cc] - xc);
+      }
+    } else {
 #pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      const int a = i + kNbrDx[n], b = j + kNbrDy[n];
-      if (a < 0 || a >= nx || b < 0 || b >= ny) continue;
-      const int m = b * nx + a;
-      const R cn = n < 4 ? ca : cd;
-      acc += (cn * (Kc + K[m])) * (x[m] - xc);
+      for (int n = 0; n < 8; ++n) {
+        const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
+        if (a < 0 || a >= nx || bb < 0 || bb >= ny) continue;
+        const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
+        acc += ((n < 4 ? ca : cd) * (Kc + sk[rr][cc])) * (sx[rr][cc] - xc);
+      }
     }
+    y[j * nx + i] = xc + dt * acc;
   }
-  y[c] = xc + dt * acc;
 }
 
 // Adjoint (the operator is symmetric in x):
 //   g'[m] = g[m] + dt * sum_n (c_n*(K[m]+K[n]))*(g[n]-g[m])
 //   dK[m] += dt * sum_n (c_n*(x[n]-x[m]))*(g[m]-g[n])      (x = x_{t-1})
 // the second line being the coefficient-field gradient of step t, fused.
-template <class R, bool WANT_DK>
-__global__ __launch_bounds__(kThreads) void adj_vardiff2d9(const R* __restrict__ x,
-                                                           const R* __restrict__ K,
-                                                           const R* __restrict__ g,
-                                                           R* __restrict__ gp, R* __restrict__ dK,
-                                                           int dk_first, int nx, int ny,
-                                                           int tiles_x, R dt, R ca, R cd) {
-  const Tile2 t = tile2(tiles_x);
-  if (t.i >= nx || t.j >= ny) return;
-  const int i = t.i, j = t.j;
-  const int c = j * nx + i;
-  const R gc = g[c], Kc = K[c];
-  const R xc = WANT_DK ? x[c] : R(0);
-  R ag = R(0), ak = R(0);
-  const bool interior = i > 0 && i < nx - 1 && j > 0 && j < ny - 1;
+template <class R, bool WANT_DK, int TR>
+__global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
+                                                        const R* __restrict__ K,
+                                                        const R* __restrict__ g,
+                                                        R* __restrict__ gp, R* __restrict__ dK,
+                                                        int dk_first, int nx, int ny,
+                                                        int tiles_x, int ntiles, int vec, R dt,
+                                                        R ca, R cd) {
+  using G = Tile2<R, kVdTW, TR>;
+  __shared__ R sg[G::LR][G::LW];
+  __shared__ R sk[G::LR][G::LW];
+  __shared__ R sx[WANT_DK ? G::LR : 1][WANT_DK ? G::LW : 1];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * TR;
+  stage_tile<R, kVdTW, TR>(&sg[0][0], g, i0, j0, nx, ny, vec);
+  stage_tile<R, kVdTW, TR>(&sk[0][0], K, i0, j0, nx, ny, vec);
+  if (WANT_DK) stage_tile<R, kVdTW, TR>(&sx[0][0], x, i0, j0, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  if (i >= nx) return;
+  const int cx = G::V + (int)threadIdx.x;
+  const bool xin = i > 0 && i < nx - 1;
+#pragma unroll 2
+  for (int r = 0; r < TR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const int c = j * nx + i;
+    const R gc = sg[r + 1][cx], Kc = sk[r + 1][cx];
+    const R xc = WANT_DK ? sx[r + 1][cx] : R(0);
+    R ag = R(0), ak = R(0);
+    const bool inner = xin && j > 0 && j < ny - 1;
 #pragma unroll
-  for (int n = 0; n < 8; ++n) {
-    const int a = i + kNbrDx[n], b = j + kNbrDy[n];
-    if (!interior && (a < 0 || a >= nx || b < 0 || b >= ny)) continue;
-    const int m = b * nx + a;
-    const R cn = n < 4 ? ca : cd;
-    const R gn = g[m];
-    ag += (cn * (Kc + K[m])) * (gn - gc);
-    if (WANT_DK) ak += (cn * (x[m] - xc)) * (gc - gn);
+    for (int n = 0; n < 8; ++n) {
+      const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
+      if (!inner && (a < 0 || a >= nx || bb < 0 || bb >= ny)) continue;
+      const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
+      const R cn = n < 4 ? ca : cd;
+      const R gn = sg[rr][cc];
+      ag += (cn * (Kc + sk[rr][cc])) * (gn - gc);
+      if (WANT_DK) ak += (cn * (sx[rr][cc] - xc)) * (gc - gn);
+    }
+    gp[c] = gc + dt * ag;
+    if (WANT_DK) dK[c] = (dk_first ? R(0) : dK[c]) + dt * ak;
   }
-  gp[c] = gc + dt * ag;
-  if (WANT_DK) dK[c] = (dk_first ? R(0) : dK[c]) + dt * ak;
 }
 
 // --------------------------------------------------------------- loss, seed
@@ -308,26 +511,45 @@ int grid_for(int64_t n, int64_t per_block, int64_t cap) {
   return (int)b;
 }
 
+// 16-byte vector loads need every staged array 16-byte aligned and rows whose
+// starts stay aligned (nx a multiple of the vector width).
+template <class R>
+int vec_ok(int nx, const void* a, const void* b = nullptr, const void* c = nullptr) {
+  if (nx % (16 / (int)sizeof(R))) return 0;
+  for (const void* p : {a, b, c})
+    if (p && (reinterpret_cast<uintptr_t>(p) & 15u)) return 0;
+  return 1;
+}
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
 template <class R>
 hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv,
                      hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
+  const R* K = static_cast<const R*>(Kv);
   R* y = static_cast<R*>(yv);
-  const dim3 block(kBX, kBY);
-  const int tx = (s.nx + kBX - 1) / kBX, ty = (s.ny + kBY - 1) / kBY;
-  const dim3 grid((unsigned)((int64_t)tx * ty * s.nz));
   switch (s.kind) {
-    case ADST_JACOBI2D5:
-      fwd_jacobi2d5<R><<<grid, block, 0, st>>>(x, y, s.nx, s.ny, tx, R(s.p0));
+    case ADST_JACOBI2D5: {
+      const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
+      fwd_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+          x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
       break;
-    case ADST_ALLENCAHN3D7:
-      fwd_allencahn3d7<R><<<grid, block, 0, st>>>(x, y, s.nx, s.ny, s.nz, tx, ty, R(s.p0),
-                                                  R(s.p1));
+    }
+    case ADST_ALLENCAHN3D7: {
+      const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
+      const int nt = tx * ty * cdiv(s.nz, kAcZC);
+      fwd_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+          x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
       break;
-    case ADST_VARDIFF2D9:
-      fwd_vardiff2d9<R><<<grid, block, 0, st>>>(x, static_cast<const R*>(Kv), y, s.nx, s.ny, tx,
-                                                R(s.p0), R(1) / R(3), R(1) / R(12));
+    }
+    case ADST_VARDIFF2D9: {
+      const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
+      fwd_vardiff2d9<R><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+          x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
+          R(1) / R(12));
       break;
+    }
     default:
       return hipErrorInvalidValue;
   }
@@ -342,28 +564,37 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
   const R* g = static_cast<const R*>(gv);
   R* gp = static_cast<R*>(gpv);
   R* dK = static_cast<R*>(dKv);
-  const dim3 block(kBX, kBY);
-  const int tx = (s.nx + kBX - 1) / kBX, ty = (s.ny + kBY - 1) / kBY;
-  const dim3 grid((unsigned)((int64_t)tx * ty * s.nz));
   switch (s.kind) {
-    case ADST_JACOBI2D5:
-      adj_jacobi2d5<R><<<grid, block, 0, st>>>(g, gp, s.nx, s.ny, tx, R(s.p0));
+    case ADST_JACOBI2D5: {
+      const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
+      adj_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+          g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
       break;
+    }
     case ADST_ALLENCAHN3D7: {
       const R D = R(s.p0), C = R(s.p1);
       const R k0 = R(1) + D * R(-6), k1 = R(3) * C;
-      adj_allencahn3d7<R><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, D, k0, k1);
+      const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
+      const int nt = tx * ty * cdiv(s.nz, kAcZC);
+      adj_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+          x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1);
       break;
     }
-    case ADST_VARDIFF2D9:
-      if (dK)
-        adj_vardiff2d9<R, true><<<grid, block, 0, st>>>(x, K, g, gp, dK, dk_first ? 1 : 0, s.nx,
-                                                        s.ny, tx, R(s.p0), R(1) / R(3),
-                                                        R(1) / R(12));
-      else
-        adj_vardiff2d9<R, false><<<grid, block, 0, st>>>(x, K, g, gp, nullptr, 0, s.nx, s.ny, tx,
-                                                         R(s.p0), R(1) / R(3), R(1) / R(12));
+    case ADST_VARDIFF2D9: {
+      const int tx = cdiv(s.nx, kVdTW);
+      if (dK) {
+        const int nt = tx * cdiv(s.ny, kVdAdjTR);
+        adj_vardiff2d9<R, true, kVdAdjTR><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K, x),
+            R(s.p0), R(1) / R(3), R(1) / R(12));
+      } else {
+        const int nt = tx * cdiv(s.ny, kVdTR);
+        adj_vardiff2d9<R, false, kVdTR><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+            nullptr, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K),
+            R(s.p0), R(1) / R(3), R(1) / R(12));
+      }
       break;
+    }
     default:
       return hipErrorInvalidValue;
   }
