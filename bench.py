@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--sched", default=None, choices=list(SCHED_NAMES.values()))
     ap.add_argument("--budget-bytes", type=int, default=None)
     ap.add_argument("--force-tape", action="store_true")
+    ap.add_argument("--no-fuse", action="store_true",
+                    help="one launch per step (no temporal blocking)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
@@ -123,7 +125,8 @@ def main():
     if args.sched:
         sched = {v: k for k, v in SCHED_NAMES.items()}[args.sched]
     budget = w.budget_bytes if args.budget_bytes is None else args.budget_bytes
-    flags = adst.ADST_FORCE_TAPE if args.force_tape else 0
+    flags = (adst.ADST_FORCE_TAPE if args.force_tape else 0) | \
+        (adst.ADST_NO_FUSE if args.no_fuse else 0)
 
     print(f"# bench workload={name} sched={SCHED_NAMES[sched]} budget={budget} "
           f"force_tape={args.force_tape}", file=sys.stderr, flush=True)
@@ -172,18 +175,31 @@ def main():
         ti = call(tprob)
         for k in acc:
             acc[k] += getattr(ti, k) / args.steps
+    # Roofline of the dominant kernel: algorithmic bytes of one launch (its
+    # inputs read once and its output written once; a fused two-step launch
+    # moves the same bytes as a single step) over its average launch time.
     isz = 8 if w.dtype == adst.ADST_F64 else 4
     fwd_B = {0: 2, 1: 2, 2: 3}[w.kind] * isz
     adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3}[w.kind] * isz
-    n_fwd, n_adj = info.fwd_steps_total, info.adj_steps
+    n_fwd, n_adj = info.fwd_launches, info.adj_launches
+    fused_fwd = info.fwd_steps_total - info.fwd_launches
+    fused_adj = info.adj_steps - info.adj_launches
     ms_fwd = acc["ms_fwd_sweep"] + acc["ms_fwd_recompute"]
     fwd_avg = ms_fwd / max(n_fwd, 1)
     adj_avg = acc["ms_adj"] / max(n_adj, 1)
     kname = KERNELS[w.kind]
+
+    def launched(base, n, fused):
+        if fused == 0:
+            return base
+        return base + "_x2" if fused == n else base + " + " + base + "_x2"
+
     if ms_fwd >= acc["ms_adj"]:
-        kernel, avg_ms, per_pt = kname[0], fwd_avg, fwd_B
+        kernel, avg_ms, per_pt, nl, ns = (launched(kname[0], n_fwd, fused_fwd), fwd_avg, fwd_B,
+                                          n_fwd, info.fwd_steps_total)
     else:
-        kernel, avg_ms, per_pt = kname[1], adj_avg, adj_B
+        kernel, avg_ms, per_pt, nl, ns = (launched(kname[1], n_adj, fused_adj), adj_avg, adj_B,
+                                          n_adj, info.adj_steps)
     alg_bytes = per_pt * w.npoints
     achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
     traffic = traffic_for(name, kernel, 1)
@@ -191,7 +207,8 @@ def main():
         "bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
         "traffic": traffic, "alg_bytes_per_launch": alg_bytes,
-        "avg_launch_ms": round(avg_ms, 5), "launches_per_step": n_fwd if kernel == kname[0] else n_adj,
+        "avg_launch_ms": round(avg_ms, 5), "launches_per_step": nl,
+        "steps_per_launch": round(ns / max(nl, 1), 3),
         "fwd_avg_ms": round(fwd_avg, 5), "fwd_gbps": round(fwd_B * w.npoints / fwd_avg / 1e6, 1),
         "adj_avg_ms": round(adj_avg, 5), "adj_gbps": round(adj_B * w.npoints / adj_avg / 1e6, 1),
     }
@@ -206,8 +223,9 @@ def main():
             "loss": LOSS_NAMES[w.loss], "budget_bytes": budget,
             "schedule": SCHED_NAMES[info.sched] + ("" if info.needs_state else " (tape elided)"),
             "slots": info.slots, "fwd_steps": info.fwd_steps_total,
-            "recompute_steps": info.recompute_steps, "grads": "dx0,dK" if w.want_dK else "dx0",
-            "force_tape": bool(args.force_tape),
+            "recompute_steps": info.recompute_steps, "fwd_launches": info.fwd_launches,
+            "adj_launches": info.adj_launches, "grads": "dx0,dK" if w.want_dK else "dx0",
+            "force_tape": bool(args.force_tape), "temporal_blocking": not args.no_fuse,
         },
         "hbm_gbps_effective": round(info.alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "event_ms_per_step": ev_ms / args.steps,

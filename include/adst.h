@@ -98,8 +98,10 @@ typedef enum {
 /* Problem flags. */
 #define ADST_FORCE_TAPE 0x1u /* treat every step as reading x_{t-1} in its adjoint, even when
                                 the kind is linear, so store/recompute runs at any shape */
-#define ADST_TRACE 0x2u      /* time every launch with HIP events, synchronise the stream at
+#define ADST_TRACE 0x2u      /* time the launches with HIP events, synchronise the stream at
                                 the end of the call and fill the ms_* fields of adst_plan_info */
+#define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking);
+                                results are bit-identical either way */
 
 typedef struct {
   int32_t kind;   /* adst_kind */
@@ -107,7 +109,7 @@ typedef struct {
   int64_t n[3];   /* n[0] = nx (fastest), n[1] = ny, n[2] = nz (1 for the 2-D kinds);
                      every n[i] >= 1 and n[0]*n[1]*n[2] < 2^31 */
   double p[2];    /* step constants, see the kinds above; rounded to the working precision */
-  uint32_t flags; /* ADST_FORCE_TAPE | ADST_TRACE */
+  uint32_t flags; /* ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE */
 } adst_problem;
 
 /* One action of a reverse-sweep plan. Buffers are named by small integers:
@@ -116,8 +118,21 @@ typedef struct {
  *   ADST_OP_FWD   x_t = F(state in src), written to dst
  *   ADST_OP_SEED  loss and seed g_T from x_T held in src (t = T)
  *   ADST_OP_ADJ   g_{t-1} = J_t^T g_t, reading x_{t-1} from src
- *                 (src = ADST_BUF_NONE when the step's adjoint reads no state) */
-typedef enum { ADST_OP_FWD = 0, ADST_OP_SEED = 1, ADST_OP_ADJ = 2 } adst_op;
+ *                 (src = ADST_BUF_NONE when the step's adjoint reads no state)
+ *   ADST_OP_FWD2  x_t = F(F(state in src)) (steps t-1 and t in one launch, the
+ *                 intermediate x_{t-1} kept on chip; emitted only where nothing
+ *                 else reads x_{t-1}), written to dst
+ *   ADST_OP_ADJ2  g_{t-2} = J_{t-1}^T J_t^T g_t in one launch (state-free
+ *                 adjoints only; src = ADST_BUF_NONE)
+ * Fused actions (temporal blocking) evaluate every point with the same
+ * expression as the single steps, so results are bit-identical. */
+typedef enum {
+  ADST_OP_FWD = 0,
+  ADST_OP_SEED = 1,
+  ADST_OP_ADJ = 2,
+  ADST_OP_FWD2 = 3,
+  ADST_OP_ADJ2 = 4
+} adst_op;
 enum {
   ADST_BUF_NONE = -1,
   ADST_BUF_X0 = 0,
@@ -142,6 +157,8 @@ typedef struct {
   int64_t recompute_steps;  /* fwd_steps_total - T */
   int64_t adj_steps;        /* T */
   int64_t n_actions;        /* length of the action list */
+  int64_t fwd_launches;     /* forward launches (a fused pair counts once) */
+  int64_t adj_launches;     /* adjoint launches (a fused pair counts once) */
   uint64_t state_bytes;     /* bytes of one state */
   uint64_t budget_bytes;    /* the budget passed in */
   uint64_t slot_bytes_peak; /* slots * state_bytes: checkpoint storage actually used */

@@ -21,8 +21,8 @@ ADST_JACOBI2D5, ADST_ALLENCAHN3D7, ADST_VARDIFF2D9 = 0, 1, 2
 ADST_F64, ADST_F32 = 0, 1
 ADST_SCHED_AUTO, ADST_SCHED_STORE_ALL, ADST_SCHED_UNIFORM, ADST_SCHED_BINOMIAL = 0, 1, 2, 3
 ADST_LOSS_HALF_SQ, ADST_LOSS_DOT_W, ADST_LOSS_HALF_SQ_DIFF, ADST_LOSS_SEED = 0, 1, 2, 3
-ADST_FORCE_TAPE, ADST_TRACE = 0x1, 0x2
-ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ = 0, 1, 2
+ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE = 0x1, 0x2, 0x4
+ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2 = 0, 1, 2, 3, 4
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
 EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_status_str",
@@ -43,7 +43,8 @@ class adst_plan_info(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int32), ("sched", ctypes.c_int32), ("slots", ctypes.c_int32),
                 ("needs_state", ctypes.c_int32), ("fwd_steps_total", ctypes.c_int64),
                 ("recompute_steps", ctypes.c_int64), ("adj_steps", ctypes.c_int64),
-                ("n_actions", ctypes.c_int64), ("state_bytes", ctypes.c_uint64),
+                ("n_actions", ctypes.c_int64), ("fwd_launches", ctypes.c_int64),
+                ("adj_launches", ctypes.c_int64), ("state_bytes", ctypes.c_uint64),
                 ("budget_bytes", ctypes.c_uint64), ("slot_bytes_peak", ctypes.c_uint64),
                 ("workspace_bytes", ctypes.c_uint64), ("fwd_workspace_bytes", ctypes.c_uint64),
                 ("alg_bytes", ctypes.c_uint64), ("ms_fwd_sweep", ctypes.c_float),

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "adst.h"
@@ -40,6 +41,7 @@ struct Checked {
   uint64_t state_bytes = 0;
   bool needs_state = false;
   bool trace = false;
+  bool fuse_fwd = false, fuse_adj = false;
 };
 
 adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* out) {
@@ -48,7 +50,7 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
     return fail(ADST_ERR_ARG, "unknown kind " + std::to_string(p->kind));
   if (p->dtype != ADST_F64 && p->dtype != ADST_F32)
     return fail(ADST_ERR_ARG, "unknown dtype " + std::to_string(p->dtype));
-  if (p->flags & ~(ADST_FORCE_TAPE | ADST_TRACE))
+  if (p->flags & ~(ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE))
     return fail(ADST_ERR_ARG, "unknown flag bits");
   for (int d = 0; d < 3; ++d)
     if (p->n[d] < 1) return fail(ADST_ERR_ARG, "every extent n[i] must be >= 1");
@@ -58,13 +60,13 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
   if (n >= (int64_t(1) << 31)) return fail(ADST_ERR_ARG, "grid must have fewer than 2^31 points");
   if ((p->kind == ADST_JACOBI2D5 || p->kind == ADST_VARDIFF2D9) && p->n[2] != 1)
     return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
-  // Every launch covers the grid with workgroups of 256 work-items: 256 x 4
-  // (or x 8) tiles for the 2-D kinds, 64 x 8 x 32 columns for the 3-D kind.
-  // The work-item count must fit the 32-bit dispatch grid.
+  // Every launch covers the grid with workgroups of 256 work-items: tiles of
+  // 252 or 256 columns by 4 or 8 rows for the 2-D kinds, 64 x 8 x 32 columns
+  // for the 3-D kind. The work-item count must fit the 32-bit dispatch grid.
   const int64_t tiles =
       p->kind == ADST_ALLENCAHN3D7
           ? ((p->n[0] + 63) / 64) * ((p->n[1] + 7) / 8) * ((p->n[2] + 31) / 32)
-          : ((p->n[0] + 255) / 256) * ((p->n[1] + 3) / 4);
+          : ((p->n[0] + 251) / 252) * ((p->n[1] + 3) / 4);
   if ((tiles + 8) * 256 >= (int64_t(1) << 32))
     return fail(ADST_ERR_UNSUPPORTED, "grid too thin in x/y for the tile shape");
   if (want_dcoeff && p->kind != ADST_VARDIFF2D9)
@@ -77,6 +79,9 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
                                 (p->kind == ADST_VARDIFF2D9 && want_dcoeff);
   out->needs_state = kind_reads_state || (p->flags & ADST_FORCE_TAPE);
   out->trace = (p->flags & ADST_TRACE) != 0;
+  const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
+  out->fuse_fwd = fuse && has_forward2(p->kind);
+  out->fuse_adj = fuse && has_adjoint2(p->kind);
   return ADST_OK;
 }
 
@@ -137,14 +142,17 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
   info->recompute_steps = plan.fwd_total - plan.steps;
   info->adj_steps = plan.adj_total;
   info->n_actions = (int64_t)plan.acts.size();
+  info->fwd_launches = plan.fwd_launches;
+  info->adj_launches = plan.adj_launches;
   info->state_bytes = c.state_bytes;
   info->budget_bytes = budget;
   info->slot_bytes_peak = uint64_t(plan.slots) * c.state_bytes;
   info->workspace_bytes = L.total;
   info->fwd_workspace_bytes = plan.steps >= 2 ? c.state_bytes : 0;
+  // A fused launch moves its inputs and outputs once for two steps.
   const uint64_t n = uint64_t(c.npoints);
-  uint64_t adj_total = plan.adj_total > 0 ? ab1 + uint64_t(plan.adj_total - 1) * ab : 0;
-  info->alg_bytes = n * (uint64_t(plan.fwd_total) * fb + adj_total + sb);
+  uint64_t adj_total = plan.adj_launches > 0 ? ab1 + uint64_t(plan.adj_launches - 1) * ab : 0;
+  info->alg_bytes = n * (uint64_t(plan.fwd_launches) * fb + adj_total + sb);
 }
 
 adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
@@ -154,7 +162,7 @@ adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, 
   if (steps < 0) return fail(ADST_ERR_ARG, "steps must be >= 0");
   const int64_t slots_avail = (int64_t)std::min<uint64_t>(budget / c->state_bytes, INT32_MAX);
   std::string err;
-  st = build_plan(steps, slots_avail, sched, c->needs_state, plan, &err);
+  st = build_plan(steps, slots_avail, sched, c->needs_state, c->fuse_fwd, c->fuse_adj, plan, &err);
   if (st != ADST_OK) return fail(st, err);
   return ADST_OK;
 }
@@ -322,14 +330,23 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
     g_last_error.clear();
     return ADST_OK;
   }
-  // x_t lands in xT when (T - t) is even, so x_T ends in xT.
+  // One single step first when the count is odd, then fused pairs where the
+  // kind has them; launches alternate between xT and ws so that the last one
+  // writes xT.
+  const bool pairs = c.fuse_fwd;
+  const int32_t n_launch = pairs ? steps / 2 + steps % 2 : steps;
   const void* cur = x0;
-  for (int32_t t = 1; t <= steps; ++t) {
-    void* dst = ((steps - t) % 2 == 0) ? xT : ws;
-    e = launch_forward(c.shape, cur, coeff, dst, stream);
+  int32_t done = 0;
+  for (int32_t k = 0; k < n_launch; ++k) {
+    void* dst = ((n_launch - 1 - k) % 2 == 0) ? xT : ws;
+    const bool two = pairs && !(k == 0 && steps % 2 == 1);
+    e = two ? launch_forward2(c.shape, cur, coeff, dst, stream)
+            : launch_forward(c.shape, cur, coeff, dst, stream);
     if (e != hipSuccess) return hip_fail(e, "forward step");
+    done += two ? 2 : 1;
     cur = dst;
   }
+  if (done != steps) return fail(ADST_ERR_ARG, "internal: forward launch count");
   g_last_error.clear();
   return ADST_OK;
 }
@@ -367,17 +384,21 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   if (info) fill_info(c, plan, mem_budget_bytes, want_dk != 0, loss, info);
 
   // ---- interpret the plan
+  // The adjoint ping-pongs between dx0 and the workspace buffer G, one swap
+  // per adjoint launch; g_T starts where the last launch leaves g_0 in dx0.
   char* wsb = static_cast<char*>(ws);
   double* partials = reinterpret_cast<double*>(wsb);
   double* loss_out = loss_dev ? loss_dev : reinterpret_cast<double*>(wsb + kLossOffset);
-  void* gbuf_odd = wsb + L.g;
-  auto gbuf = [&](int32_t t) -> void* { return (t % 2 == 0) ? dx0 : gbuf_odd; };
+  void* gws = wsb + L.g;
+  void* gcur = (plan.adj_launches % 2 == 0) ? dx0 : gws;
+  void* gnext = (gcur == dx0) ? gws : dx0;
+  void* const g_T = gcur;
   auto buffer = [&](int32_t id) -> void* {
     switch (id) {
       case ADST_BUF_X0: return const_cast<void*>(x0);
       case ADST_BUF_W0: return wsb + L.w0;
       case ADST_BUF_W1: return wsb + L.w1;
-      case ADST_BUF_XT: return xT ? xT : gbuf(steps);
+      case ADST_BUF_XT: return xT ? xT : g_T;
       default: return wsb + L.slot0 + uint64_t(id - ADST_BUF_SLOT0) * L.state_stride;
     }
   };
@@ -386,26 +407,42 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   bool seeded = false;
   hipError_t e = hipSuccess;
   for (const adst_action& a : plan.acts) {
-    const Tracer::Cat cat = a.op == ADST_OP_FWD    ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
+    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2;
+    const Tracer::Cat cat = fwd_op               ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
                             : a.op == ADST_OP_SEED ? Tracer::SEED
                                                    : Tracer::ADJ;
     if ((e = tr.before(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
-    if (a.op == ADST_OP_FWD) {
-      e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
-    } else if (a.op == ADST_OP_SEED) {
-      const void* xsrc = buffer(a.src);
-      void* xcopy = (steps == 0 && xT) ? xT : nullptr;
-      e = launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, gbuf(steps), xcopy,
-                      partials, stream);
-      if (e == hipSuccess)
-        e = launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
-      if (e == hipSuccess && steps == 0 && dcoeff)
-        e = launch_fill_zero(dcoeff, (int64_t)S, stream);
-      seeded = true;
-    } else {
-      const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
-      e = launch_adjoint(c.shape, xs, coeff, gbuf(a.t), gbuf(a.t - 1), dcoeff, a.t == steps,
-                         stream);
+    switch (a.op) {
+      case ADST_OP_FWD:
+        e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+        break;
+      case ADST_OP_FWD2:
+        e = launch_forward2(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+        break;
+      case ADST_OP_SEED: {
+        const void* xsrc = buffer(a.src);
+        void* xcopy = (steps == 0 && xT) ? xT : nullptr;
+        e = launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, g_T, xcopy, partials,
+                        stream);
+        if (e == hipSuccess)
+          e = launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
+        if (e == hipSuccess && steps == 0 && dcoeff)
+          e = launch_fill_zero(dcoeff, (int64_t)S, stream);
+        seeded = true;
+        break;
+      }
+      case ADST_OP_ADJ: {
+        const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
+        e = launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps, stream);
+        std::swap(gcur, gnext);
+        break;
+      }
+      case ADST_OP_ADJ2:
+        e = launch_adjoint2(c.shape, gcur, gnext, stream);
+        std::swap(gcur, gnext);
+        break;
+      default:
+        e = hipErrorInvalidValue;
     }
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
   }

@@ -20,6 +20,18 @@ struct StepShape {
 hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void* y,
                           hipStream_t stream);
 
+// Kinds with a fused two-step kernel (temporal blocking of depth 2).
+bool has_forward2(int32_t kind);
+bool has_adjoint2(int32_t kind);  // state-free adjoints only
+
+// x_t = F(F(x_{t-2})): two forward steps, the intermediate kept on chip.
+hipError_t launch_forward2(const StepShape& s, const void* x, const void* K, void* y,
+                           hipStream_t stream);
+
+// g_{t-2} = J_{t-1}^T J_t^T g_t for a state-free adjoint.
+hipError_t launch_adjoint2(const StepShape& s, const void* g_next, void* g_prev,
+                           hipStream_t stream);
+
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
 // reads no state and dK is not asked for). dK (nullable) is accumulated:
 // dK = (dk_first ? 0 : dK) + contribution of step t.

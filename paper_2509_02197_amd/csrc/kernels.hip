@@ -40,31 +40,26 @@ __device__ inline int xcd_tile(int ntiles) {
 inline unsigned xcd_grid(int64_t ntiles) { return (unsigned)(8 * ((ntiles + 7) / 8)); }
 
 // ------------------------------------------------------- 2-D LDS tiles
-// A workgroup of TW threads owns a TW x TR tile of the output; one thread per
-// column, TR rows each. It first stages rows j0-1 .. j0+TR of every input
-// array, columns i0-V .. i0+TW+V-1 (V elements = 16 bytes), in LDS with all
-// loads in flight at once (16-byte vector loads when rows are 16-byte
-// aligned), then computes from LDS. Cells outside the grid read 0 and are
-// never used by a formula that drops them.
-template <class R, int TW, int TR>
-struct Tile2 {
-  static constexpr int V = 16 / sizeof(R);
-  static constexpr int LW = TW + 2 * V;  // LDS row length
-  static constexpr int LR = TR + 2;      // LDS rows
-  static constexpr int CH = LW / V;      // 16-byte chunks per LDS row
-};
+// A workgroup owns a tile of the output: one thread per column, several
+// rows each. It first stages the tile's input rows and columns, plus a halo,
+// in LDS with all loads in flight at once (16-byte vector loads when rows are
+// 16-byte aligned), then computes from LDS. Cells outside the grid read 0;
+// no formula evaluated at an in-grid point uses them.
 
-template <class R, int TW, int TR>
-__device__ inline void stage_tile(R* lds, const R* __restrict__ a, int i0, int j0, int nx, int ny,
-                                  bool vec) {
-  using G = Tile2<R, TW, TR>;
-  constexpr int V = G::V;
+// Stage LR x LW elements of a, starting at global row row0 and column col0
+// (col0 a multiple of the vector width), into lds (row stride LW).
+template <class R, int NT, int LR, int LW>
+__device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int row0, int nx,
+                                  int ny, bool vec) {
+  constexpr int V = 16 / sizeof(R);
+  constexpr int CH = LW / V;
+  static_assert(LW % V == 0, "LDS rows hold whole 16-byte chunks");
   typedef R vec_t __attribute__((ext_vector_type(V)));
-  for (int q = threadIdx.x; q < G::LR * G::CH; q += TW) {
-    const int rr = q / G::CH, ch = q - rr * G::CH;
-    const int jj = j0 - 1 + rr;
-    const int ii = i0 - V + ch * V;
-    R* dst = lds + rr * G::LW + ch * V;
+  for (int q = threadIdx.x; q < LR * CH; q += NT) {
+    const int rr = q / CH, ch = q - rr * CH;
+    const int jj = row0 + rr;
+    const int ii = col0 + ch * V;
+    R* dst = lds + rr * LW + ch * V;
     if (jj < 0 || jj >= ny) {
 #pragma unroll
       for (int e = 0; e < V; ++e) dst[e] = R(0);
@@ -82,87 +77,225 @@ __device__ inline void stage_tile(R* lds, const R* __restrict__ a, int i0, int j
   }
 }
 
+// Point updates read from an LDS array with row stride LW; q is the flat
+// index of the point, (i, j) its grid coordinates. Single-step and fused
+// kernels call the same functions, so a fused launch is bit-identical to two
+// single launches.
+
+// w*((((v[c]+v[W])+v[E])+v[S])+v[N]): the forward step at an interior point,
+// and also the adjoint step at a point whose neighbours are all interior.
+template <class R, int LW>
+__device__ inline R jacobi_avg_at(const R* s, int q, R w) {
+  R sum = s[q];
+  sum += s[q - 1];
+  sum += s[q + 1];
+  sum += s[q - LW];
+  sum += s[q + LW];
+  return w * sum;
+}
+
+// Jacobi forward: interior x'[c] = w*((((x[c]+x[W])+x[E])+x[S])+x[N]);
+// the ring is copied.
+template <class R, int LW>
+__device__ inline R jacobi_fwd_at(const R* s, int q, int i, int j, int nx, int ny, R w) {
+  if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) return jacobi_avg_at<R, LW>(s, q, w);
+  return s[q];
+}
+
+// Jacobi adjoint (gather): with gi(p) = g[p] on interior p and 0 elsewhere,
+//   interior m: g'[m] = w * (g[m] + sum_{p in nbr(m)} gi(p))
+//   ring m:     g'[m] = g[m] + w * sum_{p in nbr(m)} gi(p)
+// Points two or more cells from the edge see only interior neighbours.
+template <class R, int LW>
+__device__ inline R jacobi_adj_at(const R* s, int q, int i, int j, int nx, int ny, R w) {
+  if (i >= 2 && i <= nx - 3 && j >= 2 && j <= ny - 3) return jacobi_avg_at<R, LW>(s, q, w);
+  const R c = s[q];
+  auto interior = [&](int a, int b) { return a > 0 && a < nx - 1 && b > 0 && b < ny - 1; };
+  R sum = interior(i - 1, j) ? s[q - 1] : R(0);
+  sum += interior(i + 1, j) ? s[q + 1] : R(0);
+  sum += interior(i, j - 1) ? s[q - LW] : R(0);
+  sum += interior(i, j + 1) ? s[q + LW] : R(0);
+  return interior(i, j) ? w * (c + sum) : c + w * sum;
+}
+
+// Variable-coefficient diffusion. Neighbour order (-1,0),(+1,0),(0,-1),
+// (0,+1),(-1,-1),(+1,-1),(-1,+1),(+1,+1); the first four carry weight ca
+// (1/3), the last four cd (1/12).
+constexpr int kNbrDx[8] = {-1, 1, 0, 0, -1, 1, -1, 1};
+constexpr int kNbrDy[8] = {0, 0, -1, 1, -1, -1, 1, 1};
+
+// Forward: acc = sum over in-grid n of (c_n*(K[c]+K[n]))*(x[n]-x[c]),
+// x' = x[c] + dt*acc.
+template <class R, int LW>
+__device__ inline R vardiff_fwd_at(const R* sx, const R* sk, int q, int i, int j, int nx, int ny,
+                                   R dt, R ca, R cd) {
+  const R xc = sx[q], Kc = sk[q];
+  R acc = R(0);
+  if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      const int m = q + kNbrDy[n] * LW + kNbrDx[n];
+      acc += ((n < 4 ? ca : cd) * (Kc + sk[m])) * (sx[m] - xc);
+    }
+  } else {
+#pragma unroll
+    for (int n = 0; n < 8; ++n) {
+      const int a = i + kNbrDx[n], b = j + kNbrDy[n];
+      if (a < 0 || a >= nx || b < 0 || b >= ny) continue;
+      const int m = q + kNbrDy[n] * LW + kNbrDx[n];
+      acc += ((n < 4 ? ca : cd) * (Kc + sk[m])) * (sx[m] - xc);
+    }
+  }
+  return xc + dt * acc;
+}
+
+// Single-step tiles: TW columns x TR rows, halo one cell (staged as one
+// 16-byte chunk on each side).
+template <class R, int TW, int TR>
+struct Tile2 {
+  static constexpr int V = 16 / sizeof(R);
+  static constexpr int LW = TW + 2 * V;  // LDS row length
+  static constexpr int LR = TR + 2;      // LDS rows
+};
+
+// Fused-pair tiles: kX2TW output columns, TR rows, halo two cells. The first
+// step is evaluated on kX2TW + 2 columns and TR + 2 rows, so 254 columns fit
+// the 256 threads one each and no wavefront does double work.
+constexpr int kX2TW = 252, kX2Threads = 256, kX2TR = 4;
+template <class R, int TR>
+struct Tile2x2 {
+  static constexpr int V = 16 / sizeof(R);
+  static constexpr int PADL = ((2 + V - 1) / V) * V;  // left halo, whole chunks
+  static constexpr int LW = PADL + ((kX2TW + 2 + V - 1) / V) * V;
+  static constexpr int LR = TR + 4;
+};
+
 // ------------------------------------------------------------- Jacobi 2-D
 constexpr int kJacTW = 256, kJacTR = 8;
 
-// Forward: interior x'[c] = w*((((x[c]+x[W])+x[E])+x[S])+x[N]); ring copied.
+// Every point of rows [ja, jb] x columns [ia, ib] takes the plain average:
+// interior for the forward, two cells from the edge for the adjoint.
+template <bool ADJ>
+__device__ inline bool jacobi_all_avg(int ia, int ib, int ja, int jb, int nx, int ny) {
+  const int m = ADJ ? 2 : 1;
+  return ia >= m && ib <= nx - 1 - m && ja >= m && jb <= ny - 1 - m;
+}
+
+// Forward (ADJ = false) or adjoint (ADJ = true) Jacobi step on one tile.
+template <class R, bool ADJ>
+__device__ inline void jacobi_tile(const R* __restrict__ x, R* __restrict__ y, int nx, int ny,
+                                   int tiles_x, int ntiles, int vec, R w) {
+  using G = Tile2<R, kJacTW, kJacTR>;
+  __shared__ R s[G::LR * G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacTR;
+  stage_rows<R, kJacTW, G::LR, G::LW>(s, x, i0 - G::V, j0 - 1, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  if (i >= nx) return;
+  const int cx = G::V + (int)threadIdx.x;
+  if (jacobi_all_avg<ADJ>(i0, i0 + kJacTW - 1, j0, j0 + kJacTR - 1, nx, ny)) {
+#pragma unroll
+    for (int r = 0; r < kJacTR; ++r)
+      y[(j0 + r) * nx + i] = jacobi_avg_at<R, G::LW>(s, (r + 1) * G::LW + cx, w);
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < kJacTR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const int q = (r + 1) * G::LW + cx;
+    y[j * nx + i] = ADJ ? jacobi_adj_at<R, G::LW>(s, q, i, j, nx, ny, w)
+                        : jacobi_fwd_at<R, G::LW>(s, q, i, j, nx, ny, w);
+  }
+}
+
+// Two Jacobi steps (forward or adjoint) on one tile in one launch.
+template <class R, bool ADJ>
+__device__ inline void jacobi_tile_x2(const R* __restrict__ x, R* __restrict__ y, int nx, int ny,
+                                      int tiles_x, int ntiles, int vec, R w) {
+  using G = Tile2x2<R, kX2TR>;
+  __shared__ R s[G::LR * G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kX2TW, j0 = (b / tiles_x) * kX2TR;
+  stage_rows<R, kX2Threads, G::LR, G::LW>(s, x, i0 - G::PADL, j0 - 2, nx, ny, vec);
+  // the first step covers the tile plus one cell; whole tiles away from the
+  // edges take the plain average everywhere (workgroup-uniform)
+  const bool avg = jacobi_all_avg<ADJ>(i0 - 1, i0 + kX2TW, j0 - 1, j0 + kX2TR, nx, ny);
+  __syncthreads();
+  const int t = threadIdx.x;
+  // first step: LDS rows 1..TR+2, LDS columns PADL-1 .. PADL+kX2TW
+  const int c = G::PADL - 1 + t;
+  const bool act = t < kX2TW + 2;
+  const int ic = i0 - 1 + t;
+  R v[kX2TR + 2];
+  if (act) {
+    if (avg) {
+#pragma unroll
+      for (int r = 1; r <= kX2TR + 2; ++r) v[r - 1] = jacobi_avg_at<R, G::LW>(s, r * G::LW + c, w);
+    } else {
+#pragma unroll
+      for (int r = 1; r <= kX2TR + 2; ++r) {
+        const int q = r * G::LW + c;
+        const int j = j0 - 2 + r;
+        v[r - 1] = ADJ ? jacobi_adj_at<R, G::LW>(s, q, ic, j, nx, ny, w)
+                       : jacobi_fwd_at<R, G::LW>(s, q, ic, j, nx, ny, w);
+      }
+    }
+  }
+  __syncthreads();
+  if (act) {
+#pragma unroll
+    for (int r = 1; r <= kX2TR + 2; ++r) s[r * G::LW + c] = v[r - 1];
+  }
+  __syncthreads();
+  // second step on the output tile
+  const int i = i0 + t;
+  if (t >= kX2TW || i >= nx) return;
+  const int cx = G::PADL + t;
+  if (avg) {
+#pragma unroll
+    for (int r = 0; r < kX2TR; ++r)
+      y[(j0 + r) * nx + i] = jacobi_avg_at<R, G::LW>(s, (r + 2) * G::LW + cx, w);
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < kX2TR; ++r) {
+    const int j = j0 + r;
+    if (j >= ny) break;
+    const int q = (r + 2) * G::LW + cx;
+    y[j * nx + i] = ADJ ? jacobi_adj_at<R, G::LW>(s, q, i, j, nx, ny, w)
+                        : jacobi_fwd_at<R, G::LW>(s, q, i, j, nx, ny, w);
+  }
+}
+
 template <class R>
 __global__ __launch_bounds__(kJacTW) void fwd_jacobi2d5(const R* __restrict__ x,
                                                         R* __restrict__ y, int nx, int ny,
                                                         int tiles_x, int ntiles, int vec, R w) {
-  using G = Tile2<R, kJacTW, kJacTR>;
-  __shared__ R s[G::LR][G::LW];
-  const int b = xcd_tile(ntiles);
-  if (b >= ntiles) return;
-  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacTR;
-  stage_tile<R, kJacTW, kJacTR>(&s[0][0], x, i0, j0, nx, ny, vec);
-  __syncthreads();
-  const int i = i0 + (int)threadIdx.x;
-  if (i >= nx) return;
-  const int cx = G::V + (int)threadIdx.x;
-  const bool xin = i > 0 && i < nx - 1;
-#pragma unroll
-  for (int r = 0; r < kJacTR; ++r) {
-    const int j = j0 + r;
-    if (j >= ny) break;
-    const R c = s[r + 1][cx];
-    R out;
-    if (xin && j > 0 && j < ny - 1) {
-      R sum = c;
-      sum += s[r + 1][cx - 1];
-      sum += s[r + 1][cx + 1];
-      sum += s[r][cx];
-      sum += s[r + 2][cx];
-      out = w * sum;
-    } else {
-      out = c;
-    }
-    y[j * nx + i] = out;
-  }
+  jacobi_tile<R, false>(x, y, nx, ny, tiles_x, ntiles, vec, w);
 }
-
-// Adjoint (gather): with gi(q) = g[q] on interior q and 0 elsewhere,
-//   interior m: g'[m] = w * (g[m] + sum_{q in nbr(m)} gi(q))
-//   ring m:     g'[m] = g[m] + w * sum_{q in nbr(m)} gi(q)
-// Points two or more cells from the edge see only interior neighbours.
 template <class R>
 __global__ __launch_bounds__(kJacTW) void adj_jacobi2d5(const R* __restrict__ g,
                                                         R* __restrict__ gp, int nx, int ny,
                                                         int tiles_x, int ntiles, int vec, R w) {
-  using G = Tile2<R, kJacTW, kJacTR>;
-  __shared__ R s[G::LR][G::LW];
-  const int b = xcd_tile(ntiles);
-  if (b >= ntiles) return;
-  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacTR;
-  stage_tile<R, kJacTW, kJacTR>(&s[0][0], g, i0, j0, nx, ny, vec);
-  __syncthreads();
-  const int i = i0 + (int)threadIdx.x;
-  if (i >= nx) return;
-  const int cx = G::V + (int)threadIdx.x;
-  const bool deep_cols = i >= 2 && i <= nx - 3;
-  auto interior = [&](int a, int bb) { return a > 0 && a < nx - 1 && bb > 0 && bb < ny - 1; };
-#pragma unroll
-  for (int r = 0; r < kJacTR; ++r) {
-    const int j = j0 + r;
-    if (j >= ny) break;
-    const R c = s[r + 1][cx];
-    R out;
-    if (deep_cols && j >= 2 && j <= ny - 3) {
-      R sum = c;
-      sum += s[r + 1][cx - 1];
-      sum += s[r + 1][cx + 1];
-      sum += s[r][cx];
-      sum += s[r + 2][cx];
-      out = w * sum;
-    } else {
-      R sum = interior(i - 1, j) ? s[r + 1][cx - 1] : R(0);
-      sum += interior(i + 1, j) ? s[r + 1][cx + 1] : R(0);
-      sum += interior(i, j - 1) ? s[r][cx] : R(0);
-      sum += interior(i, j + 1) ? s[r + 2][cx] : R(0);
-      out = interior(i, j) ? w * (c + sum) : c + w * sum;
-    }
-    gp[j * nx + i] = out;
-  }
+  jacobi_tile<R, true>(g, gp, nx, ny, tiles_x, ntiles, vec, w);
+}
+template <class R>
+__global__ __launch_bounds__(kX2Threads) void fwd_jacobi2d5_x2(const R* __restrict__ x,
+                                                               R* __restrict__ y, int nx, int ny,
+                                                               int tiles_x, int ntiles, int vec,
+                                                               R w) {
+  jacobi_tile_x2<R, false>(x, y, nx, ny, tiles_x, ntiles, vec, w);
+}
+template <class R>
+__global__ __launch_bounds__(kX2Threads) void adj_jacobi2d5_x2(const R* __restrict__ g,
+                                                               R* __restrict__ gp, int nx, int ny,
+                                                               int tiles_x, int ntiles, int vec,
+                                                               R w) {
+  jacobi_tile_x2<R, true>(g, gp, nx, ny, tiles_x, ntiles, vec, w);
 }
 
 // ------------------------------------------------------- Allen-Cahn 3-D
@@ -332,14 +465,8 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
 }
 
 // ------------------------------------------ variable-coefficient diffusion 2-D
-// Neighbour order (-1,0),(+1,0),(0,-1),(0,+1),(-1,-1),(+1,-1),(-1,+1),(+1,+1);
-// the first four carry weight ca (1/3), the last four cd (1/12).
-constexpr int kNbrDx[8] = {-1, 1, 0, 0, -1, 1, -1, 1};
-constexpr int kNbrDy[8] = {0, 0, -1, 1, -1, -1, 1, 1};
 constexpr int kVdTW = 256, kVdTR = 8, kVdAdjTR = 4;
 
-// Forward: acc = sum over in-grid n of (c_n*(K[c]+K[n]))*(x[n]-x[c]),
-// x' = x[c] + dt*acc.
 template <class R>
 __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
                                                         const R* __restrict__ K,
@@ -347,40 +474,22 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
                                                         int tiles_x, int ntiles, int vec, R dt,
                                                         R ca, R cd) {
   using G = Tile2<R, kVdTW, kVdTR>;
-  __shared__ R sx[G::LR][G::LW];
-  __shared__ R sk[G::LR][G::LW];
+  __shared__ R sx[G::LR * G::LW];
+  __shared__ R sk[G::LR * G::LW];
   const int b = xcd_tile(ntiles);
   if (b >= ntiles) return;
   const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * kVdTR;
-  stage_tile<R, kVdTW, kVdTR>(&sx[0][0], x, i0, j0, nx, ny, vec);
-  stage_tile<R, kVdTW, kVdTR>(&sk[0][0], K, i0, j0, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, G::LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, G::LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
   __syncthreads();
   const int i = i0 + (int)threadIdx.x;
   if (i >= nx) return;
   const int cx = G::V + (int)threadIdx.x;
-  const bool xin = i > 0 && i < nx - 1;
 #pragma unroll 4
   for (int r = 0; r < kVdTR; ++r) {
     const int j = j0 + r;
     if (j >= ny) break;
-    const R xc = sx[r + 1][cx], Kc = sk[r + 1][cx];
-    R acc = R(0);
-    if (xin && j > 0 && j < ny - 1) {
-#pragma unroll
-      for (int n = 0; n < 8; ++n) {
-        const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
-        acc += ((n < 4 ? ca : cd) * (Kc + sk[rr][cc])) * (sx[rr][cc] - xc);
-      }
-    } else {
-#pragma unroll
-      for (int n = 0; n < 8; ++n) {
-        const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
-        if (a < 0 || a >= nx || bb < 0 || bb >= ny) continue;
-        const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
-        acc += ((n < 4 ? ca : cd) * (Kc + sk[rr][cc])) * (sx[rr][cc] - xc);
-      }
-    }
-    y[j * nx + i] = xc + dt * acc;
+    y[j * nx + i] = vardiff_fwd_at<R, G::LW>(sx, sk, (r + 1) * G::LW + cx, i, j, nx, ny, dt, ca, cd);
   }
 }
 
@@ -397,15 +506,16 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
                                                         int tiles_x, int ntiles, int vec, R dt,
                                                         R ca, R cd) {
   using G = Tile2<R, kVdTW, TR>;
-  __shared__ R sg[G::LR][G::LW];
-  __shared__ R sk[G::LR][G::LW];
-  __shared__ R sx[WANT_DK ? G::LR : 1][WANT_DK ? G::LW : 1];
+  constexpr int LW = G::LW;
+  __shared__ R sg[G::LR * LW];
+  __shared__ R sk[G::LR * LW];
+  __shared__ R sx[WANT_DK ? G::LR * LW : 1];
   const int b = xcd_tile(ntiles);
   if (b >= ntiles) return;
   const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * TR;
-  stage_tile<R, kVdTW, TR>(&sg[0][0], g, i0, j0, nx, ny, vec);
-  stage_tile<R, kVdTW, TR>(&sk[0][0], K, i0, j0, nx, ny, vec);
-  if (WANT_DK) stage_tile<R, kVdTW, TR>(&sx[0][0], x, i0, j0, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
+  if (WANT_DK) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
   __syncthreads();
   const int i = i0 + (int)threadIdx.x;
   if (i >= nx) return;
@@ -415,23 +525,24 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   for (int r = 0; r < TR; ++r) {
     const int j = j0 + r;
     if (j >= ny) break;
-    const int c = j * nx + i;
-    const R gc = sg[r + 1][cx], Kc = sk[r + 1][cx];
-    const R xc = WANT_DK ? sx[r + 1][cx] : R(0);
+    const int q = (r + 1) * LW + cx;
+    const R gc = sg[q], Kc = sk[q];
+    const R xc = WANT_DK ? sx[q] : R(0);
     R ag = R(0), ak = R(0);
     const bool inner = xin && j > 0 && j < ny - 1;
 #pragma unroll
     for (int n = 0; n < 8; ++n) {
       const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
       if (!inner && (a < 0 || a >= nx || bb < 0 || bb >= ny)) continue;
-      const int rr = r + 1 + kNbrDy[n], cc = cx + kNbrDx[n];
+      const int m = q + kNbrDy[n] * LW + kNbrDx[n];
       const R cn = n < 4 ? ca : cd;
-      const R gn = sg[rr][cc];
-      ag += (cn * (Kc + sk[rr][cc])) * (gn - gc);
-      if (WANT_DK) ak += (cn * (sx[rr][cc] - xc)) * (gc - gn);
+      const R gn = sg[m];
+      ag += (cn * (Kc + sk[m])) * (gn - gc);
+      if (WANT_DK) ak += (cn * (sx[m] - xc)) * (gc - gn);
     }
-    gp[c] = gc + dt * ag;
-    if (WANT_DK) dK[c] = (dk_first ? R(0) : dK[c]) + dt * ak;
+    const int o = j * nx + i;
+    gp[o] = gc + dt * ag;
+    if (WANT_DK) dK[o] = (dk_first ? R(0) : dK[o]) + dt * ak;
   }
 }
 
@@ -524,19 +635,26 @@ int vec_ok(int nx, const void* a, const void* b = nullptr, const void* c = nullp
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 template <class R>
-hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv,
+hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv, bool two,
                      hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
   const R* K = static_cast<const R*>(Kv);
   R* y = static_cast<R*>(yv);
   switch (s.kind) {
     case ADST_JACOBI2D5: {
-      const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
-      fwd_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
-          x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
+      if (two) {
+        const int tx = cdiv(s.nx, kX2TW), nt = tx * cdiv(s.ny, kX2TR);
+        fwd_jacobi2d5_x2<R><<<dim3(xcd_grid(nt)), dim3(kX2Threads), 0, st>>>(
+            x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
+      } else {
+        const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
+        fwd_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+            x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
+      }
       break;
     }
     case ADST_ALLENCAHN3D7: {
+      if (two) return hipErrorInvalidValue;
       const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
       const int nt = tx * ty * cdiv(s.nz, kAcZC);
       fwd_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
@@ -544,6 +662,7 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       break;
     }
     case ADST_VARDIFF2D9: {
+      if (two) return hipErrorInvalidValue;
       const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
       fwd_vardiff2d9<R><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
           x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
@@ -602,6 +721,17 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
 }
 
 template <class R>
+hipError_t adjoint2_t(const StepShape& s, const void* gv, void* gpv, hipStream_t st) {
+  const R* g = static_cast<const R*>(gv);
+  R* gp = static_cast<R*>(gpv);
+  if (s.kind != ADST_JACOBI2D5) return hipErrorInvalidValue;
+  const int tx = cdiv(s.nx, kX2TW), nt = tx * cdiv(s.ny, kX2TR);
+  adj_jacobi2d5_x2<R><<<dim3(xcd_grid(nt)), dim3(kX2Threads), 0, st>>>(
+      g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
+  return hipGetLastError();
+}
+
+template <class R>
 hipError_t seed_t(int32_t loss, int64_t n, const void* xv, const void* auxv, void* gv,
                   void* xcopyv, double* partials, hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
@@ -631,8 +761,23 @@ hipError_t seed_t(int32_t loss, int64_t n, const void* xv, const void* auxv, voi
 
 hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void* y,
                           hipStream_t stream) {
-  return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, stream)
-                             : forward_t<float>(s, x, K, y, stream);
+  return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, false, stream)
+                             : forward_t<float>(s, x, K, y, false, stream);
+}
+
+bool has_forward2(int32_t kind) { return kind == ADST_JACOBI2D5; }
+bool has_adjoint2(int32_t kind) { return kind == ADST_JACOBI2D5; }
+
+hipError_t launch_forward2(const StepShape& s, const void* x, const void* K, void* y,
+                           hipStream_t stream) {
+  return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, true, stream)
+                             : forward_t<float>(s, x, K, y, true, stream);
+}
+
+hipError_t launch_adjoint2(const StepShape& s, const void* g_next, void* g_prev,
+                           hipStream_t stream) {
+  return s.dtype == ADST_F64 ? adjoint2_t<double>(s, g_next, g_prev, stream)
+                             : adjoint2_t<float>(s, g_next, g_prev, stream);
 }
 
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,

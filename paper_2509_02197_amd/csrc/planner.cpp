@@ -55,11 +55,12 @@ int64_t best_split(int64_t l, int64_t c) {
 
 class Builder {
  public:
-  Builder(int32_t T, bool needs_state) : T_(T), needs_state_(needs_state) {}
+  Builder(int32_t T, bool needs_state, bool fuse_fwd, bool fuse_adj)
+      : T_(T), needs_state_(needs_state), fuse_fwd_(fuse_fwd), fuse_adj_(fuse_adj) {}
 
   std::vector<adst_action> acts;
   int32_t slots_used = 0;
-  int64_t nfwd = 0;
+  int64_t nfwd = 0, fwd_launches = 0, adj_launches = 0;
 
   int32_t alloc_slot() {
     if (!free_.empty()) {
@@ -74,6 +75,13 @@ class Builder {
   void fwd(int32_t t, int32_t src, int32_t dst) {
     acts.push_back({ADST_OP_FWD, t, src, dst});
     ++nfwd;
+    ++fwd_launches;
+  }
+  // Steps t-1 and t in one launch; x_{t-1} is never materialised.
+  void fwd2(int32_t t, int32_t src, int32_t dst) {
+    acts.push_back({ADST_OP_FWD2, t, src, dst});
+    nfwd += 2;
+    ++fwd_launches;
   }
 
   static int32_t other_work(int32_t cur) {
@@ -82,12 +90,19 @@ class Builder {
 
   // From buffer b holding x_i, compute x_{i+1}..x_j through the work buffers;
   // the last step writes final_dst instead when one is given. Returns the
-  // buffer holding x_j.
+  // buffer holding x_j. The intermediate states are read by nothing else, so
+  // with fusion on they are computed two steps per launch.
   int32_t advance(int32_t b, int32_t i, int32_t j, int32_t final_dst) {
     int32_t cur = b;
-    for (int32_t t = i + 1; t <= j; ++t) {
-      int32_t dst = (t == j && final_dst != ADST_BUF_NONE) ? final_dst : other_work(cur);
-      fwd(t, cur, dst);
+    int32_t t = i;
+    while (t < j) {
+      const int32_t n = (fuse_fwd_ && j - t >= 2) ? 2 : 1;
+      t += n;
+      const int32_t dst = (t == j && final_dst != ADST_BUF_NONE) ? final_dst : other_work(cur);
+      if (n == 2)
+        fwd2(t, cur, dst);
+      else
+        fwd(t, cur, dst);
       cur = dst;
     }
     return cur;
@@ -99,10 +114,15 @@ class Builder {
   void adjoint(int32_t t, int32_t xbuf) {
     if (!seeded_) {
       fwd(T_, xbuf, ADST_BUF_XT);
-      acts.push_back({ADST_OP_SEED, T_, ADST_BUF_XT, ADST_BUF_NONE});
-      seeded_ = true;
+      seed();
     }
     acts.push_back({ADST_OP_ADJ, t, needs_state_ ? xbuf : ADST_BUF_NONE, ADST_BUF_NONE});
+    ++adj_launches;
+  }
+
+  void seed() {
+    acts.push_back({ADST_OP_SEED, T_, ADST_BUF_XT, ADST_BUF_NONE});
+    seeded_ = true;
   }
 
   // Reverse steps i+1..i+l from x_i in `base` keeping every state but the
@@ -170,14 +190,16 @@ class Builder {
     const int32_t k = (T + c - 1) / c;
     std::vector<int32_t> where(T, ADST_BUF_NONE);  // checkpoint buffers by state
     where[0] = ADST_BUF_X0;
-    int32_t cur = ADST_BUF_X0;
-    for (int32_t t = 1; t <= T - 1; ++t) {
-      const bool keep = (t % k == 0) && t <= T - 2;
-      const int32_t dst = keep ? alloc_slot() : other_work(cur);
-      fwd(t, cur, dst);
-      if (keep) where[t] = dst;
-      cur = dst;
+    // Sweep: the checkpoints at the multiples of k below T-1 are written in
+    // place by the step producing them; the states between are transient.
+    int32_t cur = ADST_BUF_X0, at = 0;
+    for (int32_t cp = k; cp <= T - 2; cp += k) {
+      const int32_t s = alloc_slot();
+      cur = advance(cur, at, cp, s);
+      where[cp] = s;
+      at = cp;
     }
+    cur = advance(cur, at, T - 1, ADST_BUF_NONE);
     adjoint(T, cur);
     for (int32_t t = T - 1; t >= 1; --t) {
       const int32_t s = t - 1;
@@ -186,9 +208,22 @@ class Builder {
     }
   }
 
+  // No adjoint step reads state: one sweep straight to x_T, the seed, then
+  // the adjoint steps, two per launch when fusion is on.
   void elided() {
-    adjoint(T_, advance(ADST_BUF_X0, 0, T_ - 1, ADST_BUF_NONE));
-    for (int32_t t = T_ - 1; t >= 1; --t) adjoint(t, ADST_BUF_NONE);
+    advance(ADST_BUF_X0, 0, T_, ADST_BUF_XT);
+    seed();
+    int32_t t = T_;
+    while (t >= 1) {
+      if (fuse_adj_ && t >= 2) {
+        acts.push_back({ADST_OP_ADJ2, t, ADST_BUF_NONE, ADST_BUF_NONE});
+        t -= 2;
+      } else {
+        acts.push_back({ADST_OP_ADJ, t, ADST_BUF_NONE, ADST_BUF_NONE});
+        t -= 1;
+      }
+      ++adj_launches;
+    }
   }
 
   void zero_steps() { acts.push_back({ADST_OP_SEED, 0, ADST_BUF_X0, ADST_BUF_NONE}); }
@@ -196,6 +231,7 @@ class Builder {
  private:
   int32_t T_;
   bool needs_state_;
+  bool fuse_fwd_, fuse_adj_;
   bool seeded_ = false;
   std::vector<int32_t> free_;
 };
@@ -218,7 +254,7 @@ constexpr int64_t kMaxActions = int64_t(1) << 24;
 }  // namespace
 
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       Plan* out, std::string* err) {
+                       bool fuse_fwd, bool fuse_adj, Plan* out, std::string* err) {
   if (steps < 0) {
     *err = "steps must be >= 0";
     return ADST_ERR_ARG;
@@ -247,7 +283,7 @@ adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool n
     return ADST_ERR_UNSUPPORTED;
   }
 
-  Builder b(steps, needs_state);
+  Builder b(steps, needs_state, fuse_fwd, fuse_adj && !needs_state);
   if (steps == 0) {
     b.zero_steps();
   } else if (!needs_state) {
@@ -266,6 +302,8 @@ adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool n
   out->needs_state = needs_state;
   out->fwd_total = b.nfwd;
   out->adj_total = steps;
+  out->fwd_launches = b.fwd_launches;
+  out->adj_launches = b.adj_launches;
   out->acts = std::move(b.acts);
   return ADST_OK;
 }

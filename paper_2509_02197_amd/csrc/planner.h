@@ -16,8 +16,10 @@ struct Plan {
   int32_t sched = ADST_SCHED_STORE_ALL;  // resolved
   int32_t slots = 0;                     // slots the actions use (x0 excluded)
   bool needs_state = false;
-  int64_t fwd_total = 0;
-  int64_t adj_total = 0;
+  int64_t fwd_total = 0;     // forward steps (a fused pair counts 2)
+  int64_t adj_total = 0;     // adjoint steps
+  int64_t fwd_launches = 0;  // forward actions (a fused pair counts 1)
+  int64_t adj_launches = 0;  // adjoint actions
   std::vector<adst_action> acts;
 };
 
@@ -30,9 +32,11 @@ int64_t binomial_cost(int64_t l, int64_t c);
 inline int64_t store_all_slots(int64_t T) { return T > 2 ? T - 2 : 0; }
 
 // Build the action list. slots_avail is the number of checkpoint slots the
-// budget allows (x0 excluded). sched may be AUTO. Returns ADST_OK or
-// ADST_ERR_BUDGET / ADST_ERR_ARG with *err filled.
+// budget allows (x0 excluded). sched may be AUTO. fuse_fwd lets two forward
+// steps whose intermediate state nothing reads share one launch (FWD2);
+// fuse_adj does the same for state-free adjoint steps (ADJ2). Returns ADST_OK
+// or ADST_ERR_BUDGET / ADST_ERR_ARG / ADST_ERR_UNSUPPORTED with *err filled.
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       Plan* out, std::string* err);
+                       bool fuse_fwd, bool fuse_adj, Plan* out, std::string* err);
 
 }  // namespace adst

@@ -8,11 +8,15 @@ checks what makes a plan correct, independently of how it was built:
   * adjoint steps run T, T-1, ..., 1, each reading a buffer that holds
     x_{t-1} at that moment when the step's adjoint needs state;
   * the x_T buffer is not read again after the seed (it may alias g_T);
-  * checkpoint slots used stay within the allowed count.
+  * checkpoint slots used stay within the allowed count;
+  * a fused forward pair (FWD2, steps t-1 and t) reads x_{t-2} and leaves
+    x_{t-1} nowhere, so any later use of x_{t-1} fails the checks above;
+    a fused adjoint pair (ADJ2, steps t and t-1) only appears for
+    state-free adjoints.
 Returns the forward-step count and the set of slots touched.
 """
 X0, W0, W1, XT, SLOT0 = 0, 1, 2, 3, 4
-FWD, SEED, ADJ = 0, 1, 2
+FWD, SEED, ADJ, FWD2, ADJ2 = 0, 1, 2, 3, 4
 NONE = -1
 
 
@@ -23,9 +27,10 @@ def replay(actions, T, needs_state, max_slots):
     nfwd = 0
     slots = set()
     for k, (op, t, src, dst) in enumerate(actions):
-        if op == FWD:
+        if op in (FWD, FWD2):
+            n = 1 if op == FWD else 2
             assert not (seeded and src == XT), f"action {k}: reads x_T buffer after the seed"
-            assert holds.get(src) == t - 1, f"action {k}: FWD {t} reads buffer {src} holding {holds.get(src)}"
+            assert holds.get(src) == t - n, f"action {k}: FWD {t} reads buffer {src} holding {holds.get(src)}"
             assert dst not in (X0, src, NONE), f"action {k}: bad destination {dst}"
             assert 1 <= t <= T
             if dst == XT:
@@ -33,7 +38,7 @@ def replay(actions, T, needs_state, max_slots):
             if dst >= SLOT0:
                 slots.add(dst)
             holds[dst] = t
-            nfwd += 1
+            nfwd += n
         elif op == SEED:
             assert not seeded, "seeded twice"
             assert holds.get(src) == T, f"seed reads buffer {src} holding {holds.get(src)}"
@@ -49,6 +54,10 @@ def replay(actions, T, needs_state, max_slots):
             else:
                 assert src == NONE
             next_adj -= 1
+        elif op == ADJ2:
+            assert seeded and not needs_state and src == NONE
+            assert t == next_adj and t >= 2, f"fused adjoint {t} out of order"
+            next_adj -= 2
         else:
             raise AssertionError(f"unknown op {op}")
     assert seeded

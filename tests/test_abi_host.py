@@ -53,7 +53,8 @@ def test_struct_layouts_match_header():
     # int32 x2, int64 x3, double x2, uint32 (+pad) = 56 bytes
     assert ctypes.sizeof(adst.adst_problem) == 56
     assert ctypes.sizeof(adst.adst_action) == 16
-    assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 4 * 8 + 6 * 8 + 6 * 4
+    # int32 x4, int64 x6, uint64 x6, float x6
+    assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 6 * 8 + 6 * 8 + 6 * 4
 
 
 def _p(kind=adst.ADST_ALLENCAHN3D7, dims=(8, 8, 8), dtype=adst.ADST_F64, flags=0):

@@ -178,3 +178,45 @@ def test_workspace_reuse_between_calls():
     ws.fill_(0xA5)
     b = gpu_vjp(VD, inp, 8, DIFF, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL, True, ws=ws)
     assert np.array_equal(a["dx0"], b["dx0"]) and np.array_equal(a["dK"], b["dK"])
+
+
+FUSION_CASES = [
+    # kind, dtype, shape, T, loss, dK, flags, sched, slots (None = unlimited)
+    (J, F64, (64, 64), 10, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (333, 517), 7, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F32, (130, 70), 9, DIFF, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (1, 1), 5, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (2, 9), 4, DOT_W, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (3, 3), 3, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (5, 260), 6, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (517, 253), 11, SEED, False, 0, adst.ADST_SCHED_AUTO, None),
+    (J, F64, (90, 130), 15, HALF_SQ, False, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_BINOMIAL, 2),
+    (J, F32, (77, 300), 13, DIFF, False, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_UNIFORM, 3),
+    (VD, F32, (257, 300), 9, DIFF, True, 0, adst.ADST_SCHED_BINOMIAL, 2),
+    (VD, F64, (70, 129), 6, DOT_W, False, 0, adst.ADST_SCHED_AUTO, None),
+    (VD, F32, (1, 7), 3, DIFF, True, 0, adst.ADST_SCHED_BINOMIAL, 1),
+    (VD, F64, (3, 300), 5, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
+    (VD, F32, (66, 517), 12, DIFF, True, 0, adst.ADST_SCHED_UNIFORM, 2),
+]
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T,loss,dK,flags,sched,slots", FUSION_CASES)
+def test_fused_launches_match_single_steps_bitwise(kind, dtype, shape, T, loss, dK, flags, sched,
+                                                   slots):
+    """Temporal blocking (two steps per launch) gives the bits of one launch
+    per step, and both match the oracle."""
+    say(f"fusion kind={kind} dtype={dtype} shape={shape} T={T} flags={flags} sched={sched}")
+    inp = inputs(kind, dtype, shape, 8)
+    budget = None if slots is None else slots * inp["x0"].nbytes
+    a = gpu_vjp(kind, inp, T, loss, budget, sched, dK, flags)
+    b = gpu_vjp(kind, inp, T, loss, budget, sched, dK, flags | adst.ADST_NO_FUSE)
+    assert b["info"]["fwd_launches"] == b["info"]["fwd_steps_total"]
+    assert a["info"]["fwd_launches"] <= b["info"]["fwd_launches"]
+    if kind == J and T >= 2 and not flags:
+        assert a["info"]["fwd_launches"] < b["info"]["fwd_launches"]
+        assert a["info"]["adj_launches"] < b["info"]["adj_launches"]
+    for key in ("dx0", "dK", "xT"):
+        if a[key] is not None:
+            assert np.array_equal(a[key], b[key]), key
+    assert a["loss"] == b["loss"]
+    check_against_oracle(kind, dtype, inp, T, loss, dK, a)

@@ -150,3 +150,42 @@ def test_workspace_and_bytes():
 def test_zero_steps_plan():
     acts = adst.adst_plan_actions(prob(), 0, 0, adst.ADST_SCHED_AUTO)
     assert acts == [(adst.ADST_OP_SEED, 0, adst.ADST_BUF_X0, adst.ADST_BUF_NONE)]
+
+
+@pytest.mark.parametrize("kind,flags,sched,slots", [
+    (adst.ADST_JACOBI2D5, 0, adst.ADST_SCHED_AUTO, 0),
+    (adst.ADST_JACOBI2D5, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_BINOMIAL, 3),
+    (adst.ADST_JACOBI2D5, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_UNIFORM, 3),
+    (adst.ADST_JACOBI2D5, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_STORE_ALL, 100),
+    (adst.ADST_VARDIFF2D9, 0, adst.ADST_SCHED_BINOMIAL, 2),
+])
+def test_fused_plans_replay_with_the_same_step_counts(kind, flags, sched, slots):
+    """Temporal blocking changes launches, never which states are computed:
+    fused plans replay, take the same forward steps, and fewer launches."""
+    for T in list(range(0, 23)) + [64, 100]:
+        p = prob(kind, (6, 5, 1), flags=flags)
+        pn = prob(kind, (6, 5, 1), flags=flags | adst.ADST_NO_FUSE)
+        want_dK = kind == adst.ADST_VARDIFF2D9
+        b = budget_for(slots, p)
+        fused = adst.adst_plan_actions(p, T, b, sched, want_dK)
+        plain = adst.adst_plan_actions(pn, T, b, sched, want_dK)
+        ns = bool(flags & adst.ADST_FORCE_TAPE) or want_dK
+        nf, _ = replay(fused, T, ns, slots)
+        np_, _ = replay(plain, T, ns, slots)
+        assert nf == np_
+        assert not any(op in (adst.ADST_OP_FWD2, adst.ADST_OP_ADJ2) for op, *_ in plain)
+        info, infon = adst.adst_plan(p, T, b, sched, want_dK), adst.adst_plan(pn, T, b, sched, want_dK)
+        assert info.fwd_steps_total == infon.fwd_steps_total == nf
+        assert info.fwd_launches <= infon.fwd_launches == infon.fwd_steps_total
+        assert info.adj_launches <= infon.adj_launches == T
+
+
+def test_elided_jacobi_fuses_everything():
+    p = prob(adst.ADST_JACOBI2D5, (6, 5, 1))
+    info = adst.adst_plan(p, 100, 0, adst.ADST_SCHED_AUTO)
+    assert info.fwd_launches == 50 and info.adj_launches == 50
+    info = adst.adst_plan(p, 7, 0, adst.ADST_SCHED_AUTO)
+    assert info.fwd_launches == 4 and info.adj_launches == 4
+    # Allen-Cahn has no fused kernel: one launch per step
+    info = adst.adst_plan(prob(), 30, budget_for(4), adst.ADST_SCHED_BINOMIAL)
+    assert info.fwd_launches == info.fwd_steps_total
