@@ -351,6 +351,18 @@ __device__ inline void ac_halo_cell(int tid, int* ly, int* lx) {
 // Forward, zero ghost values:
 //   lap = (((((x[-x]+x[+x])+x[-y])+x[+y])+x[-z])+x[+z]) - 6*a
 //   x'  = (a + D*lap) - C*((a*a)*a)
+// Single-step and fused kernels evaluate every point through this function.
+template <class R>
+__device__ inline R allencahn_point(R a, R xm, R xp, R ym, R yp, R zm, R zp, R D, R C) {
+  R lap = xm + xp;
+  lap += ym;
+  lap += yp;
+  lap += zm;
+  lap += zp;
+  lap = lap - R(6) * a;
+  return (a + D * lap) - C * ((a * a) * a);
+}
+
 template <class R>
 __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict__ x,
                                                              R* __restrict__ y, int nx, int ny,
@@ -379,30 +391,119 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
     tile[ty + 5][tx + 1] = curB;
     if (hly >= 0) tile[hly][hlx] = halo;
     __syncthreads();
-    if (va) {
-      const R a = curA;
-      R lap = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
-      lap += tile[ty][tx + 1];
-      lap += tile[ty + 2][tx + 1];
-      lap += belowA;
-      lap += aboveA;
-      lap = lap - R(6) * a;
-      y[k * plane + t.ja * nx + t.i] = (a + D * lap) - C * ((a * a) * a);
-    }
-    if (vb) {
-      const R a = curB;
-      R lap = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
-      lap += tile[ty + 4][tx + 1];
-      lap += tile[ty + 6][tx + 1];
-      lap += belowB;
-      lap += aboveB;
-      lap = lap - R(6) * a;
-      y[k * plane + t.jb * nx + t.i] = (a + D * lap) - C * ((a * a) * a);
-    }
+    if (va)
+      y[k * plane + t.ja * nx + t.i] =
+          allencahn_point(curA, tile[ty + 1][tx], tile[ty + 1][tx + 2], tile[ty][tx + 1],
+                          tile[ty + 2][tx + 1], belowA, aboveA, D, C);
+    if (vb)
+      y[k * plane + t.jb * nx + t.i] =
+          allencahn_point(curB, tile[ty + 5][tx], tile[ty + 5][tx + 2], tile[ty + 4][tx + 1],
+                          tile[ty + 6][tx + 1], belowB, aboveB, D, C);
     belowA = curA;
     belowB = curB;
     curA = aboveA;
     curB = aboveB;
+  }
+}
+
+// Two forward steps in one launch (temporal blocking in 2.5-D). The first
+// step is evaluated on a 64 x 16 region of each plane (four rows per
+// thread), the second on its inner 62 x 14 tile, marching in z: at plane p
+// the workgroup computes the intermediate state y1(p) from x(p-1..p+1) and
+// then the output plane p-1 from y1(p-2..p). x(p) and y1(p-1) are staged in
+// LDS for their xy neighbours, the z neighbours stay in registers. y1 is set
+// to 0 outside the grid, which is the zero ghost value the second step reads.
+constexpr int kAc2RPT = 4, kAc2SX = 64, kAc2SY = 4 * kAc2RPT;
+constexpr int kAc2OX = kAc2SX - 2, kAc2OY = kAc2SY - 2, kAc2ZC = 32;
+
+template <class R>
+__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_x2(const R* __restrict__ x,
+                                                                R* __restrict__ y, int nx, int ny,
+                                                                int nz, int tiles_x, int tiles_y,
+                                                                int ntiles, R D, R C) {
+  constexpr int SX = kAc2SX, SY = kAc2SY, LX = SX + 2, LY = SY + 2, RPT = kAc2RPT;
+  __shared__ R xt[LY][LX];
+  __shared__ R yt[SY][SX];
+  int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int bx = b % tiles_x;
+  b /= tiles_x;
+  const int by = b % tiles_y;
+  const int bz = b / tiles_y;
+  const int i0 = bx * kAc2OX, j0 = by * kAc2OY;
+  const int z0 = bz * kAc2ZC, z1 = min(z0 + kAc2ZC, nz);
+  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
+  const int i1 = i0 - 1 + tx;  // column of this thread in the first-step region
+  const int plane = nx * ny;
+  auto inxy = [&](int j, int i) { return i >= 0 && i < nx && j >= 0 && j < ny; };
+  auto ld = [&](int k, int j, int i) -> R {
+    return (k >= 0 && k < nz && inxy(j, i)) ? x[k * plane + j * nx + i] : R(0);
+  };
+  // one cell of the LDS ring around the region (2*LX + 2*SY = 164 < 256)
+  int hly = -1, hlx = 0;
+  if (tid < LX) {
+    hly = 0;
+    hlx = tid;
+  } else if (tid < 2 * LX) {
+    hly = LY - 1;
+    hlx = tid - LX;
+  } else if (tid < 2 * LX + SY) {
+    hly = tid - 2 * LX + 1;
+    hlx = 0;
+  } else if (tid < 2 * LX + 2 * SY) {
+    hly = tid - 2 * LX - SY + 1;
+    hlx = LX - 1;
+  }
+  const int hj = j0 - 2 + hly, hi = i0 - 2 + hlx;
+  R xprev[RPT], xcur[RPT], xnext[RPT], yb[RPT], yc[RPT], yn[RPT];
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) {
+    const int j1 = j0 - 1 + ty + 4 * q;
+    xprev[q] = ld(z0 - 2, j1, i1);
+    xcur[q] = ld(z0 - 1, j1, i1);
+    yb[q] = R(0);
+    yc[q] = R(0);
+  }
+  for (int p = z0 - 1; p <= z1; ++p) {
+    const R hv = hly >= 0 ? ld(p, hj, hi) : R(0);
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) xnext[q] = ld(p + 1, j0 - 1 + ty + 4 * q, i1);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) xt[ty + 4 * q + 1][tx + 1] = xcur[q];
+    if (hly >= 0) xt[hly][hlx] = hv;
+    __syncthreads();
+    const bool pin = p >= 0 && p < nz;
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const int r = ty + 4 * q;
+      yn[q] = (pin && inxy(j0 - 1 + r, i1))
+                  ? allencahn_point(xcur[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
+                                    xt[r + 2][tx + 1], xprev[q], xnext[q], D, C)
+                  : R(0);
+    }
+    if (p >= z0 + 1) {
+      const int k = p - 1;
+#pragma unroll
+      for (int q = 0; q < RPT; ++q) {
+        const int r = ty + 4 * q;
+        const int j = j0 - 1 + r;
+        if (tx >= 1 && tx <= kAc2OX && r >= 1 && r <= kAc2OY && inxy(j, i1))
+          y[k * plane + j * nx + i1] =
+              allencahn_point(yc[q], yt[r][tx - 1], yt[r][tx + 1], yt[r - 1][tx], yt[r + 1][tx],
+                              yb[q], yn[q], D, C);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) yt[ty + 4 * q][tx] = yn[q];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      xprev[q] = xcur[q];
+      xcur[q] = xnext[q];
+      yb[q] = yc[q];
+      yc[q] = yn[q];
+    }
   }
 }
 
@@ -654,11 +755,17 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       break;
     }
     case ADST_ALLENCAHN3D7: {
-      if (two) return hipErrorInvalidValue;
-      const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
-      const int nt = tx * ty * cdiv(s.nz, kAcZC);
-      fwd_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-          x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+      if (two) {
+        const int tx = cdiv(s.nx, kAc2OX), ty = cdiv(s.ny, kAc2OY);
+        const int nt = tx * ty * cdiv(s.nz, kAc2ZC);
+        fwd_allencahn3d7_x2<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+            x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+      } else {
+        const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
+        const int nt = tx * ty * cdiv(s.nz, kAcZC);
+        fwd_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+            x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+      }
       break;
     }
     case ADST_VARDIFF2D9: {
@@ -765,7 +872,7 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
                              : forward_t<float>(s, x, K, y, false, stream);
 }
 
-bool has_forward2(int32_t kind) { return kind == ADST_JACOBI2D5; }
+bool has_forward2(int32_t kind) { return kind == ADST_JACOBI2D5 || kind == ADST_ALLENCAHN3D7; }
 bool has_adjoint2(int32_t kind) { return kind == ADST_JACOBI2D5; }
 
 hipError_t launch_forward2(const StepShape& s, const void* x, const void* K, void* y,

@@ -197,6 +197,12 @@ FUSION_CASES = [
     (VD, F32, (1, 7), 3, DIFF, True, 0, adst.ADST_SCHED_BINOMIAL, 1),
     (VD, F64, (3, 300), 5, HALF_SQ, False, 0, adst.ADST_SCHED_AUTO, None),
     (VD, F32, (66, 517), 12, DIFF, True, 0, adst.ADST_SCHED_UNIFORM, 2),
+    (AC, F64, (39, 45, 67), 9, DOT_W, False, 0, adst.ADST_SCHED_BINOMIAL, 2),
+    (AC, F32, (17, 33, 130), 11, DIFF, False, 0, adst.ADST_SCHED_UNIFORM, 2),
+    (AC, F64, (70, 15, 63), 8, HALF_SQ, False, 0, adst.ADST_SCHED_BINOMIAL, 1),
+    (AC, F64, (1, 1, 1), 6, SEED, False, 0, adst.ADST_SCHED_BINOMIAL, 0),
+    (AC, F64, (3, 1, 200), 7, HALF_SQ, False, 0, adst.ADST_SCHED_BINOMIAL, 1),
+    (AC, F64, (33, 14, 62), 5, DOT_W, False, 0, adst.ADST_SCHED_BINOMIAL, 0),
 ]
 
 

@@ -141,9 +141,10 @@ def test_workspace_and_bytes():
     assert info.state_bytes == S
     assert info.workspace_bytes == 16384 + (3 + info.slots) * stride
     assert info.fwd_workspace_bytes == S
-    # Allen-Cahn: 16 B per point per forward step, 24 per adjoint, 16 for the seed
+    # Allen-Cahn: 16 B per point per forward launch (one or two steps), 24 per
+    # adjoint, 16 for the seed
     n = 100 * 30 * 7
-    assert info.alg_bytes == n * (16 * info.fwd_steps_total + 24 * 12 + 16)
+    assert info.alg_bytes == n * (16 * info.fwd_launches + 24 * 12 + 16)
     assert adst.adst_plan(p, 0, 0, 0).workspace_bytes == 16384
 
 
@@ -158,18 +159,21 @@ def test_zero_steps_plan():
     (adst.ADST_JACOBI2D5, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_UNIFORM, 3),
     (adst.ADST_JACOBI2D5, adst.ADST_FORCE_TAPE, adst.ADST_SCHED_STORE_ALL, 100),
     (adst.ADST_VARDIFF2D9, 0, adst.ADST_SCHED_BINOMIAL, 2),
+    (adst.ADST_ALLENCAHN3D7, 0, adst.ADST_SCHED_BINOMIAL, 3),
+    (adst.ADST_ALLENCAHN3D7, 0, adst.ADST_SCHED_UNIFORM, 2),
 ])
 def test_fused_plans_replay_with_the_same_step_counts(kind, flags, sched, slots):
     """Temporal blocking changes launches, never which states are computed:
     fused plans replay, take the same forward steps, and fewer launches."""
     for T in list(range(0, 23)) + [64, 100]:
-        p = prob(kind, (6, 5, 1), flags=flags)
-        pn = prob(kind, (6, 5, 1), flags=flags | adst.ADST_NO_FUSE)
+        dims = (6, 5, 4) if kind == AC else (6, 5, 1)
+        p = prob(kind, dims, flags=flags)
+        pn = prob(kind, dims, flags=flags | adst.ADST_NO_FUSE)
         want_dK = kind == adst.ADST_VARDIFF2D9
         b = budget_for(slots, p)
         fused = adst.adst_plan_actions(p, T, b, sched, want_dK)
         plain = adst.adst_plan_actions(pn, T, b, sched, want_dK)
-        ns = bool(flags & adst.ADST_FORCE_TAPE) or want_dK
+        ns = bool(flags & adst.ADST_FORCE_TAPE) or want_dK or kind == AC
         nf, _ = replay(fused, T, ns, slots)
         np_, _ = replay(plain, T, ns, slots)
         assert nf == np_
@@ -186,6 +190,9 @@ def test_elided_jacobi_fuses_everything():
     assert info.fwd_launches == 50 and info.adj_launches == 50
     info = adst.adst_plan(p, 7, 0, adst.ADST_SCHED_AUTO)
     assert info.fwd_launches == 4 and info.adj_launches == 4
-    # Allen-Cahn has no fused kernel: one launch per step
+    # Allen-Cahn fuses forward chains; its adjoint reads state, so it does not
     info = adst.adst_plan(prob(), 30, budget_for(4), adst.ADST_SCHED_BINOMIAL)
+    assert info.fwd_launches < info.fwd_steps_total and info.adj_launches == 30
+    pn = prob(flags=adst.ADST_NO_FUSE)
+    info = adst.adst_plan(pn, 30, budget_for(4), adst.ADST_SCHED_BINOMIAL)
     assert info.fwd_launches == info.fwd_steps_total
