@@ -213,6 +213,64 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
                      void* dx0, void* dcoeff, void* xT, double* loss_dev, void* ws,
                      uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info);
 
+/* ---- Store/recompute selection for a general program (Sec. IV) --------
+ * The integer program of Sec. IV-A: one binary per forwarded array (store or
+ * recompute), objective sum_i cost_i * (1 - store_i), and every memory
+ * measurement of the program's allocation timeline at or below the limit;
+ * with control flow every path contributes its own timeline (Sec. IV-B).
+ * The timeline is a list of events; each changes the running total of the
+ * current path by an affine amount and records one measurement:
+ *   ALLOC / FREE      +amount / -amount
+ *   PRODUCE i         +size_i                     the forward pass creates A_i
+ *   DROP i            -size_i * (1 - store_i)     after its forward use
+ *   RECOMPUTE i       +(overhead_i + size_i) * (1 - store_i)   backward rebuild
+ *   RECOMPUTE_DONE i  -overhead_i * (1 - store_i) rebuild temporaries freed
+ *   RELEASE i         -size_i                     backward use is over
+ *   PATH              starts the next path's timeline at 0
+ * Units are the caller's (e.g. MiB and FLOP). Solved exactly by branch and
+ * bound (exponential in the worst case; n_arrays <= 48). Among optimal
+ * choices the lower peak wins, then storing lower-numbered arrays. */
+typedef struct {
+  double size;     /* memory of the array */
+  double overhead; /* peak extra memory while recomputing it */
+  double cost;     /* cost of recomputing it (e.g. FLOP) */
+} adst_ilp_array;
+
+typedef enum {
+  ADST_ILP_ALLOC = 0,
+  ADST_ILP_FREE = 1,
+  ADST_ILP_PRODUCE = 2,
+  ADST_ILP_DROP = 3,
+  ADST_ILP_RECOMPUTE = 4,
+  ADST_ILP_RECOMPUTE_DONE = 5,
+  ADST_ILP_RELEASE = 6,
+  ADST_ILP_PATH = 7
+} adst_ilp_kind;
+
+typedef struct {
+  int32_t kind;  /* adst_ilp_kind */
+  int32_t array; /* array index for PRODUCE .. RELEASE */
+  double amount; /* for ALLOC / FREE, >= 0 */
+} adst_ilp_event;
+
+typedef struct {
+  double objective;     /* recompute cost of the choice */
+  double peak;          /* largest measurement under the choice */
+  int64_t measurements; /* measurements over all paths */
+  int64_t nodes;        /* search nodes visited */
+  int32_t paths;
+  int32_t reserved;
+} adst_ilp_info;
+
+/* Host only. store_out[i] receives 1 (store) or 0 (recompute); info
+ * (optional) the objective and peak. Errors: ADST_ERR_ARG (NULL arrays or
+ * events with a positive count, n_arrays outside [0, 48], a bad event kind
+ * or index, a negative or non-finite amount or limit), ADST_ERR_BUDGET (no
+ * choice fits the limit). */
+adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,
+                           const adst_ilp_event* events, int64_t n_events, double limit,
+                           int32_t* store_out, adst_ilp_info* info);
+
 /* Static description of a status code. */
 const char* adst_status_str(adst_status status);
 

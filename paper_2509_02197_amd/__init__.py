@@ -25,8 +25,10 @@ ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE = 0x1, 0x2, 0x4
 ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2 = 0, 1, 2, 3, 4
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
-EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_status_str",
-            "adst_last_error")
+EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
+            "adst_status_str", "adst_last_error")
+ILP_EVENTS = {"alloc": 0, "free": 1, "produce": 2, "drop": 3, "recompute": 4,
+              "recompute_done": 5, "release": 6, "path": 7}
 
 
 class adst_problem(ctypes.Structure):
@@ -56,6 +58,21 @@ class adst_plan_info(ctypes.Structure):
         return {f[0]: getattr(self, f[0]) for f in self._fields_ if f[0] != "reserved"}
 
 
+class adst_ilp_array(ctypes.Structure):
+    _fields_ = [("size", ctypes.c_double), ("overhead", ctypes.c_double),
+                ("cost", ctypes.c_double)]
+
+
+class adst_ilp_event(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("array", ctypes.c_int32), ("amount", ctypes.c_double)]
+
+
+class adst_ilp_info(ctypes.Structure):
+    _fields_ = [("objective", ctypes.c_double), ("peak", ctypes.c_double),
+                ("measurements", ctypes.c_int64), ("nodes", ctypes.c_int64),
+                ("paths", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class AdstError(RuntimeError):
     def __init__(self, status, detail):
         self.status = status
@@ -82,7 +99,9 @@ def lib():
     L.adst_forward.argtypes = [P(adst_problem), vp, vp, i32, vp, vp, u64, vp]
     L.adst_vjp.argtypes = [P(adst_problem), vp, vp, i32, i32, vp, u64, i32, vp, vp, vp, vp, vp, u64,
                            vp, P(adst_plan_info)]
-    for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp"):
+    L.adst_ilp_solve.argtypes = [P(adst_ilp_array), i32, P(adst_ilp_event), i64, ctypes.c_double,
+                                 P(i32), P(adst_ilp_info)]
+    for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve"):
         getattr(L, f).restype = ctypes.c_int
     L.adst_status_str.argtypes = [ctypes.c_int]
     L.adst_status_str.restype = ctypes.c_char_p
@@ -167,6 +186,27 @@ def adst_vjp(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx
                           _ptr(loss_dev), _ptr(ws), ws_bytes, _stream(stream),
                           ctypes.byref(info) if info is not None else None))
     return info
+
+
+def adst_ilp_solve(arrays, events, limit):
+    """arrays: sequence of (size, overhead, cost); events: sequence of
+    ("alloc"|"free", amount), (kind, array_index) or ("path",).
+    Returns (store flags, adst_ilp_info)."""
+    n = len(arrays)
+    A = (adst_ilp_array * max(n, 1))()
+    for k, (size, overhead, cost) in enumerate(arrays):
+        A[k].size, A[k].overhead, A[k].cost = size, overhead, cost
+    E = (adst_ilp_event * max(len(events), 1))()
+    for k, ev in enumerate(events):
+        E[k].kind = ILP_EVENTS[ev[0]]
+        if ev[0] in ("alloc", "free"):
+            E[k].amount = float(ev[1])
+        elif ev[0] != "path":
+            E[k].array = int(ev[1])
+    store = (ctypes.c_int32 * max(n, 1))()
+    info = adst_ilp_info()
+    _check(lib().adst_ilp_solve(A, n, E, len(events), float(limit), store, ctypes.byref(info)))
+    return [store[k] for k in range(n)], info
 
 
 # ------------------------------------------------------------ conveniences

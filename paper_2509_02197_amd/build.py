@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libadst.so")
 ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
-HOST_SOURCES = ["planner.cpp", "abi.cpp"]
+HOST_SOURCES = ["planner.cpp", "ilp.cpp", "abi.cpp"]
 HIP_SOURCES = ["kernels.hip"]
 
 COMMON = ["-std=c++17", "-O3", "-fPIC", "-ffp-contract=off", "-Wall",

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -15,9 +16,12 @@
 
 #include "adst.h"
 #include "kernels.h"
+#include "ilp.h"
 #include "planner.h"
 
 namespace adst {
+
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -447,6 +451,39 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
   }
   if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,
+                           const adst_ilp_event* events, int64_t n_events, double limit,
+                           int32_t* store_out, adst_ilp_info* info) {
+  if (n_arrays < 0 || n_arrays > 48) return fail(ADST_ERR_ARG, "n_arrays must be in [0, 48]");
+  if (n_events < 0) return fail(ADST_ERR_ARG, "n_events must be >= 0");
+  if ((n_arrays > 0 && (!arrays || !store_out)) || (n_events > 0 && !events))
+    return fail(ADST_ERR_ARG, "NULL arrays, events or store_out");
+  if (!std::isfinite(limit) || limit < 0) return fail(ADST_ERR_ARG, "limit must be finite and >= 0");
+  for (int32_t i = 0; i < n_arrays; ++i) {
+    const adst_ilp_array& a = arrays[i];
+    if (!std::isfinite(a.size) || !std::isfinite(a.overhead) || !std::isfinite(a.cost) ||
+        a.size < 0 || a.overhead < 0 || a.cost < 0)
+      return fail(ADST_ERR_ARG, "array " + std::to_string(i) + ": values must be finite and >= 0");
+  }
+  IlpResult r;
+  std::string err;
+  const adst_status st = ilp_solve(arrays, n_arrays, events, n_events, limit, &r, &err);
+  if (info) {
+    *info = adst_ilp_info{};
+    info->measurements = r.measurements;
+    info->nodes = r.nodes;
+    info->paths = r.paths;
+  }
+  if (st != ADST_OK) return fail(st, err);
+  for (int32_t i = 0; i < n_arrays; ++i) store_out[i] = r.v[i];
+  if (info) {
+    info->objective = r.objective;
+    info->peak = r.peak;
+  }
   g_last_error.clear();
   return ADST_OK;
 }
