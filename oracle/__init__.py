@@ -14,7 +14,7 @@ import os
 
 import numpy as np
 
-JACOBI2D5, ALLENCAHN3D7, VARDIFF2D9 = 0, 1, 2
+JACOBI2D5, ALLENCAHN3D7, VARDIFF2D9, GAUSSSEIDEL2D5 = 0, 1, 2, 3
 HALF_SQ, DOT_W, HALF_SQ_DIFF, SEED = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -47,9 +47,11 @@ def _load():
 
 
 def default_params(kind):
-    """The step constants of the three kinds: Jacobi w = 0.2; Allen-Cahn
-    diffusion 0.1 and cubic 0.1; variable-coefficient diffusion dt = 0.1."""
-    return {JACOBI2D5: (0.2, 0.0), ALLENCAHN3D7: (0.1, 0.1), VARDIFF2D9: (0.1, 0.0)}[kind]
+    """The step constants of the kinds: Jacobi and Gauss-Seidel w = 0.2;
+    Allen-Cahn diffusion 0.1 and cubic 0.1; variable-coefficient diffusion
+    dt = 0.1."""
+    return {JACOBI2D5: (0.2, 0.0), ALLENCAHN3D7: (0.1, 0.1), VARDIFF2D9: (0.1, 0.0),
+            GAUSSSEIDEL2D5: (0.2, 0.0)}[kind]
 
 
 def _suffix(dtype):

@@ -23,13 +23,21 @@
 // A tangent-linear (forward-mode) sweep is included so that tests can check
 // the adjoint dot-product identity <J v, w> = <v, J^T w>.
 //
-// The three step kinds (the stencil programs the gradient is taken of):
+// The four step kinds (the stencil programs the gradient is taken of):
 //   JACOBI2D5  x'[c] = w * (x[c] + x[W] + x[E] + x[S] + x[N]) on interior
 //              points, x'[c] = x[c] on the outer ring (boundary held fixed);
 //              p[0] = w.
 //   ALLENCAHN3D7  every point is updated, out-of-grid neighbours read 0:
 //              lap = sum of the 6 face neighbours - 6 x[c]
 //              x'  = (x[c] + D*lap) - C*x[c]^3;            p[0] = D, p[1] = C.
+//   GAUSSSEIDEL2D5  the in-place counterpart of JACOBI2D5: interior points
+//              are overwritten one at a time in row-major order (x fastest)
+//              with x[c] = w * ((((x[c] + x[E]) + x[N]) + x[S]) + x[W]), so
+//              x[S] and x[W] already hold this sweep's values while x[c],
+//              x[E] and x[N] still hold the previous sweep's; the ring stays
+//              fixed; p[0] = w. (The paper's Seidel2d case study, Sec. V-B,
+//              names an in-place two-dimensional stencil in a time loop
+//              without printing it; this is the five-point reading.)
 //   VARDIFF2D9 conservative edge form of div(K grad x) on the isotropic
 //              9-point stencil with no-flux boundary (edges leaving the grid
 //              are dropped): x' = x[c] + dt * sum_n c_n (K[c]+K[n]) (x[n]-x[c]),
@@ -53,7 +61,7 @@
 
 namespace {
 
-enum Kind { JACOBI2D5 = 0, ALLENCAHN3D7 = 1, VARDIFF2D9 = 2 };
+enum Kind { JACOBI2D5 = 0, ALLENCAHN3D7 = 1, VARDIFF2D9 = 2, GAUSSSEIDEL2D5 = 3 };
 enum Loss { HALF_SQ = 0, DOT_W = 1, HALF_SQ_DIFF = 2, SEED = 3 };
 
 struct Grid {
@@ -78,9 +86,30 @@ template <class R> R nine_weight(int n) {
 }
 
 // ---------------------------------------------------------------- forward
+// One in-place Gauss-Seidel sweep over the interior in row-major order.
+template <class R>
+void gauss_seidel_sweep(const Grid& g, const double* p, R* x) {
+  const R w = R(p[0]);
+  for (int64_t y = 1; y < g.ny - 1; ++y)
+    for (int64_t i = 1; i < g.nx - 1; ++i) {
+      const int64_t c = g.at(i, y, 0);
+      R s = x[c];
+      s += x[g.at(i + 1, y, 0)];  // E: previous sweep's value
+      s += x[g.at(i, y + 1, 0)];  // N: previous sweep's value
+      s += x[g.at(i, y - 1, 0)];  // S: this sweep's value
+      s += x[g.at(i - 1, y, 0)];  // W: this sweep's value
+      x[c] = w * s;
+    }
+}
+
 template <class R>
 void step_forward(int kind, const Grid& g, const double* p, const R* x,
                   const R* K, R* out) {
+  if (kind == GAUSSSEIDEL2D5) {
+    std::memcpy(out, x, sizeof(R) * g.size());
+    gauss_seidel_sweep<R>(g, p, out);
+    return;
+  }
   for (int64_t z = 0; z < g.nz; ++z)
     for (int64_t y = 0; y < g.ny; ++y)
       for (int64_t i = 0; i < g.nx; ++i) {
@@ -130,9 +159,35 @@ void step_forward(int kind, const Grid& g, const double* p, const R* x,
 // -------------------------------------------------------- reverse (scatter)
 // gin receives g_{t-1} (must be zeroed by the caller), dK (if non-null)
 // accumulates; x is the step's input state x_{t-1}; gout is g_t.
+// Reverse of one in-place sweep: the sweep is the product of point updates
+// U_1 ... U_n (row-major), so its transpose applies U_n^T ... U_1^T, i.e. the
+// points in reverse order; U_k^T moves g[k] into the adjoints of the values
+// the update read: g[k] <- w*g[k] (its old value) and w*g[k] added to each
+// neighbour (whatever sweep's value it was). The gradient of the overwritten
+// value is cleared by the assignment, as for any overwrite.
+template <class R>
+void gauss_seidel_reverse(const Grid& g, const double* p, R* gr) {
+  const R w = R(p[0]);
+  for (int64_t y = g.ny - 2; y >= 1; --y)
+    for (int64_t i = g.nx - 2; i >= 1; --i) {
+      const int64_t c = g.at(i, y, 0);
+      const R gc = gr[c];
+      gr[c] = w * gc;
+      gr[g.at(i - 1, y, 0)] += w * gc;
+      gr[g.at(i + 1, y, 0)] += w * gc;
+      gr[g.at(i, y - 1, 0)] += w * gc;
+      gr[g.at(i, y + 1, 0)] += w * gc;
+    }
+}
+
 template <class R>
 void step_adjoint_scatter(int kind, const Grid& g, const double* p, const R* x,
                           const R* K, const R* gout, R* gin, R* dK) {
+  if (kind == GAUSSSEIDEL2D5) {
+    for (int64_t c = 0; c < g.size(); ++c) gin[c] += gout[c];
+    gauss_seidel_reverse<R>(g, p, gin);
+    return;
+  }
   for (int64_t z = 0; z < g.nz; ++z)
     for (int64_t y = 0; y < g.ny; ++y)
       for (int64_t i = 0; i < g.nx; ++i) {
@@ -188,6 +243,11 @@ void step_adjoint_scatter(int kind, const Grid& g, const double* p, const R* x,
 template <class R>
 void step_tangent(int kind, const Grid& g, const double* p, const R* x,
                   const R* K, const R* xd, const R* kd, R* xd_out) {
+  if (kind == GAUSSSEIDEL2D5) {  // linear: the tangent takes the same sweep
+    std::memcpy(xd_out, xd, sizeof(R) * g.size());
+    gauss_seidel_sweep<R>(g, p, xd_out);
+    return;
+  }
   for (int64_t z = 0; z < g.nz; ++z)
     for (int64_t y = 0; y < g.ny; ++y)
       for (int64_t i = 0; i < g.nx; ++i) {
@@ -228,7 +288,7 @@ void step_tangent(int kind, const Grid& g, const double* p, const R* x,
 template <class R>
 int check_problem(int kind, const Grid& g, const R* K) {
   if (g.nx < 1 || g.ny < 1 || g.nz < 1) return -1;
-  if (kind == JACOBI2D5 || kind == VARDIFF2D9) {
+  if (kind == JACOBI2D5 || kind == VARDIFF2D9 || kind == GAUSSSEIDEL2D5) {
     if (g.nz != 1) return -1;
   } else if (kind != ALLENCAHN3D7) {
     return -1;

@@ -45,6 +45,40 @@ def jacobi_matrix(ny, nx, w=0.2):
     return interior[:, None] * avg + np.diag(1.0 - interior)
 
 
+def gauss_seidel_matrix(ny, nx, w=0.2):
+    """One in-place Gauss-Seidel sweep in row-major order as the textbook
+    matrix splitting. Split the axis adjacency A = L + U into its strictly
+    lower part L (the W and S neighbours, which precede a point in row-major
+    order and so already hold new values) and strictly upper part U (E and
+    N, still old). With D the interior indicator, one sweep solves
+        (I - w D L) x' = (w D (I + U) + (I - D)) x,
+    a unit lower-triangular system (ring rows are identity rows)."""
+    n = nx * ny
+    yy, xx = np.divmod(np.arange(n), nx)
+    interior = ((xx > 0) & (xx < nx - 1) & (yy > 0) & (yy < ny - 1)).astype(float)
+    A = grid2d_axis(ny, nx)
+    L = np.tril(A, -1)
+    U = np.triu(A, 1)
+    D = np.diag(interior)
+    lhs = np.eye(n) - w * D @ L
+    rhs = w * D @ (np.eye(n) + U) + (np.eye(n) - D)
+    return np.linalg.solve(lhs, rhs)
+
+
+def laplace_dirichlet_solution(ring):
+    """Discrete harmonic function of the 5-point Laplacian with the ring of
+    `ring` as Dirichlet data (interior values of `ring` ignored): solves
+    4 u[c] - sum of the 4 neighbours = 0 on interior points."""
+    ny, nx = ring.shape
+    n = nx * ny
+    yy, xx = np.divmod(np.arange(n), nx)
+    interior = (xx > 0) & (xx < nx - 1) & (yy > 0) & (yy < ny - 1)
+    lap = 4.0 * np.eye(n) - grid2d_axis(ny, nx)
+    M = np.where(interior[:, None], lap, np.eye(n))
+    b = np.where(interior, 0.0, ring.reshape(-1))
+    return np.linalg.solve(M, b).reshape(ny, nx)
+
+
 def heat3d_matrix(nz, ny, nx, D=0.1):
     """The linear part of the Allen-Cahn step, I + D * (A - 6 I), with
     out-of-grid neighbours reading zero (Dirichlet ghost values)."""

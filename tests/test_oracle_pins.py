@@ -17,7 +17,8 @@ import numpy as np
 import pytest
 
 import oracle
-from oracle import ALLENCAHN3D7, DOT_W, HALF_SQ, HALF_SQ_DIFF, JACOBI2D5, SEED, VARDIFF2D9
+from oracle import (ALLENCAHN3D7, DOT_W, GAUSSSEIDEL2D5, HALF_SQ, HALF_SQ_DIFF, JACOBI2D5, SEED,
+                    VARDIFF2D9)
 from tests import linalg_forms as lf
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
@@ -46,6 +47,35 @@ def test_jacobi_closed_form(ny, nx, T):
     assert rel(xT, xT_ref) < 1e-13
     assert rel(dx0, dx0_ref) < 1e-13
     assert abs(L - 0.5 * np.sum(xT_ref ** 2)) <= 1e-13 * abs(L)
+
+
+@pytest.mark.parametrize("ny,nx,T", [(3, 3, 1), (4, 4, 1), (9, 11, 7), (16, 13, 10), (2, 7, 3)])
+def test_gauss_seidel_closed_form(ny, nx, T):
+    """x_T = M^T x0 and dx0 = (M^T)^T (x_T - Y) with M the matrix-splitting
+    form of one in-place sweep (a triangular solve, not a loop over points)."""
+    x0 = rng(8).uniform(0, 1, (ny, nx))
+    Y = rng(9).uniform(0, 1, (ny, nx))
+    M = lf.gauss_seidel_matrix(ny, nx)
+    MT = np.linalg.matrix_power(M, T)
+    xT_ref = MT @ x0.reshape(-1)
+    dx0_ref = MT.T @ (xT_ref - Y.reshape(-1))
+    dx0, _, xT, _ = oracle.vjp(GAUSSSEIDEL2D5, x0, steps=T, loss=HALF_SQ_DIFF, aux=Y)
+    assert rel(xT.reshape(-1), xT_ref) < 1e-13
+    assert rel(dx0.reshape(-1), dx0_ref) < 1e-13
+    # the in-place sweep is not the Jacobi step
+    if ny >= 4 and nx >= 4:
+        J = np.linalg.matrix_power(lf.jacobi_matrix(ny, nx), T)
+        assert rel(J @ x0.reshape(-1), xT_ref) > 1e-3
+
+
+def test_gauss_seidel_converges_to_harmonic():
+    """With w = 1/5 the fixed point satisfies 4 x[c] = sum of the four
+    neighbours: many sweeps reach the discrete harmonic function with the
+    ring as Dirichlet data (Gauss-Seidel converges for this system)."""
+    x0 = rng(41).uniform(0, 1, (9, 12))
+    ref = lf.laplace_dirichlet_solution(x0)
+    xT = oracle.forward(GAUSSSEIDEL2D5, x0, steps=1500)
+    assert np.max(np.abs(xT - ref)) < 1e-12
 
 
 @pytest.mark.parametrize("shape,T", [((3, 4, 5), 4), ((6, 5, 7), 6), ((1, 1, 1), 3)])
@@ -131,6 +161,12 @@ def test_fd_jacobi():
     _fd_check(JACOBI2D5, rng(10).uniform(0, 1, (6, 5)), None, 4, HALF_SQ, None, False)
 
 
+@pytest.mark.parametrize("loss", [HALF_SQ, HALF_SQ_DIFF])
+def test_fd_gauss_seidel(loss):
+    aux = rng(19).uniform(0, 1, (5, 7))
+    _fd_check(GAUSSSEIDEL2D5, rng(18).uniform(0, 1, (5, 7)), None, 5, loss, aux, False)
+
+
 @pytest.mark.parametrize("loss", [DOT_W, HALF_SQ, HALF_SQ_DIFF])
 def test_fd_allencahn(loss):
     x0 = rng(11).uniform(-1, 1, (3, 4, 5))
@@ -156,6 +192,7 @@ def test_fd_vardiff_dx0_and_dK(loss):
 # ------------------------------------------------ tangent and dot product
 @pytest.mark.parametrize("kind,shape,T,withK", [
     (JACOBI2D5, (13, 17), 6, False),
+    (GAUSSSEIDEL2D5, (13, 17), 6, False),
     (ALLENCAHN3D7, (5, 6, 7), 5, False),
     (VARDIFF2D9, (11, 15), 5, True),
 ])
@@ -178,6 +215,8 @@ def test_jvp_matches_fd(kind, shape, T, withK):
 @pytest.mark.parametrize("kind,shape,T,withK", [
     (JACOBI2D5, (13, 17), 6, False),
     (JACOBI2D5, (40, 33), 20, False),
+    (GAUSSSEIDEL2D5, (13, 17), 6, False),
+    (GAUSSSEIDEL2D5, (40, 33), 20, False),
     (ALLENCAHN3D7, (5, 6, 7), 5, False),
     (ALLENCAHN3D7, (9, 8, 10), 12, False),
     (VARDIFF2D9, (11, 15), 5, True),
@@ -201,9 +240,11 @@ def test_dot_product_identity(kind, shape, T, withK):
 
 
 # ---------------------------------------------------------------- invariants
-def test_jacobi_ones_fixed_point():
+@pytest.mark.parametrize("kind", [JACOBI2D5, GAUSSSEIDEL2D5])
+def test_ones_fixed_point(kind):
+    """0.2 rounds so that 5 * 0.2 == 1 exactly: constants stay put."""
     x = np.ones((20, 30))
-    assert np.array_equal(oracle.forward(JACOBI2D5, x, steps=25), x)
+    assert np.array_equal(oracle.forward(kind, x, steps=25), x)
 
 
 def test_vardiff_constant_fixed_point_and_conservation():
@@ -249,7 +290,8 @@ def test_linear_part_symmetric(kind, shape, params, withK):
 
 
 @pytest.mark.parametrize("kind,shape,withK", [
-    (JACOBI2D5, (5, 7), False), (ALLENCAHN3D7, (2, 3, 4), False), (VARDIFF2D9, (6, 5), True)])
+    (JACOBI2D5, (5, 7), False), (ALLENCAHN3D7, (2, 3, 4), False), (VARDIFF2D9, (6, 5), True),
+    (GAUSSSEIDEL2D5, (4, 6), False)])
 def test_zero_steps_returns_seed(kind, shape, withK):
     r = rng(35)
     x0 = r.uniform(0, 1, shape)
@@ -285,6 +327,32 @@ def test_jacobi_3x3_hand_case():
     assert L == 142.5
 
 
+def test_gauss_seidel_4x4_hand_case():
+    """4x4 grid, one sweep, w = 1/4 so every value is a dyadic rational and
+    exact in binary. Interior points in row-major order (y, x):
+      (1,1): C 0, E 0, N 0, S 2, W 5                  -> 7/4
+      (1,2): C 0, E 6, N 0, S 3, W x'(1,1) = 7/4      -> 43/16
+      (2,1): C 0, E 0, N 10, S x'(1,1) = 7/4, W 7     -> 75/16
+      (2,2): C 0, E 8, N 11, S x'(1,2), W x'(2,1)     -> 211/32
+    For the gradient of x'(2,2) (loss SEED, cotangent e_(2,2)): x0(2,2)
+    enters through C (1/4), through E of (2,1) and through N of (1,2)
+    (1/4 * 1/4 each), so dx0(2,2) = 3/8; the ring point (3,2) only through
+    N of (2,2): 1/4. x0(1,1), x0(0,1) and x0(1,0) reach x'(2,2) only through
+    x'(1,1) (as its C, S and W), then along (1,2) -> (2,2) or (2,1) -> (2,2):
+    2 * (1/4)^3 each; the corner x0(0,0) is read by nothing: 0."""
+    x0 = np.array([[1, 2, 3, 4], [5, 0, 0, 6], [7, 0, 0, 8], [9, 10, 11, 12]], dtype=float)
+    x1 = oracle.forward(GAUSSSEIDEL2D5, x0, steps=1, params=(0.25, 0.0))
+    expect = x0.copy()
+    expect[1, 1], expect[1, 2], expect[2, 1], expect[2, 2] = 7 / 4, 43 / 16, 75 / 16, 211 / 32
+    assert np.array_equal(x1, expect)
+    e = np.zeros_like(x0)
+    e[2, 2] = 1.0
+    dx0, _, _, _ = oracle.vjp(GAUSSSEIDEL2D5, x0, steps=1, loss=SEED, aux=e, params=(0.25, 0.0))
+    assert dx0[2, 2] == 3 / 8 and dx0[3, 2] == 1 / 4
+    assert dx0[1, 1] == dx0[0, 1] == dx0[1, 0] == 2 / 64
+    assert dx0[0, 0] == 0.0
+
+
 def test_allencahn_single_point_is_scalar_map():
     """On a 1x1x1 grid every neighbour is a zero ghost value and the step is
     the scalar map x' = (1-6D) x - C x^3 with derivative (1-6D) - 3 C x^2;
@@ -307,6 +375,7 @@ def test_allencahn_single_point_is_scalar_map():
 # ------------------------------------------------------------- precisions
 @pytest.mark.parametrize("kind,shape,T,withK", [
     (JACOBI2D5, (33, 47), 12, False),
+    (GAUSSSEIDEL2D5, (33, 47), 12, False),
     (ALLENCAHN3D7, (9, 10, 11), 8, False),
     (VARDIFF2D9, (37, 29), 20, True),
 ])
