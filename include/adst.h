@@ -30,6 +30,15 @@
  *                     precision); edges leaving the grid are dropped (no flux).
  *                     p[0] = dt (0.1). The per-point field K is the
  *                     coefficient ("coeff") whose gradient dK may be asked for.
+ *   ADST_GAUSSSEIDEL2D5  2-D, in place: interior points are overwritten one
+ *                     at a time in row-major order (x fastest) with
+ *                     x[c] = w*((((x[c]+x[E])+x[N])+x[S])+x[W]), so x[S] and x[W]
+ *                     already hold the current step's values; the outer ring
+ *                     is held fixed. p[0] = w (0.2). The paper's Seidel2d case
+ *                     study (Sec. V-B) is an in-place stencil of this kind: a
+ *                     dependency carried through every sweep, whose reverse
+ *                     visits the points in reverse order and clears each
+ *                     overwritten value's gradient (Sec. II, Sec. III-C).
  * Each forward formula is evaluated in the order written, in the working
  * precision, without fused multiply-add contraction.
  *
@@ -64,7 +73,12 @@ typedef enum {
   ADST_ERR_HIP = 5          /* a HIP launch or runtime call failed */
 } adst_status;
 
-typedef enum { ADST_JACOBI2D5 = 0, ADST_ALLENCAHN3D7 = 1, ADST_VARDIFF2D9 = 2 } adst_kind;
+typedef enum {
+  ADST_JACOBI2D5 = 0,
+  ADST_ALLENCAHN3D7 = 1,
+  ADST_VARDIFF2D9 = 2,
+  ADST_GAUSSSEIDEL2D5 = 3
+} adst_kind;
 typedef enum { ADST_F64 = 0, ADST_F32 = 1 } adst_dtype;
 
 /* Checkpoint schedules (Sec. IV: store-all default, a manual choice, or an
@@ -124,14 +138,22 @@ typedef struct {
  *                 else reads x_{t-1}), written to dst
  *   ADST_OP_ADJ2  g_{t-2} = J_{t-1}^T J_t^T g_t in one launch (state-free
  *                 adjoints only; src = ADST_BUF_NONE)
- * Fused actions (temporal blocking) evaluate every point with the same
- * expression as the single steps, so results are bit-identical. */
+ *   ADST_OP_FWDW  x_t from x_{t-n} in src by n steps of the in-place kind,
+ *                 pipelined in one sequence of wavefront launches (tiles of
+ *                 several steps share a launch), written to dst
+ *   ADST_OP_ADJW  g_{t-n} = J_{t-n+1}^T ... J_t^T g_t for the in-place kind,
+ *                 pipelined the same way (its adjoint reads no state)
+ * Fused and pipelined actions evaluate every point with the same expression
+ * as the single steps, so results are bit-identical. `n` is the number of
+ * steps an action covers (1 for FWD/ADJ, 2 for FWD2/ADJ2, 0 for SEED). */
 typedef enum {
   ADST_OP_FWD = 0,
   ADST_OP_SEED = 1,
   ADST_OP_ADJ = 2,
   ADST_OP_FWD2 = 3,
-  ADST_OP_ADJ2 = 4
+  ADST_OP_ADJ2 = 4,
+  ADST_OP_FWDW = 5,
+  ADST_OP_ADJW = 6
 } adst_op;
 enum {
   ADST_BUF_NONE = -1,
@@ -143,9 +165,10 @@ enum {
 };
 typedef struct {
   int32_t op;
-  int32_t t;
+  int32_t t;   /* the step the action ends at (forward) or starts from (adjoint) */
   int32_t src;
   int32_t dst;
+  int32_t n;   /* steps covered */
 } adst_action;
 
 typedef struct {
@@ -157,8 +180,10 @@ typedef struct {
   int64_t recompute_steps;  /* fwd_steps_total - T */
   int64_t adj_steps;        /* T */
   int64_t n_actions;        /* length of the action list */
-  int64_t fwd_launches;     /* forward launches (a fused pair counts once) */
-  int64_t adj_launches;     /* adjoint launches (a fused pair counts once) */
+  int64_t fwd_launches;     /* forward actions (a fused pair or a pipelined run counts once) */
+  int64_t adj_launches;     /* adjoint actions (likewise) */
+  int64_t fwd_kernels;      /* forward kernel dispatches the actions enqueue */
+  int64_t adj_kernels;      /* adjoint kernel dispatches the actions enqueue */
   uint64_t state_bytes;     /* bytes of one state */
   uint64_t budget_bytes;    /* the budget passed in */
   uint64_t slot_bytes_peak; /* slots * state_bytes: checkpoint storage actually used */
@@ -177,7 +202,10 @@ typedef struct {
  * The budget counts checkpoint-slot storage only: slots = floor(budget /
  * state_bytes); x0 is the caller's and is the free base checkpoint, so the
  * schedule has c = slots + 1 checkpoints. want_dcoeff != 0 asks for dK
- * (VARDIFF2D9 only), which makes its adjoint read x_{t-1}.
+ * (VARDIFF2D9 only), which makes its adjoint read x_{t-1}. For the in-place
+ * kind (GAUSSSEIDEL2D5, linear) nothing is stored: the plan is one pipelined
+ * forward run, the seed and one pipelined reverse run (FWDW, SEED, ADJW);
+ * with ADST_FORCE_TAPE it is a per-step checkpointed plan like the others.
  * Errors: ADST_ERR_ARG (NULL prob/out, steps < 0, bad kind/dtype/sched, bad
  * shape), ADST_ERR_UNSUPPORTED (shape not valid for the kind, or dK asked for
  * a kind without a coefficient field), ADST_ERR_BUDGET (STORE_ALL does not fit). */
@@ -193,7 +221,8 @@ adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t 
 
 /* x_T after `steps` forward steps (the unmodified program). coeff is K for
  * VARDIFF2D9 and must be NULL-or-ignored otherwise. ws must hold
- * adst_plan_info.fwd_workspace_bytes (one state when steps >= 2, else 0).
+ * adst_plan_info.fwd_workspace_bytes (one state when steps >= 2, else 0;
+ * always 0 for the in-place kind, which runs in xT).
  * Errors: as adst_plan, plus ADST_ERR_WORKSPACE and ADST_ERR_HIP. */
 adst_status adst_forward(const adst_problem* prob, const void* x0, const void* coeff,
                          int32_t steps, void* xT, void* ws, uint64_t ws_bytes,
@@ -203,7 +232,8 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
  * `stream`. Outputs: dx0 (required), dcoeff (dK, VARDIFF2D9 only, NULL = not
  * requested), xT (optional), loss_dev (optional device double). ws must hold
  * adst_plan_info.workspace_bytes and is clobbered. dx0 doubles as one of the
- * two adjoint buffers. steps = 0 is valid: dx0 = seed, dK = 0.
+ * two adjoint buffers (for the in-place kind, the only one: the reverse
+ * sweeps run in place in dx0). steps = 0 is valid: dx0 = seed, dK = 0.
  * info (optional, host) receives the plan; with ADST_TRACE it also receives
  * the per-phase kernel times, and the call synchronises the stream.
  * Errors: as adst_plan, plus ADST_ERR_ARG for overlapping input/output ranges

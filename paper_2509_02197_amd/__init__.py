@@ -17,12 +17,12 @@ LIB_PATH = os.path.join(_HERE, "libadst.so")
 
 # enums of adst.h
 ADST_OK, ADST_ERR_ARG, ADST_ERR_BUDGET, ADST_ERR_WORKSPACE, ADST_ERR_UNSUPPORTED, ADST_ERR_HIP = range(6)
-ADST_JACOBI2D5, ADST_ALLENCAHN3D7, ADST_VARDIFF2D9 = 0, 1, 2
+ADST_JACOBI2D5, ADST_ALLENCAHN3D7, ADST_VARDIFF2D9, ADST_GAUSSSEIDEL2D5 = 0, 1, 2, 3
 ADST_F64, ADST_F32 = 0, 1
 ADST_SCHED_AUTO, ADST_SCHED_STORE_ALL, ADST_SCHED_UNIFORM, ADST_SCHED_BINOMIAL = 0, 1, 2, 3
 ADST_LOSS_HALF_SQ, ADST_LOSS_DOT_W, ADST_LOSS_HALF_SQ_DIFF, ADST_LOSS_SEED = 0, 1, 2, 3
 ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE = 0x1, 0x2, 0x4
-ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2 = 0, 1, 2, 3, 4
+ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2, ADST_OP_FWDW, ADST_OP_ADJW = range(7)
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
 EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
@@ -38,7 +38,7 @@ class adst_problem(ctypes.Structure):
 
 class adst_action(ctypes.Structure):
     _fields_ = [("op", ctypes.c_int32), ("t", ctypes.c_int32), ("src", ctypes.c_int32),
-                ("dst", ctypes.c_int32)]
+                ("dst", ctypes.c_int32), ("n", ctypes.c_int32)]
 
 
 class adst_plan_info(ctypes.Structure):
@@ -46,7 +46,8 @@ class adst_plan_info(ctypes.Structure):
                 ("needs_state", ctypes.c_int32), ("fwd_steps_total", ctypes.c_int64),
                 ("recompute_steps", ctypes.c_int64), ("adj_steps", ctypes.c_int64),
                 ("n_actions", ctypes.c_int64), ("fwd_launches", ctypes.c_int64),
-                ("adj_launches", ctypes.c_int64), ("state_bytes", ctypes.c_uint64),
+                ("adj_launches", ctypes.c_int64), ("fwd_kernels", ctypes.c_int64),
+                ("adj_kernels", ctypes.c_int64), ("state_bytes", ctypes.c_uint64),
                 ("budget_bytes", ctypes.c_uint64), ("slot_bytes_peak", ctypes.c_uint64),
                 ("workspace_bytes", ctypes.c_uint64), ("fwd_workspace_bytes", ctypes.c_uint64),
                 ("alg_bytes", ctypes.c_uint64), ("ms_fwd_sweep", ctypes.c_float),
@@ -162,7 +163,7 @@ def adst_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
 
 
 def adst_plan_actions(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
-    """The plan's action list as a list of (op, t, src, dst) tuples."""
+    """The plan's action list as a list of (op, t, src, dst, n) tuples."""
     n = ctypes.c_int64(0)
     L = lib()
     _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
@@ -170,7 +171,7 @@ def adst_plan_actions(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
     buf = (adst_action * max(n.value, 1))()
     _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
                                int(want_dcoeff), buf, n.value, ctypes.byref(n)))
-    return [(a.op, a.t, a.src, a.dst) for a in buf[:n.value]]
+    return [(a.op, a.t, a.src, a.dst, a.n) for a in buf[:n.value]]
 
 
 def adst_forward(prob, x0, coeff, steps, xT, ws, ws_bytes, stream=None):
@@ -239,11 +240,13 @@ def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
 
 
 def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_bytes=None,
-        sched=ADST_SCHED_AUTO, want_dcoeff=False, params=None, flags=0, stream=None, ws=None):
+        sched=ADST_SCHED_AUTO, want_dcoeff=False, params=None, flags=0, stream=None, ws=None,
+        want_xT=True):
     """Allocate outputs and workspace with torch and run adst_vjp.
 
     budget_bytes=None means unlimited (store-all). Returns a dict with dx0,
-    dK (or None), xT, loss (0-d device tensor), info and the workspace."""
+    dK (or None), xT (None unless want_xT), loss (0-d device tensor), info
+    and the workspace."""
     import torch
     prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags)
     if budget_bytes is None:
@@ -253,7 +256,7 @@ def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_
         ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=x0.device)
     dx0 = torch.empty_like(x0)
     dK = torch.empty_like(x0) if want_dcoeff else None
-    xT = torch.empty_like(x0)
+    xT = torch.empty_like(x0) if want_xT else None
     L = torch.empty((), dtype=torch.float64, device=x0.device)
     info = adst_vjp(prob, x0, coeff, steps, loss, aux, budget_bytes, sched, dx0, dK, xT, L, ws,
                     ws.numel(), stream)

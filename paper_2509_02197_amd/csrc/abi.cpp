@@ -46,11 +46,12 @@ struct Checked {
   bool needs_state = false;
   bool trace = false;
   bool fuse_fwd = false, fuse_adj = false;
+  bool in_place = false;  // the Gauss-Seidel kind: pipelined sweeps, adjoint in place
 };
 
 adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* out) {
   if (!p) return fail(ADST_ERR_ARG, "problem is NULL");
-  if (p->kind < ADST_JACOBI2D5 || p->kind > ADST_VARDIFF2D9)
+  if (p->kind < ADST_JACOBI2D5 || p->kind > ADST_GAUSSSEIDEL2D5)
     return fail(ADST_ERR_ARG, "unknown kind " + std::to_string(p->kind));
   if (p->dtype != ADST_F64 && p->dtype != ADST_F32)
     return fail(ADST_ERR_ARG, "unknown dtype " + std::to_string(p->dtype));
@@ -62,7 +63,7 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
     return fail(ADST_ERR_ARG, "extent too large");
   const int64_t n = p->n[0] * p->n[1] * p->n[2];
   if (n >= (int64_t(1) << 31)) return fail(ADST_ERR_ARG, "grid must have fewer than 2^31 points");
-  if ((p->kind == ADST_JACOBI2D5 || p->kind == ADST_VARDIFF2D9) && p->n[2] != 1)
+  if (p->kind != ADST_ALLENCAHN3D7 && p->n[2] != 1)
     return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
   // Every launch covers the grid with workgroups of 256 work-items: tiles of
   // 252 or 256 columns by 4 or 8 rows for the 2-D kinds, columns of 62 or 64
@@ -86,6 +87,7 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
   const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
   out->fuse_fwd = fuse && has_forward2(p->kind);
   out->fuse_adj = fuse && has_adjoint2(p->kind);
+  out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
   return ADST_OK;
 }
 
@@ -94,6 +96,9 @@ struct Layout {
   uint64_t w0 = 0, w1 = 0, g = 0, slot0 = 0, total = 0;
 };
 
+// Header, two work states, the second adjoint buffer G, then the slots. The
+// in-place kind keeps its gradient in dx0 (no G) and needs the work states
+// only for a forced tape: its pipelined plan runs x0 -> x_T directly.
 Layout layout_for(const Checked& c, const Plan& plan) {
   Layout L;
   L.state_stride = align_up(c.state_bytes);
@@ -101,10 +106,11 @@ Layout layout_for(const Checked& c, const Plan& plan) {
     L.total = kHeaderBytes;
     return L;
   }
+  const uint64_t nwork = (c.in_place && !plan.needs_state) ? 0 : 2;
   L.w0 = kHeaderBytes;
-  L.w1 = L.w0 + L.state_stride;
-  L.g = L.w1 + L.state_stride;
-  L.slot0 = L.g + L.state_stride;
+  L.w1 = L.w0 + (nwork ? L.state_stride : 0);
+  L.g = L.w1 + (nwork ? L.state_stride : 0);
+  L.slot0 = L.g + (c.in_place ? 0 : L.state_stride);
   L.total = L.slot0 + uint64_t(plan.slots) * L.state_stride;
   return L;
 }
@@ -116,6 +122,7 @@ void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd
   const uint64_t s = itemsize(c.shape.dtype);
   switch (c.shape.kind) {
     case ADST_JACOBI2D5:
+    case ADST_GAUSSSEIDEL2D5:  // in place: read and write each point once per step
       *fwd = 2 * s;
       *adj = *adj_first = 2 * s;
       break;
@@ -148,15 +155,46 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
   info->n_actions = (int64_t)plan.acts.size();
   info->fwd_launches = plan.fwd_launches;
   info->adj_launches = plan.adj_launches;
+  for (const adst_action& a : plan.acts) {
+    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
+    const bool adj_op = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJ2 || a.op == ADST_OP_ADJW;
+    if (!fwd_op && !adj_op) continue;
+    const int64_t k = c.in_place ? gs_kernel_launches(c.shape, adj_op, a.n) : 1;
+    (fwd_op ? info->fwd_kernels : info->adj_kernels) += k;
+  }
   info->state_bytes = c.state_bytes;
   info->budget_bytes = budget;
   info->slot_bytes_peak = uint64_t(plan.slots) * c.state_bytes;
   info->workspace_bytes = L.total;
-  info->fwd_workspace_bytes = plan.steps >= 2 ? c.state_bytes : 0;
-  // A fused launch moves its inputs and outputs once for two steps.
+  info->fwd_workspace_bytes = (plan.steps >= 2 && !c.in_place) ? c.state_bytes : 0;
+  // A fused launch moves its inputs and outputs once for two steps; a
+  // pipelined run of the in-place kind is counted as its n steps.
   const uint64_t n = uint64_t(c.npoints);
-  uint64_t adj_total = plan.adj_launches > 0 ? ab1 + uint64_t(plan.adj_launches - 1) * ab : 0;
-  info->alg_bytes = n * (uint64_t(plan.fwd_launches) * fb + adj_total + sb);
+  uint64_t per_point = sb;
+  bool first_adj = true;
+  for (const adst_action& a : plan.acts) {
+    switch (a.op) {
+      case ADST_OP_FWD:
+      case ADST_OP_FWD2:
+        per_point += fb;
+        break;
+      case ADST_OP_FWDW:
+        per_point += uint64_t(a.n) * fb;
+        break;
+      case ADST_OP_ADJ:
+      case ADST_OP_ADJ2:
+        per_point += first_adj ? ab1 : ab;
+        first_adj = false;
+        break;
+      case ADST_OP_ADJW:
+        per_point += uint64_t(a.n) * ab;
+        first_adj = false;
+        break;
+      default:
+        break;
+    }
+  }
+  info->alg_bytes = n * per_point;
 }
 
 adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
@@ -166,7 +204,8 @@ adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, 
   if (steps < 0) return fail(ADST_ERR_ARG, "steps must be >= 0");
   const int64_t slots_avail = (int64_t)std::min<uint64_t>(budget / c->state_bytes, INT32_MAX);
   std::string err;
-  st = build_plan(steps, slots_avail, sched, c->needs_state, c->fuse_fwd, c->fuse_adj, plan, &err);
+  st = build_plan(steps, slots_avail, sched, c->needs_state, c->fuse_fwd, c->fuse_adj,
+                  c->in_place, plan, &err);
   if (st != ADST_OK) return fail(st, err);
   return ADST_OK;
 }
@@ -317,7 +356,7 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
   if (prob->kind == ADST_VARDIFF2D9 && !coeff)
     return fail(ADST_ERR_ARG, "the variable-coefficient kind needs coeff (K)");
   const uint64_t S = c.state_bytes;
-  const uint64_t need = steps >= 2 ? S : 0;
+  const uint64_t need = (steps >= 2 && !c.in_place) ? S : 0;
   if (ws_bytes < need || (need && !ws))
     return fail(ADST_ERR_WORKSPACE, "adst_forward needs " + std::to_string(need) + " workspace bytes");
   std::vector<Range> outs = {range_of("xT", xT, S)};
@@ -331,6 +370,12 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
   if (steps == 0) {
     e = launch_copy(xT, x0, (int64_t)S, stream);
     if (e != hipSuccess) return hip_fail(e, "copy");
+    g_last_error.clear();
+    return ADST_OK;
+  }
+  if (c.in_place) {  // pipelined sweeps from x0 straight into xT
+    e = launch_gs_forward(c.shape, x0, xT, steps, stream);
+    if (e != hipSuccess) return hip_fail(e, "forward sweeps");
     g_last_error.clear();
     return ADST_OK;
   }
@@ -390,11 +435,12 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   // ---- interpret the plan
   // The adjoint ping-pongs between dx0 and the workspace buffer G, one swap
   // per adjoint launch; g_T starts where the last launch leaves g_0 in dx0.
+  // The in-place kind reverses its sweeps in dx0 itself.
   char* wsb = static_cast<char*>(ws);
   double* partials = reinterpret_cast<double*>(wsb);
   double* loss_out = loss_dev ? loss_dev : reinterpret_cast<double*>(wsb + kLossOffset);
   void* gws = wsb + L.g;
-  void* gcur = (plan.adj_launches % 2 == 0) ? dx0 : gws;
+  void* gcur = (c.in_place || plan.adj_launches % 2 == 0) ? dx0 : gws;
   void* gnext = (gcur == dx0) ? gws : dx0;
   void* const g_T = gcur;
   auto buffer = [&](int32_t id) -> void* {
@@ -411,11 +457,21 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   bool seeded = false;
   hipError_t e = hipSuccess;
   for (const adst_action& a : plan.acts) {
-    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2;
+    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
     const Tracer::Cat cat = fwd_op               ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
                             : a.op == ADST_OP_SEED ? Tracer::SEED
                                                    : Tracer::ADJ;
     if ((e = tr.before(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
+    if (c.in_place && a.op != ADST_OP_SEED) {
+      if (a.op == ADST_OP_FWD || a.op == ADST_OP_FWDW)
+        e = launch_gs_forward(c.shape, buffer(a.src), buffer(a.dst), a.n, stream);
+      else if (a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJW)
+        e = launch_gs_adjoint(c.shape, dx0, a.n, stream);
+      else
+        e = hipErrorInvalidValue;
+      if (e != hipSuccess) return hip_fail(e, "kernel launch");
+      continue;
+    }
     switch (a.op) {
       case ADST_OP_FWD:
         e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);

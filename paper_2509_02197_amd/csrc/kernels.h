@@ -51,6 +51,15 @@ hipError_t launch_seed(int32_t dtype, int32_t loss, int64_t n, const void* x, co
 hipError_t launch_finalize(const double* partials, int32_t nparts, double* loss,
                            hipStream_t stream);
 
+// In-place Gauss-Seidel kind: `sweeps` forward sweeps from src into dst
+// (src may equal dst), and `sweeps` reverse sweeps applied to g in place.
+// Each call is a sequence of wavefront launches (gs_kernel_launches of them)
+// that pipelines the sweeps.
+hipError_t launch_gs_forward(const StepShape& s, const void* src, void* dst, int32_t sweeps,
+                             hipStream_t stream);
+hipError_t launch_gs_adjoint(const StepShape& s, void* g, int32_t sweeps, hipStream_t stream);
+int64_t gs_kernel_launches(const StepShape& s, bool adjoint, int32_t sweeps);
+
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream);
 

@@ -73,13 +73,13 @@ class Builder {
   void release_slot(int32_t b) { free_.push_back(b); }
 
   void fwd(int32_t t, int32_t src, int32_t dst) {
-    acts.push_back({ADST_OP_FWD, t, src, dst});
+    acts.push_back({ADST_OP_FWD, t, src, dst, 1});
     ++nfwd;
     ++fwd_launches;
   }
   // Steps t-1 and t in one launch; x_{t-1} is never materialised.
   void fwd2(int32_t t, int32_t src, int32_t dst) {
-    acts.push_back({ADST_OP_FWD2, t, src, dst});
+    acts.push_back({ADST_OP_FWD2, t, src, dst, 2});
     nfwd += 2;
     ++fwd_launches;
   }
@@ -116,12 +116,12 @@ class Builder {
       fwd(T_, xbuf, ADST_BUF_XT);
       seed();
     }
-    acts.push_back({ADST_OP_ADJ, t, needs_state_ ? xbuf : ADST_BUF_NONE, ADST_BUF_NONE});
+    acts.push_back({ADST_OP_ADJ, t, needs_state_ ? xbuf : ADST_BUF_NONE, ADST_BUF_NONE, 1});
     ++adj_launches;
   }
 
   void seed() {
-    acts.push_back({ADST_OP_SEED, T_, ADST_BUF_XT, ADST_BUF_NONE});
+    acts.push_back({ADST_OP_SEED, T_, ADST_BUF_XT, ADST_BUF_NONE, 0});
     seeded_ = true;
   }
 
@@ -216,17 +216,29 @@ class Builder {
     int32_t t = T_;
     while (t >= 1) {
       if (fuse_adj_ && t >= 2) {
-        acts.push_back({ADST_OP_ADJ2, t, ADST_BUF_NONE, ADST_BUF_NONE});
+        acts.push_back({ADST_OP_ADJ2, t, ADST_BUF_NONE, ADST_BUF_NONE, 2});
         t -= 2;
       } else {
-        acts.push_back({ADST_OP_ADJ, t, ADST_BUF_NONE, ADST_BUF_NONE});
+        acts.push_back({ADST_OP_ADJ, t, ADST_BUF_NONE, ADST_BUF_NONE, 1});
         t -= 1;
       }
       ++adj_launches;
     }
   }
 
-  void zero_steps() { acts.push_back({ADST_OP_SEED, 0, ADST_BUF_X0, ADST_BUF_NONE}); }
+  // The in-place kind without a tape: its T steps run as one pipelined
+  // forward sequence straight into x_T, then the seed, then one pipelined
+  // reverse sequence.
+  void pipelined() {
+    acts.push_back({ADST_OP_FWDW, T_, ADST_BUF_X0, ADST_BUF_XT, T_});
+    nfwd += T_;
+    ++fwd_launches;
+    seed();
+    acts.push_back({ADST_OP_ADJW, T_, ADST_BUF_NONE, ADST_BUF_NONE, T_});
+    ++adj_launches;
+  }
+
+  void zero_steps() { acts.push_back({ADST_OP_SEED, 0, ADST_BUF_X0, ADST_BUF_NONE, 0}); }
 
  private:
   int32_t T_;
@@ -254,7 +266,8 @@ constexpr int64_t kMaxActions = int64_t(1) << 24;
 }  // namespace
 
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       bool fuse_fwd, bool fuse_adj, Plan* out, std::string* err) {
+                       bool fuse_fwd, bool fuse_adj, bool pipelined, Plan* out,
+                       std::string* err) {
   if (steps < 0) {
     *err = "steps must be >= 0";
     return ADST_ERR_ARG;
@@ -286,6 +299,8 @@ adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool n
   Builder b(steps, needs_state, fuse_fwd, fuse_adj && !needs_state);
   if (steps == 0) {
     b.zero_steps();
+  } else if (!needs_state && pipelined) {
+    b.pipelined();
   } else if (!needs_state) {
     b.elided();
   } else if (resolved == ADST_SCHED_STORE_ALL) {

@@ -34,9 +34,12 @@ inline int64_t store_all_slots(int64_t T) { return T > 2 ? T - 2 : 0; }
 // Build the action list. slots_avail is the number of checkpoint slots the
 // budget allows (x0 excluded). sched may be AUTO. fuse_fwd lets two forward
 // steps whose intermediate state nothing reads share one launch (FWD2);
-// fuse_adj does the same for state-free adjoint steps (ADJ2). Returns ADST_OK
-// or ADST_ERR_BUDGET / ADST_ERR_ARG / ADST_ERR_UNSUPPORTED with *err filled.
+// fuse_adj does the same for state-free adjoint steps (ADJ2). pipelined (the
+// in-place kind) turns a state-free plan into one pipelined forward run and
+// one pipelined reverse run (FWDW, ADJW). Returns ADST_OK or ADST_ERR_BUDGET
+// / ADST_ERR_ARG / ADST_ERR_UNSUPPORTED with *err filled.
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       bool fuse_fwd, bool fuse_adj, Plan* out, std::string* err);
+                       bool fuse_fwd, bool fuse_adj, bool pipelined, Plan* out,
+                       std::string* err);
 
 }  // namespace adst

@@ -1,6 +1,6 @@
 """Seeded synthetic workloads: shapes, step counts, budgets and input arrays.
 
-This module holds none of the method's arithmetic. It only names the five
+This module holds none of the method's arithmetic. It only names the
 workloads and draws their inputs, so that the GPU path, the CPU oracle and
 the benchmark all see the same arrays.
 
@@ -13,13 +13,15 @@ from typing import Dict, Optional, Tuple
 
 import numpy as np
 
-JACOBI2D5, ALLENCAHN3D7, VARDIFF2D9 = 0, 1, 2
+JACOBI2D5, ALLENCAHN3D7, VARDIFF2D9, GAUSSSEIDEL2D5 = 0, 1, 2, 3
 F64, F32 = 0, 1
 HALF_SQ, DOT_W, HALF_SQ_DIFF, SEED = 0, 1, 2, 3
 SCHED_AUTO, SCHED_STORE_ALL, SCHED_UNIFORM, SCHED_BINOMIAL = 0, 1, 2, 3
 
-KIND_NAMES = {JACOBI2D5: "jacobi2d5", ALLENCAHN3D7: "allencahn3d7", VARDIFF2D9: "vardiff2d9"}
-DEFAULT_PARAMS = {JACOBI2D5: (0.2, 0.0), ALLENCAHN3D7: (0.1, 0.1), VARDIFF2D9: (0.1, 0.0)}
+KIND_NAMES = {JACOBI2D5: "jacobi2d5", ALLENCAHN3D7: "allencahn3d7", VARDIFF2D9: "vardiff2d9",
+              GAUSSSEIDEL2D5: "gaussseidel2d5"}
+DEFAULT_PARAMS = {JACOBI2D5: (0.2, 0.0), ALLENCAHN3D7: (0.1, 0.1), VARDIFF2D9: (0.1, 0.0),
+                  GAUSSSEIDEL2D5: (0.2, 0.0)}
 
 
 @dataclass(frozen=True)
@@ -99,6 +101,18 @@ WORKLOADS: Dict[str, Workload] = {
         budget_bytes=64_000_000_000, sched=SCHED_BINOMIAL, want_dK=False,
         x0=Dist("uniform", 7, -1.0, 1.0), aux=Dist("normal", 8),
         params=DEFAULT_PARAMS[ALLENCAHN3D7]),
+    # In-place 5-point Gauss-Seidel, fp64, at the size of the paper's Seidel2d
+    # case study (N = 400, 100 time steps, Sec. V-B). Linear: nothing is
+    # stored at any budget.
+    "gaussseidel2d5_f64_400x400_T100": Workload(
+        "gaussseidel2d5_f64_400x400_T100", GAUSSSEIDEL2D5, F64, (400, 400), 100, HALF_SQ,
+        budget_bytes=0, sched=SCHED_AUTO, want_dK=False,
+        x0=Dist("uniform", 9), params=DEFAULT_PARAMS[GAUSSSEIDEL2D5]),
+    # The same sweep on a grid that fills the GPU (128 MiB per state).
+    "gaussseidel2d5_f64_4096x4096_T100": Workload(
+        "gaussseidel2d5_f64_4096x4096_T100", GAUSSSEIDEL2D5, F64, (4096, 4096), 100, HALF_SQ,
+        budget_bytes=0, sched=SCHED_AUTO, want_dK=False,
+        x0=Dist("uniform", 10), params=DEFAULT_PARAMS[GAUSSSEIDEL2D5]),
 }
 
 # The workload the headline metric is quoted on (fits one GPU).

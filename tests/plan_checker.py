@@ -12,11 +12,15 @@ checks what makes a plan correct, independently of how it was built:
   * a fused forward pair (FWD2, steps t-1 and t) reads x_{t-2} and leaves
     x_{t-1} nowhere, so any later use of x_{t-1} fails the checks above;
     a fused adjoint pair (ADJ2, steps t and t-1) only appears for
-    state-free adjoints.
+    state-free adjoints;
+  * a pipelined forward run (FWDW, steps t-n+1..t) reads x_{t-n} and leaves
+    only x_t behind; a pipelined reverse run (ADJW, steps t..t-n+1) is
+    state-free;
+  * every action's step count n matches its op.
 Returns the forward-step count and the set of slots touched.
 """
 X0, W0, W1, XT, SLOT0 = 0, 1, 2, 3, 4
-FWD, SEED, ADJ, FWD2, ADJ2 = 0, 1, 2, 3, 4
+FWD, SEED, ADJ, FWD2, ADJ2, FWDW, ADJW = 0, 1, 2, 3, 4, 5, 6
 NONE = -1
 
 
@@ -26,9 +30,11 @@ def replay(actions, T, needs_state, max_slots):
     next_adj = T
     nfwd = 0
     slots = set()
-    for k, (op, t, src, dst) in enumerate(actions):
-        if op in (FWD, FWD2):
-            n = 1 if op == FWD else 2
+    for k, (op, t, src, dst, n) in enumerate(actions):
+        if op in (FWD, FWD2, FWDW):
+            if op != FWDW:
+                assert n == (1 if op == FWD else 2), f"action {k}: step count {n}"
+            assert n >= 1
             assert not (seeded and src == XT), f"action {k}: reads x_T buffer after the seed"
             assert holds.get(src) == t - n, f"action {k}: FWD {t} reads buffer {src} holding {holds.get(src)}"
             assert dst not in (X0, src, NONE), f"action {k}: bad destination {dst}"
@@ -40,6 +46,7 @@ def replay(actions, T, needs_state, max_slots):
             holds[dst] = t
             nfwd += n
         elif op == SEED:
+            assert n == 0
             assert not seeded, "seeded twice"
             assert holds.get(src) == T, f"seed reads buffer {src} holding {holds.get(src)}"
             seeded = True
@@ -47,6 +54,7 @@ def replay(actions, T, needs_state, max_slots):
                 assert src == XT
                 holds[XT] = None  # now holds g_T
         elif op == ADJ:
+            assert n == 1
             assert seeded, "adjoint before seed"
             assert t == next_adj, f"adjoint {t} out of order (expected {next_adj})"
             if needs_state:
@@ -55,9 +63,14 @@ def replay(actions, T, needs_state, max_slots):
                 assert src == NONE
             next_adj -= 1
         elif op == ADJ2:
+            assert n == 2
             assert seeded and not needs_state and src == NONE
             assert t == next_adj and t >= 2, f"fused adjoint {t} out of order"
             next_adj -= 2
+        elif op == ADJW:
+            assert seeded and not needs_state and src == NONE
+            assert t == next_adj and 1 <= n <= t, f"pipelined adjoint {t}/{n} out of order"
+            next_adj -= n
         else:
             raise AssertionError(f"unknown op {op}")
     assert seeded

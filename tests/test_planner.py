@@ -108,6 +108,61 @@ def test_linear_kind_elides_the_tape():
     assert nfwd == cp.forward_steps_binomial(37, 4)
 
 
+GS = adst.ADST_GAUSSSEIDEL2D5
+
+
+def gs_levels(nx, ny, itemsize, phases):
+    """Wavefront launches of one pipelined run: tiles of 64 lanes x 16 bytes
+    by 32 rows, levels tau = I + 3 J + 3 s."""
+    V = 16 // itemsize
+    nb = -(-nx // V)
+    nti, ntj = -(-(ny + 63) // 32), -(-nb // 64)
+    return (nti - 1) + 3 * (ntj - 1) + 3 * (phases - 1) + 1
+
+
+@pytest.mark.parametrize("dims,dtype", [((6, 5, 1), F64), ((400, 400, 1), F64),
+                                        ((4096, 4096, 1), F64), ((301, 70, 1), adst.ADST_F32)])
+def test_in_place_kind_plans_one_pipelined_run_each_way(dims, dtype):
+    """The Gauss-Seidel kind is linear: at every budget and schedule the plan
+    is one pipelined forward run to x_T, the seed and one pipelined reverse
+    run, with nothing stored and no work states."""
+    p = prob(GS, dims, dtype)
+    isz = 8 if dtype == F64 else 4
+    n = dims[0] * dims[1]
+    for T in (1, 2, 7, 100):
+        for sched in range(4):
+            for slots in (0, 5):
+                acts = adst.adst_plan_actions(p, T, budget_for(slots, p), sched)
+                assert acts == [(adst.ADST_OP_FWDW, T, adst.ADST_BUF_X0, adst.ADST_BUF_XT, T),
+                                (adst.ADST_OP_SEED, T, adst.ADST_BUF_XT, adst.ADST_BUF_NONE, 0),
+                                (adst.ADST_OP_ADJW, T, adst.ADST_BUF_NONE, adst.ADST_BUF_NONE, T)]
+                nfwd, used = replay(acts, T, False, 0)
+                assert nfwd == T and not used
+        info = adst.adst_plan(p, T, 0, adst.ADST_SCHED_AUTO)
+        assert info.workspace_bytes == 16384 and info.fwd_workspace_bytes == 0
+        assert info.fwd_launches == info.adj_launches == 1
+        assert info.fwd_kernels == gs_levels(dims[0], dims[1], isz, T)
+        assert info.adj_kernels == gs_levels(dims[0], dims[1], isz, T + 1)
+        # read and write every point once per step each way, plus the seed
+        assert info.alg_bytes == n * isz * (2 * T + 2 * T + 2)
+
+
+def test_in_place_kind_with_forced_tape_uses_the_schedule():
+    p = prob(GS, (9, 7, 1), flags=adst.ADST_FORCE_TAPE)
+    S = 9 * 7 * 8
+    stride = -(-S // 4096) * 4096
+    for sched, slots in ((adst.ADST_SCHED_BINOMIAL, 3), (adst.ADST_SCHED_UNIFORM, 3),
+                         (adst.ADST_SCHED_STORE_ALL, 35)):
+        acts = adst.adst_plan_actions(p, 37, budget_for(slots, p), sched)
+        nfwd, used = replay(acts, 37, True, slots)
+        info = adst.adst_plan(p, 37, budget_for(slots, p), sched)
+        assert info.fwd_steps_total == nfwd and info.adj_kernels == 37 * gs_levels(9, 7, 8, 2)
+        assert info.fwd_kernels == nfwd * gs_levels(9, 7, 8, 1)
+        # work states and slots, but no second gradient buffer
+        assert info.workspace_bytes == 16384 + (2 + info.slots) * stride
+    assert nfwd == 37
+
+
 def test_auto_picks_store_all_when_it_fits():
     p = prob()
     info = adst.adst_plan(p, 20, budget_for(18), adst.ADST_SCHED_AUTO)
@@ -150,7 +205,7 @@ def test_workspace_and_bytes():
 
 def test_zero_steps_plan():
     acts = adst.adst_plan_actions(prob(), 0, 0, adst.ADST_SCHED_AUTO)
-    assert acts == [(adst.ADST_OP_SEED, 0, adst.ADST_BUF_X0, adst.ADST_BUF_NONE)]
+    assert acts == [(adst.ADST_OP_SEED, 0, adst.ADST_BUF_X0, adst.ADST_BUF_NONE, 0)]
 
 
 @pytest.mark.parametrize("kind,flags,sched,slots", [
