@@ -30,7 +30,9 @@ KERNELS = {  # (forward, adjoint) kernel names as rocprofv3 reports them
     0: ("fwd_jacobi2d5", "adj_jacobi2d5"),
     1: ("fwd_allencahn3d7", "adj_allencahn3d7"),
     2: ("fwd_vardiff2d9", "adj_vardiff2d9"),
+    3: ("gs_wave<fwd>", "gs_wave<adj>"),
 }
+KERNEL_SOURCE = {0: "kernels.hip", 1: "kernels.hip", 2: "kernels.hip", 3: "gauss_seidel.hip"}
 
 
 def parse():
@@ -53,15 +55,15 @@ def parse():
     return ap.parse_args()
 
 
-def source_sha():
+def source_sha(kind):
+    """Hash of the source file holding the kind's kernels."""
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.h"):
-        with open(os.path.join(ROOT, "paper_2509_02197_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    with open(os.path.join(ROOT, "paper_2509_02197_amd", "csrc", KERNEL_SOURCE[kind]), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_for(workload, kernel, launches_per_call):
+def traffic_for(workload, kernel, kind):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     or None when none exists for this kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -70,7 +72,7 @@ def traffic_for(workload, kernel, launches_per_call):
     with open(path) as f:
         table = json.load(f)
     e = table.get(f"{workload}:{kernel}")
-    if not e or e.get("src_sha") != source_sha():
+    if not e or e.get("src_sha") != source_sha(kind):
         return None
     return e["bytes_per_launch"]
 
@@ -175,15 +177,21 @@ def main():
         ti = call(tprob)
         for k in acc:
             acc[k] += getattr(ti, k) / args.steps
-    # Roofline of the dominant kernel: algorithmic bytes of one launch (its
-    # inputs read once and its output written once; a fused two-step launch
-    # moves the same bytes as a single step) over its average launch time.
+    # Roofline of the dominant kernel: its algorithmic bytes (inputs read
+    # once and outputs written once per launch; a fused two-step launch
+    # moves the same bytes as a single step; the in-place kind's pipelined
+    # runs move 2 * itemsize per point per step) over its launch time.
+    # avg_launch_ms is that time over the kernel dispatches.
     isz = 8 if w.dtype == adst.ADST_F64 else 4
-    fwd_B = {0: 2, 1: 2, 2: 3}[w.kind] * isz
-    adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3}[w.kind] * isz
-    n_fwd, n_adj = info.fwd_launches, info.adj_launches
-    fused_fwd = info.fwd_steps_total - info.fwd_launches
-    fused_adj = info.adj_steps - info.adj_launches
+    fwd_B = {0: 2, 1: 2, 2: 3, 3: 2}[w.kind] * isz
+    adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3, 3: 2}[w.kind] * isz
+    in_place = w.kind == adst.ADST_GAUSSSEIDEL2D5
+    # units of fwd_B * npoints moved per call: one per launch, or one per step
+    fwd_units = info.fwd_steps_total if in_place else info.fwd_launches
+    adj_units = info.adj_steps if in_place else info.adj_launches
+    n_fwd, n_adj = info.fwd_kernels, info.adj_kernels
+    fused_fwd = 0 if in_place else info.fwd_steps_total - info.fwd_launches
+    fused_adj = 0 if in_place else info.adj_steps - info.adj_launches
     ms_fwd = acc["ms_fwd_sweep"] + acc["ms_fwd_recompute"]
     fwd_avg = ms_fwd / max(n_fwd, 1)
     adj_avg = acc["ms_adj"] / max(n_adj, 1)
@@ -195,22 +203,28 @@ def main():
         return base + "_x2" if fused == n else base + " + " + base + "_x2"
 
     if ms_fwd >= acc["ms_adj"]:
-        kernel, avg_ms, per_pt, nl, ns = (launched(kname[0], n_fwd, fused_fwd), fwd_avg, fwd_B,
-                                          n_fwd, info.fwd_steps_total)
+        kernel, ms_k, per_pt, units, nl, ns = (launched(kname[0], info.fwd_launches, fused_fwd),
+                                               ms_fwd, fwd_B, fwd_units, n_fwd,
+                                               info.fwd_steps_total)
     else:
-        kernel, avg_ms, per_pt, nl, ns = (launched(kname[1], n_adj, fused_adj), adj_avg, adj_B,
-                                          n_adj, info.adj_steps)
-    alg_bytes = per_pt * w.npoints
-    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
-    traffic = traffic_for(name, kernel, 1)
+        kernel, ms_k, per_pt, units, nl, ns = (launched(kname[1], info.adj_launches, fused_adj),
+                                               acc["ms_adj"], adj_B, adj_units, n_adj,
+                                               info.adj_steps)
+    alg_total = per_pt * w.npoints * units
+    avg_ms = ms_k / max(nl, 1)
+    alg_bytes = alg_total / max(nl, 1)
+    achieved = alg_total / (ms_k * 1e-3) / 1e9
+    traffic = traffic_for(name, kernel, w.kind)
     roofline = {
         "bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
         "traffic": traffic, "alg_bytes_per_launch": alg_bytes,
         "avg_launch_ms": round(avg_ms, 5), "launches_per_step": nl,
         "steps_per_launch": round(ns / max(nl, 1), 3),
-        "fwd_avg_ms": round(fwd_avg, 5), "fwd_gbps": round(fwd_B * w.npoints / fwd_avg / 1e6, 1),
-        "adj_avg_ms": round(adj_avg, 5), "adj_gbps": round(adj_B * w.npoints / adj_avg / 1e6, 1),
+        "fwd_avg_ms": round(fwd_avg, 5),
+        "fwd_gbps": round(fwd_B * w.npoints * fwd_units / max(ms_fwd, 1e-9) / 1e6, 1),
+        "adj_avg_ms": round(adj_avg, 5),
+        "adj_gbps": round(adj_B * w.npoints * adj_units / max(acc["ms_adj"], 1e-9) / 1e6, 1),
     }
 
     res = {
@@ -224,7 +238,8 @@ def main():
             "schedule": SCHED_NAMES[info.sched] + ("" if info.needs_state else " (tape elided)"),
             "slots": info.slots, "fwd_steps": info.fwd_steps_total,
             "recompute_steps": info.recompute_steps, "fwd_launches": info.fwd_launches,
-            "adj_launches": info.adj_launches, "grads": "dx0,dK" if w.want_dK else "dx0",
+            "adj_launches": info.adj_launches, "fwd_kernels": info.fwd_kernels,
+            "adj_kernels": info.adj_kernels, "grads": "dx0,dK" if w.want_dK else "dx0",
             "force_tape": bool(args.force_tape), "temporal_blocking": not args.no_fuse,
         },
         "hbm_gbps_effective": round(info.alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),

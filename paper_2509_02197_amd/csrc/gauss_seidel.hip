@@ -70,8 +70,10 @@ constexpr int kGsLanes = 64;  // one wave per tile
 constexpr int kGsRows = 32;   // rows each lane walks per tile
 constexpr int kGsLagJ = 3;    // tau = I + kGsLagJ * J + kGsLagS * s
 constexpr int kGsLagS = 3;
+constexpr int kGsChunk = 16;  // steps whose outputs are staged in LDS before a flush
 static_assert(kGsLagJ == 2 + (kGsLanes - 2) / kGsRows, "lane 0 waits on tiles up to I+2");
-static_assert(kGsLanes == 2 * kGsRows, "the halo load gives each lane one halo value");
+static_assert(kGsLanes == 2 * kGsRows, "each lane holds one halo value");
+static_assert(kGsRows % kGsChunk == 0, "the steps split into whole flush chunks");
 
 enum : int { kGsRecur = 0, kGsFused = 1, kGsFinish = 2 };
 
@@ -108,26 +110,46 @@ struct GsVec {
   R v[V];
 };
 
-// Load the V elements of real row `row`, real columns [c0, c0 + V), zero
-// where outside the grid. VEC: the block is whole and 16-byte aligned.
+// Value of lane `src` (a compile-time constant) in every lane.
+__device__ inline float lane_value(float v, int src) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src));
+}
+__device__ inline double lane_value(double v, int src) {
+  const uint64_t a = __double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)a, src);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(a >> 32), src);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Loads never branch: an address outside the grid is clamped into it and
+// the value replaced by 0. Without divergent branches around them, the
+// compiler waits for each load only where its value is first used, so a
+// tile starts computing as soon as its first rows arrive.
+template <class R>
+__device__ inline R gs_load1(const R* a, int row, int col, int nx, int ny, bool ok) {
+  const int r = min(max(row, 0), ny - 1);
+  const int c = min(max(col, 0), nx - 1);
+  const R v = a[(int64_t)r * nx + c];
+  return ok ? v : R(0);
+}
+
+// The V elements of real row `row`, real columns [c0, c0 + V), 0 outside
+// the grid or when !ok. VEC: nx is a multiple of V and rows are 16-byte
+// aligned, so an in-grid block is whole.
 template <class R, bool VEC>
-__device__ inline GsVec<R> gs_load(const R* a, int row, int c0, int nx, bool ok) {
+__device__ inline GsVec<R> gs_load(const R* a, int row, int c0, int nx, int ny, bool ok) {
   constexpr int V = GsVec<R>::V;
   GsVec<R> r;
   if (VEC) {
     typedef R vec_t __attribute__((ext_vector_type(V)));
-    if (ok) {
-      const vec_t t = *reinterpret_cast<const vec_t*>(a + (int64_t)row * nx + c0);
+    const int rr = min(max(row, 0), ny - 1);
+    const int cc = min(max(c0, 0), nx - V);
+    const vec_t t = *reinterpret_cast<const vec_t*>(a + (int64_t)rr * nx + cc);
 #pragma unroll
-      for (int e = 0; e < V; ++e) r.v[e] = t[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < V; ++e) r.v[e] = R(0);
-    }
+    for (int e = 0; e < V; ++e) r.v[e] = ok ? t[e] : R(0);
   } else {
 #pragma unroll
-    for (int e = 0; e < V; ++e)
-      r.v[e] = (ok && c0 + e < nx) ? a[(int64_t)row * nx + c0 + e] : R(0);
+    for (int e = 0; e < V; ++e) r.v[e] = gs_load1(a, row, c0 + e, nx, ny, ok && c0 + e < nx);
   }
   return r;
 }
@@ -162,15 +184,13 @@ __global__ __launch_bounds__(kGsLanes) void gs_wave(R* buf, const R* old_src, in
   const int I = tau - kGsLagS * s - kGsLagJ * J;
   if (I < 0 || I >= nti) return;  // whole wave: no tile at this (s, J)
 
-  __shared__ R halo_px[B];  // lane 0: new value before its block, per step
-  __shared__ R halo_nx[B];  // lane 63: old value after its block, per step
-
   const int j = (int)threadIdx.x;
   const int jj = kGsLanes * J + j;              // processing block
   const bool blk_ok = jj < nb;
   const int rb = ADJ ? nb - 1 - jj : jj;        // real block
   const int c0 = rb * V;                        // first real column of the block
   const int phase = !ADJ ? kGsFused : s == 0 ? kGsRecur : s == nphase - 1 ? kGsFinish : kGsFused;
+  const bool recur = phase == kGsRecur, finish = phase == kGsFinish;
   const R* old_a = (!ADJ && s == 0) ? old_src : buf;
   const int rho0 = B * I - j;                   // processing row of step 0
   auto real_row = [&](int rho) { return ADJ ? ny - 1 - rho : rho; };
@@ -181,42 +201,59 @@ __global__ __launch_bounds__(kGsLanes) void gs_wave(R* buf, const R* old_src, in
   auto col_before = [&](int q) { return ADJ ? (nb - q) * V : q * V - 1; };
   auto col_after = [&](int q) { return ADJ ? (nb - 2 - q) * V + V - 1 : (q + 1) * V; };
 
-  // ---- halos: lane 0's PX for steps 1..B-1 (new), lane 63's NX (old)
+  // ---- halos, one value per lane, broadcast by readlane at each step:
+  // lanes 0..B-1 hold lane 0's PX for step m = j (new values), lanes B..2B-1
+  // lane 63's NX for step m = j - B (old values).
+  R halo;
   {
+    const bool px_half = j < B;
     const int m = j % B;
-    if (j < B) {
-      const int rho = B * I + m, q = kGsLanes * J;
-      const int col = col_before(q);
-      R v = R(0);
-      if (q >= 1 && row_ok(rho) && col >= 0 && col < nx)
-        v = buf[(int64_t)real_row(rho) * nx + col];
-      halo_px[m] = v;
-    } else {
-      const int rho = B * I + m - (kGsLanes - 1), q = kGsLanes * J + kGsLanes - 1;
-      const int col = col_after(q);
-      R v = R(0);
-      if (q + 1 < nb && row_ok(rho) && col >= 0 && col < nx)
-        v = old_a[(int64_t)real_row(rho) * nx + col];
-      halo_nx[m] = v;
-    }
+    const int qa = kGsLanes * J, qb = kGsLanes * J + kGsLanes - 1;
+    const int rho = px_half ? B * I + m : B * I + m - (kGsLanes - 1);
+    const int col = px_half ? col_before(qa) : col_after(qb);
+    const bool okh = row_ok(rho) && (px_half ? qa >= 1 : qb + 1 < nb);
+    halo = gs_load1(px_half ? static_cast<const R*>(buf) : old_a, real_row(rho), col, nx, ny, okh);
   }
-
+  // PX of step 0: the new value before the block on this lane's first row.
+  const R px0 = gs_load1(buf, real_row(rho0), col_before(jj), nx, ny,
+                         blk_ok && jj >= 1 && row_ok(rho0));
   // ---- this lane's rows: L[0] is the previous row (new values), L[1..B]
   // the rows it updates and L[B+1] the row after (old values).
   GsVec<R> L[B + 2];
 #pragma unroll
   for (int k = 0; k < B + 2; ++k) {
     const int rho = rho0 - 1 + k;
-    L[k] = gs_load<R, VEC>(k == 0 ? buf : old_a, real_row(rho), c0, nx, blk_ok && row_ok(rho));
+    L[k] = gs_load<R, VEC>(k == 0 ? buf : old_a, real_row(rho), c0, nx, ny,
+                           blk_ok && row_ok(rho));
   }
-  // PX of step 0: the new value before the block on this lane's first row.
-  R px0 = R(0);
-  {
-    const int col = col_before(jj);
-    if (blk_ok && jj >= 1 && row_ok(rho0) && col >= 0 && col < nx)
-      px0 = buf[(int64_t)real_row(rho0) * nx + col];
-  }
-  __syncthreads();
+
+  // Outputs of the current chunk of steps, by (step within chunk, lane). A
+  // lane's rows are skewed against its neighbours', so storing each step
+  // directly would touch 64 rows with 16 bytes each; flushing the chunk by
+  // grid row instead stores up to kGsChunk neighbouring blocks (contiguous
+  // bytes) per instruction.
+  __shared__ GsVec<R> stage[kGsChunk][kGsLanes];
+  auto flush = [&](int m0) {
+    __syncthreads();
+    // The chunk covers grid rows rho = B*I + m0 - 63 + i, i < kGsChunk + 63;
+    // row i holds the outputs of lanes 63 - i + d at step m0 + d. Each
+    // store instruction takes four rows, sixteen lanes (d) per row.
+    constexpr int kRows = kGsChunk + kGsLanes - 1;
+    constexpr int kPer = kGsLanes / kGsChunk;
+#pragma unroll
+    for (int q = 0; q < (kRows + kPer - 1) / kPer; ++q) {
+      const int i = q * kPer + j / kGsChunk;
+      const int d = j % kGsChunk;
+      const int src = (kGsLanes - 1) - i + d;  // lane that produced it
+      const int srcc = min(max(src, 0), kGsLanes - 1);
+      const GsVec<R> v = stage[d][srcc];
+      const int rho = B * I + m0 - (kGsLanes - 1) + i;
+      const int jjs = kGsLanes * J + srcc;
+      if (i < kRows && src == srcc && jjs < nb && row_ok(rho))
+        gs_store<R, VEC>(buf, real_row(rho), (ADJ ? nb - 1 - jjs : jjs) * V, nx, v);
+    }
+    __syncthreads();
+  };
 
   GsVec<R> prev_new = L[0];
   R last_new = R(0);  // new value of this lane's last processing element, previous step
@@ -228,10 +265,10 @@ __global__ __launch_bounds__(kGsLanes) void gs_wave(R* buf, const R* old_src, in
     const bool row_in = row >= 1 && row <= ny - 2;
     // processing order element e sits at real offset ix(e) of the block
     auto ix = [&](int e) { return ADJ ? V - 1 - e : e; };
-    const R px_first = m == 0 ? px0 : lane_from_prev(last_new, halo_px[m]);
-    const R nx_last = lane_from_next(L[m + 2].v[ix(0)], halo_nx[m]);
-    const GsVec<R>& C = L[m + 1];
-    const GsVec<R>& NR = L[m + 2];
+    const R px_first = m == 0 ? px0 : lane_from_prev(last_new, lane_value(halo, m));
+    const R nx_last = lane_from_next(L[m + 2].v[ix(0)], lane_value(halo, B + m));
+    const GsVec<R> C = L[m + 1];
+    const GsVec<R> NR = L[m + 2];
     GsVec<R> out;
     R px = px_first;
 #pragma unroll
@@ -242,39 +279,44 @@ __global__ __launch_bounds__(kGsLanes) void gs_wave(R* buf, const R* old_src, in
       const R nr = NR.v[ix(e)];
       const R pr = prev_new.v[ix(e)];
       const bool col_in = col >= 1 && col <= nx - 2;
-      R y = c;
+      R y;
       if (!ADJ) {
-        if (row_in && col_in) y = w * ((((c + nxv) + nr) + pr) + px);
+        const R yi = w * ((((c + nxv) + nr) + pr) + px);
+        y = (row_in && col_in) ? yi : c;
       } else {
-        if (row_in && col_in) {
-          const R hW = col - 1 == 0 ? R(0) : nxv;   // real W: next element, old
-          const R hS = row - 1 == 0 ? R(0) : nr;    // real S: next row, old
-          const R hE = col + 1 == nx - 1 ? R(0) : px;  // real E: previous element, new
-          const R hN = row + 1 == ny - 1 ? R(0) : pr;  // real N: previous row, new
-          const R gin = phase == kGsRecur ? c : w * ((c + hW) + hS);
-          y = phase == kGsFinish ? gin : (gin + w * hN) + w * hE;
-        } else if (phase != kGsRecur && row_in && nx >= 3) {
-          // ring columns collect w * h of their interior neighbour
-          if (col == 0) y = c + w * C.v[ix(e - 1 < 0 ? 0 : e - 1)];
-          else if (col == nx - 1) y = c + w * nxv;
-        } else if (phase != kGsRecur && row == ny - 1 && col_in && ny >= 3) {
-          y = c + w * nr;  // top ring row: its neighbour row ny-2 is next, still old
-        }
+        const R hW = col - 1 == 0 ? R(0) : nxv;      // real W: next element, old
+        const R hS = row - 1 == 0 ? R(0) : nr;       // real S: next row, old
+        const R hE = col + 1 == nx - 1 ? R(0) : px;  // real E: previous element, new
+        const R hN = row + 1 == ny - 1 ? R(0) : pr;  // real N: previous row, new
+        const R gin = recur ? c : w * ((c + hW) + hS);
+        const R yi = finish ? gin : (gin + w * hN) + w * hE;
+        // Ring columns collect w * h of their interior neighbour: (row, 1) is
+        // the previous element, (row, nx-2) the next; the top ring row's
+        // neighbour row ny-2 is the next row, still old.
+        const R prev_old = e > 0 ? C.v[ix(e > 0 ? e - 1 : 0)] : c;
+        const R yc = c + w * (col == 0 ? prev_old : nxv);
+        const R yt = c + w * nr;
+        const bool ring_col = !recur && row_in && nx >= 3 && (col == 0 || col == nx - 1);
+        const bool ring_top = !recur && row == ny - 1 && col_in && ny >= 3;
+        y = (row_in && col_in) ? yi : ring_col ? yc : ring_top ? yt : c;
       }
       out.v[ix(e)] = y;
       px = y;
     }
-    if (ADJ && phase != kGsRecur && row == 1 && ny >= 3) {
+    if (ADJ) {
       // The bottom ring row is reversed after row 1, whose old h it needs:
       // push w * h(1, col) into the register copy of row 0 (the next row).
+      const bool push = !recur && row == 1 && ny >= 3;
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         const int col = c0 + e;
-        if (col >= 1 && col <= nx - 2) L[m + 2].v[e] = L[m + 2].v[e] + w * C.v[e];
+        const R pushed = L[m + 2].v[e] + w * C.v[e];
+        L[m + 2].v[e] = (push && col >= 1 && col <= nx - 2) ? pushed : L[m + 2].v[e];
       }
-      if (m == B - 1 && ok) gs_store<R, VEC>(buf, 0, c0, nx, L[m + 2]);
+      if (m == B - 1 && push && ok) gs_store<R, VEC>(buf, 0, c0, nx, L[m + 2]);
     }
-    if (ok) gs_store<R, VEC>(buf, row, c0, nx, out);
+    stage[m % kGsChunk][j] = out;
+    if (m % kGsChunk == kGsChunk - 1) flush(m - (kGsChunk - 1));
     prev_new = out;
     last_new = px;
   }
