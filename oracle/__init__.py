@@ -37,10 +37,10 @@ def _load():
         f.argtypes = [ci, i64p, dp, vp, vp, ci, vp]
         f.restype = ci
         f = getattr(lib, "oracle_vjp_" + suf)
-        f.argtypes = [ci, i64p, dp, vp, vp, ci, ci, vp, vp, vp, vp, dp]
+        f.argtypes = [ci, i64p, dp, vp, vp, ci, ci, vp, vp, vp, vp, dp, dp]
         f.restype = ci
         f = getattr(lib, "oracle_jvp_" + suf)
-        f.argtypes = [ci, i64p, dp, vp, vp, vp, vp, ci, vp, vp]
+        f.argtypes = [ci, i64p, dp, vp, vp, vp, vp, dp, ci, vp, vp]
         f.restype = ci
     _lib = lib
     return lib
@@ -102,30 +102,38 @@ def forward(kind, x0, K=None, steps=1, params=None):
     return xT
 
 
-def vjp(kind, x0, K=None, steps=1, loss=HALF_SQ, aux=None, want_dK=False, params=None):
-    """Store-all reverse-mode gradient. Returns (dx0, dK or None, x_T, L)."""
+def vjp(kind, x0, K=None, steps=1, loss=HALF_SQ, aux=None, want_dK=False, params=None,
+        want_dp=False):
+    """Store-all reverse-mode gradient. Returns (dx0, dK or None, x_T, L), and
+    with want_dp also the gradients of the two step constants (dL/dp[0],
+    dL/dp[1]) as a fifth element."""
     x0, K, aux = _prep(x0, K, aux)
     n, p = _args(kind, x0, params)
     dx0 = np.empty_like(x0)
     dK = np.empty_like(x0) if want_dK else None
     xT = np.empty_like(x0)
     L = ctypes.c_double(0.0)
+    dpv = (ctypes.c_double * 2)(0.0, 0.0)
     rc = getattr(_load(), "oracle_vjp_" + _suffix(x0.dtype))(
         kind, n, p, _ptr(x0), _ptr(K), steps, loss, _ptr(aux), _ptr(dx0), _ptr(dK),
-        _ptr(xT), ctypes.byref(L))
+        _ptr(xT), ctypes.byref(L), dpv if want_dp else None)
     if rc:
         raise ValueError("oracle_vjp rejected the problem")
+    if want_dp:
+        return dx0, dK, xT, L.value, (dpv[0], dpv[1])
     return dx0, dK, xT, L.value
 
 
-def jvp(kind, x0, v, K=None, kappa=None, steps=1, params=None):
-    """Tangent-linear sweep. Returns (x_T, xdot_T) for direction (v, kappa)."""
+def jvp(kind, x0, v, K=None, kappa=None, steps=1, params=None, pdot=None):
+    """Tangent-linear sweep. Returns (x_T, xdot_T) for direction (v, kappa,
+    pdot), pdot the direction of the two step constants."""
     x0, v, K, kappa = _prep(x0, v, K, kappa)
     n, p = _args(kind, x0, params)
     xT = np.empty_like(x0)
     xdT = np.empty_like(x0)
+    pd = None if pdot is None else (ctypes.c_double * 2)(*pdot)
     rc = getattr(_load(), "oracle_jvp_" + _suffix(x0.dtype))(
-        kind, n, p, _ptr(x0), _ptr(K), _ptr(v), _ptr(kappa), steps, _ptr(xT), _ptr(xdT))
+        kind, n, p, _ptr(x0), _ptr(K), _ptr(v), _ptr(kappa), pd, steps, _ptr(xT), _ptr(xdT))
     if rc:
         raise ValueError("oracle_jvp rejected the problem")
     return xT, xdT

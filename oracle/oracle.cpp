@@ -20,8 +20,15 @@
 //      The coefficient-field gradient dK accumulates the same way over all
 //      steps (a multiply-read array, Sec. II).
 //   4. dx0 = g_0.
+// Optionally the gradients of the two scalar step constants p[0], p[1]
+// (Sec. II: a value every point of every step reads is a multiply-read
+// input whose gradient accumulates over all its uses): for each step t and
+// point c, g_t[c] times the step's partial dF_c/dp at x_{t-1}, summed in
+// double; for the in-place kind each point update's own partial times the
+// gradient its output holds when the update is reversed.
 // A tangent-linear (forward-mode) sweep is included so that tests can check
-// the adjoint dot-product identity <J v, w> = <v, J^T w>.
+// the adjoint dot-product identity <J v, w> = <v, J^T w>, also along the
+// constants.
 //
 // The four step kinds (the stencil programs the gradient is taken of):
 //   JACOBI2D5  x'[c] = w * (x[c] + x[W] + x[E] + x[S] + x[N]) on interior
@@ -165,13 +172,18 @@ void step_forward(int kind, const Grid& g, const double* p, const R* x,
 // the update read: g[k] <- w*g[k] (its old value) and w*g[k] added to each
 // neighbour (whatever sweep's value it was). The gradient of the overwritten
 // value is cleared by the assignment, as for any overwrite.
+// With s (the sum each update formed, recorded in forward order) and dw
+// given, dw accumulates gc * s[c], the update's partial in w times the
+// gradient of its output.
 template <class R>
-void gauss_seidel_reverse(const Grid& g, const double* p, R* gr) {
+void gauss_seidel_reverse(const Grid& g, const double* p, R* gr, const R* s = nullptr,
+                          double* dw = nullptr) {
   const R w = R(p[0]);
   for (int64_t y = g.ny - 2; y >= 1; --y)
     for (int64_t i = g.nx - 2; i >= 1; --i) {
       const int64_t c = g.at(i, y, 0);
       const R gc = gr[c];
+      if (dw) *dw += double(gc) * double(s[c]);
       gr[c] = w * gc;
       gr[g.at(i - 1, y, 0)] += w * gc;
       gr[g.at(i + 1, y, 0)] += w * gc;
@@ -236,6 +248,79 @@ void step_adjoint_scatter(int kind, const Grid& g, const double* p, const R* x,
           }
         }
       }
+}
+
+// ------------------------------------------------ scalar-constant partials
+// d0[c] = dF_c/dp[0], d1[c] = dF_c/dp[1] of one step at its input x, the
+// sub-expressions the forward step forms, in its order:
+//   JACOBI2D5     dF/dw  = (((x[c]+x[W])+x[E])+x[S])+x[N] on interior points, 0 on the ring
+//   ALLENCAHN3D7  dF/dD  = lap,  dF/dC = -((x[c]*x[c])*x[c])
+//   VARDIFF2D9    dF/ddt = acc
+// (The in-place kind's partials depend on the order of the sweep; see
+// gauss_seidel_sums.)
+template <class R>
+void step_param_partials(int kind, const Grid& g, const R* x, const R* K, R* d0, R* d1) {
+  for (int64_t z = 0; z < g.nz; ++z)
+    for (int64_t y = 0; y < g.ny; ++y)
+      for (int64_t i = 0; i < g.nx; ++i) {
+        const int64_t c = g.at(i, y, z);
+        d0[c] = R(0);
+        d1[c] = R(0);
+        if (kind == JACOBI2D5) {
+          if (i > 0 && i < g.nx - 1 && y > 0 && y < g.ny - 1) {
+            R s = x[c];
+            s += x[g.at(i - 1, y, z)];
+            s += x[g.at(i + 1, y, z)];
+            s += x[g.at(i, y - 1, z)];
+            s += x[g.at(i, y + 1, z)];
+            d0[c] = s;
+          }
+        } else if (kind == ALLENCAHN3D7) {
+          R nb[6];
+          for (int n = 0; n < 6; ++n) {
+            int64_t a = i + kSeven[n][0], b = y + kSeven[n][1], d = z + kSeven[n][2];
+            nb[n] = g.inside(a, b, d) ? x[g.at(a, b, d)] : R(0);
+          }
+          const R a = x[c];
+          R lap = nb[0] + nb[1];
+          lap += nb[2];
+          lap += nb[3];
+          lap += nb[4];
+          lap += nb[5];
+          d0[c] = lap - R(6) * a;
+          d1[c] = -((a * a) * a);
+        } else if (kind == VARDIFF2D9) {
+          R acc = R(0);
+          for (int n = 0; n < 8; ++n) {
+            int64_t a = i + kNine[n][0], b = y + kNine[n][1];
+            if (!g.inside(a, b, z)) continue;
+            const int64_t m = g.at(a, b, z);
+            acc += (nine_weight<R>(n) * (K[c] + K[m])) * (x[m] - x[c]);
+          }
+          d0[c] = acc;
+        }
+      }
+}
+
+// The in-place sweep from x, recording at each interior point the sum the
+// update multiplies by w (its partial in w, formed from the values the
+// point reads at that moment).
+template <class R>
+void gauss_seidel_sums(const Grid& g, const double* p, const R* x, R* s_out) {
+  const R w = R(p[0]);
+  std::vector<R> a(x, x + g.size());
+  std::fill(s_out, s_out + g.size(), R(0));
+  for (int64_t y = 1; y < g.ny - 1; ++y)
+    for (int64_t i = 1; i < g.nx - 1; ++i) {
+      const int64_t c = g.at(i, y, 0);
+      R s = a[c];
+      s += a[g.at(i + 1, y, 0)];
+      s += a[g.at(i, y + 1, 0)];
+      s += a[g.at(i, y - 1, 0)];
+      s += a[g.at(i - 1, y, 0)];
+      s_out[c] = s;
+      a[c] = w * s;
+    }
 }
 
 // ---------------------------------------------------- forward mode (JVP)
@@ -313,7 +398,8 @@ int forward(int kind, const int64_t* n, const double* p, const R* x0, const R* K
 
 template <class R>
 int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
-        int steps, int loss, const R* aux, R* dx0, R* dK, R* xT, double* loss_out) {
+        int steps, int loss, const R* aux, R* dx0, R* dK, R* xT, double* loss_out,
+        double* dp_out) {
   Grid g{n[0], n[1], n[2]};
   if (check_problem(kind, g, K) || steps < 0) return -1;
   if (loss < HALF_SQ || loss > SEED) return -1;
@@ -348,11 +434,36 @@ int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
   std::vector<R> gprev(N);
   std::vector<R> dk_acc;
   if (dK) dk_acc.assign(N, R(0));
+  std::vector<R> d0, d1;
+  double dp[2] = {0.0, 0.0};
+  if (dp_out) {
+    d0.resize(N);
+    d1.resize(N);
+  }
   for (int t = steps; t >= 1; --t) {
+    if (dp_out && kind == GAUSSSEIDEL2D5) {
+      // the sweep's own reverse carries the partials (see gauss_seidel_reverse)
+      gauss_seidel_sums<R>(g, p, tape[t - 1].data(), d0.data());
+      gprev = gcur;
+      gauss_seidel_reverse<R>(g, p, gprev.data(), d0.data(), &dp[0]);
+      gcur.swap(gprev);
+      continue;
+    }
+    if (dp_out) {
+      step_param_partials<R>(kind, g, tape[t - 1].data(), K, d0.data(), d1.data());
+      for (int64_t i = 0; i < N; ++i) {
+        dp[0] += double(gcur[i]) * double(d0[i]);
+        dp[1] += double(gcur[i]) * double(d1[i]);
+      }
+    }
     std::fill(gprev.begin(), gprev.end(), R(0));  // clearing on overwrite
     step_adjoint_scatter<R>(kind, g, p, tape[t - 1].data(), K, gcur.data(),
                             gprev.data(), dK ? dk_acc.data() : nullptr);
     gcur.swap(gprev);
+  }
+  if (dp_out) {
+    dp_out[0] = dp[0];
+    dp_out[1] = dp[1];
   }
 
   // 4. outputs
@@ -365,13 +476,40 @@ int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
 
 template <class R>
 int jvp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
-        const R* v, const R* kappa, int steps, R* xT, R* xdT) {
+        const R* v, const R* kappa, const double* pdot, int steps, R* xT, R* xdT) {
   Grid g{n[0], n[1], n[2]};
   if (check_problem(kind, g, K) || steps < 0 || !v) return -1;
   const int64_t N = g.size();
-  std::vector<R> x(x0, x0 + N), xn(N), xd(v, v + N), xdn(N);
+  std::vector<R> x(x0, x0 + N), xn(N), xd(v, v + N), xdn(N), d0(N), d1(N);
   for (int t = 1; t <= steps; ++t) {
+    if (kind == GAUSSSEIDEL2D5 && pdot) {
+      // tangent of the in-place sweep along (v, pdot): each update
+      // x[c] = w*s becomes xd[c] = w*sd + pdot*s, in the sweep's order
+      const R w = R(p[0]), wd = R(pdot[0]);
+      std::vector<R> a = x, ad = xd;
+      for (int64_t y = 1; y < g.ny - 1; ++y)
+        for (int64_t i = 1; i < g.nx - 1; ++i) {
+          const int64_t c = g.at(i, y, 0);
+          const int64_t nb[4] = {g.at(i + 1, y, 0), g.at(i, y + 1, 0), g.at(i, y - 1, 0),
+                                 g.at(i - 1, y, 0)};
+          R sv = a[c], sd = ad[c];
+          for (int k = 0; k < 4; ++k) {
+            sv += a[nb[k]];
+            sd += ad[nb[k]];
+          }
+          a[c] = w * sv;
+          ad[c] = w * sd + wd * sv;
+        }
+      x.swap(a);
+      xd.swap(ad);
+      continue;
+    }
     step_tangent<R>(kind, g, p, x.data(), K, xd.data(), kappa, xdn.data());
+    if (pdot) {
+      step_param_partials<R>(kind, g, x.data(), K, d0.data(), d1.data());
+      for (int64_t i = 0; i < N; ++i)
+        xdn[i] = (xdn[i] + R(pdot[0]) * d0[i]) + R(pdot[1]) * d1[i];
+    }
     step_forward<R>(kind, g, p, x.data(), K, xn.data());
     x.swap(xn);
     xd.swap(xdn);
@@ -395,23 +533,23 @@ int oracle_forward_f32(int kind, const int64_t* n, const double* p, const float*
 }
 int oracle_vjp_f64(int kind, const int64_t* n, const double* p, const double* x0,
                    const double* K, int steps, int loss, const double* aux, double* dx0,
-                   double* dK, double* xT, double* loss_out) {
-  return vjp<double>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out);
+                   double* dK, double* xT, double* loss_out, double* dp_out) {
+  return vjp<double>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
 }
 int oracle_vjp_f32(int kind, const int64_t* n, const double* p, const float* x0,
                    const float* K, int steps, int loss, const float* aux, float* dx0,
-                   float* dK, float* xT, double* loss_out) {
-  return vjp<float>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out);
+                   float* dK, float* xT, double* loss_out, double* dp_out) {
+  return vjp<float>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
 }
 int oracle_jvp_f64(int kind, const int64_t* n, const double* p, const double* x0,
-                   const double* K, const double* v, const double* kappa, int steps,
-                   double* xT, double* xdT) {
-  return jvp<double>(kind, n, p, x0, K, v, kappa, steps, xT, xdT);
+                   const double* K, const double* v, const double* kappa, const double* pdot,
+                   int steps, double* xT, double* xdT) {
+  return jvp<double>(kind, n, p, x0, K, v, kappa, pdot, steps, xT, xdT);
 }
 int oracle_jvp_f32(int kind, const int64_t* n, const double* p, const float* x0,
-                   const float* K, const float* v, const float* kappa, int steps,
-                   float* xT, float* xdT) {
-  return jvp<float>(kind, n, p, x0, K, v, kappa, steps, xT, xdT);
+                   const float* K, const float* v, const float* kappa, const double* pdot,
+                   int steps, float* xT, float* xdT) {
+  return jvp<float>(kind, n, p, x0, K, v, kappa, pdot, steps, xT, xdT);
 }
 
 }  // extern "C"
