@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--force-tape", action="store_true")
     ap.add_argument("--no-fuse", action="store_true",
                     help="one launch per step (no temporal blocking)")
+    ap.add_argument("--dparams", action="store_true",
+                    help="also compute the gradients of the scalar step constants")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
@@ -138,16 +140,19 @@ def main():
     K = torch.from_numpy(inp["K"]).to(dev) if inp["K"] is not None else None
     aux = torch.from_numpy(inp["aux"]).to(dev) if inp["aux"] is not None else None
     prob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params, flags)
-    info = adst.adst_plan(prob, w.steps, budget, sched, w.want_dK)
+    grads = (adst.ADST_GRAD_COEFF if w.want_dK else 0) | \
+        (adst.ADST_GRAD_PARAMS if args.dparams else 0)
+    info = adst.adst_plan(prob, w.steps, budget, sched, grads)
     ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=dev)
     dx0 = torch.empty_like(x0)
     dK = torch.empty_like(x0) if w.want_dK else None
     L = torch.empty((), dtype=torch.float64, device=dev)
+    dP = torch.empty(2, dtype=torch.float64, device=dev) if args.dparams else None
     stream = torch.cuda.current_stream()
 
     def call(p):
-        return adst.adst_vjp(p, x0, K, w.steps, w.loss, aux, budget, sched, dx0, dK, None, L, ws,
-                             ws.numel(), stream)
+        return adst.adst_vjp(p, x0, K, w.steps, w.loss, aux, budget, sched, dx0, dK, None, L, dP,
+                             ws, ws.numel(), stream)
 
     for _ in range(args.warmup):
         call(prob)
@@ -172,7 +177,7 @@ def main():
     tprob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params,
                               flags | adst.ADST_TRACE)
     acc = {"ms_fwd_sweep": 0.0, "ms_fwd_recompute": 0.0, "ms_adj": 0.0, "ms_seed": 0.0,
-           "ms_total": 0.0}
+           "ms_dparams": 0.0, "ms_total": 0.0}
     for _ in range(args.steps):
         ti = call(tprob)
         for k in acc:
@@ -226,6 +231,11 @@ def main():
         "adj_avg_ms": round(adj_avg, 5),
         "adj_gbps": round(adj_B * w.npoints * adj_units / max(acc["ms_adj"], 1e-9) / 1e6, 1),
     }
+    if args.dparams:  # the constants' gradient kernel: reads x_{t-1}, g_t (and K) per step
+        dp_B = (3 if w.kind == adst.ADST_VARDIFF2D9 else 2) * isz
+        roofline["dparam_ms"] = round(acc["ms_dparams"], 4)
+        roofline["dparam_gbps"] = round(dp_B * w.npoints * info.adj_steps /
+                                        max(acc["ms_dparams"], 1e-9) / 1e6, 1)
 
     res = {
         "metric": METRIC, "value": value, "unit": "grid-point-steps/s", "n_gpus": 1,
@@ -239,7 +249,8 @@ def main():
             "slots": info.slots, "fwd_steps": info.fwd_steps_total,
             "recompute_steps": info.recompute_steps, "fwd_launches": info.fwd_launches,
             "adj_launches": info.adj_launches, "fwd_kernels": info.fwd_kernels,
-            "adj_kernels": info.adj_kernels, "grads": "dx0,dK" if w.want_dK else "dx0",
+            "adj_kernels": info.adj_kernels,
+            "grads": ("dx0,dK" if w.want_dK else "dx0") + (",dparams" if args.dparams else ""),
             "force_tape": bool(args.force_tape), "temporal_blocking": not args.no_fuse,
         },
         "hbm_gbps_effective": round(info.alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),

@@ -117,6 +117,20 @@ typedef enum {
 #define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking);
                                 results are bit-identical either way */
 
+/* Which gradients besides dx0 a plan is for (the `grads` argument).
+ *   ADST_GRAD_COEFF   dK, the per-point coefficient field (VARDIFF2D9 only)
+ *   ADST_GRAD_PARAMS  dL/dp[0] and dL/dp[1], the scalar step constants:
+ *                     Jacobi (dL/dw, 0), Allen-Cahn (dL/dD, dL/dC), variable
+ *                     coefficients (dL/ddt, 0), each the derivative with
+ *                     respect to the constant as rounded to the working
+ *                     precision. A constant every point of every step reads
+ *                     accumulates its gradient over all those uses (Sec. II);
+ *                     its partials read x_{t-1}, so asking for it makes every
+ *                     kind's adjoint read state. Not built for the in-place
+ *                     kind (ADST_ERR_UNSUPPORTED). */
+#define ADST_GRAD_COEFF 0x1
+#define ADST_GRAD_PARAMS 0x2
+
 typedef struct {
   int32_t kind;   /* adst_kind */
   int32_t dtype;  /* adst_dtype */
@@ -195,14 +209,16 @@ typedef struct {
   float ms_adj;             /*   ... of the adjoint steps */
   float ms_seed;            /*   ... of the loss/seed and its final reduction */
   float ms_total;           /*   first launch start to last launch end */
-  float reserved;
+  float ms_dparams;         /*   ... of the constants' gradient kernels */
 } adst_plan_info;
 
 /* Plan a forward+VJP call without touching the GPU (host only).
  * The budget counts checkpoint-slot storage only: slots = floor(budget /
  * state_bytes); x0 is the caller's and is the free base checkpoint, so the
- * schedule has c = slots + 1 checkpoints. want_dcoeff != 0 asks for dK
- * (VARDIFF2D9 only), which makes its adjoint read x_{t-1}. For the in-place
+ * schedule has c = slots + 1 checkpoints. grads is a mask of ADST_GRAD_COEFF
+ * (dK, VARDIFF2D9 only, which makes its adjoint read x_{t-1}) and
+ * ADST_GRAD_PARAMS (the constants' gradients; every adjoint then reads
+ * x_{t-1}). For the in-place
  * kind (GAUSSSEIDEL2D5, linear) nothing is stored: the plan is one pipelined
  * forward run, the seed and one pipelined reverse run (FWDW, SEED, ADJW);
  * with ADST_FORCE_TAPE it is a per-step checkpointed plan like the others.
@@ -210,13 +226,13 @@ typedef struct {
  * shape), ADST_ERR_UNSUPPORTED (shape not valid for the kind, or dK asked for
  * a kind without a coefficient field), ADST_ERR_BUDGET (STORE_ALL does not fit). */
 adst_status adst_plan(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
-                      int32_t sched, int32_t want_dcoeff, adst_plan_info* out);
+                      int32_t sched, int32_t grads, adst_plan_info* out);
 
 /* The same plan as its action list (host only; for tests and inspection).
  * Writes min(cap, n) actions to out (out may be NULL when cap == 0) and the
  * full length to *n_out. Same errors as adst_plan. */
 adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
-                              int32_t sched, int32_t want_dcoeff, adst_action* out, int64_t cap,
+                              int32_t sched, int32_t grads, adst_action* out, int64_t cap,
                               int64_t* n_out);
 
 /* x_T after `steps` forward steps (the unmodified program). coeff is K for
@@ -230,7 +246,11 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
 
 /* Forward sweep, loss, and reverse sweep under the budget, enqueued on
  * `stream`. Outputs: dx0 (required), dcoeff (dK, VARDIFF2D9 only, NULL = not
- * requested), xT (optional), loss_dev (optional device double). ws must hold
+ * requested), xT (optional), loss_dev (optional device double), dparams
+ * (optional device double[2]: the constants' gradients, see
+ * ADST_GRAD_PARAMS; NULL = not requested). The plan is the one adst_plan
+ * gives for grads = (dcoeff ? ADST_GRAD_COEFF : 0) | (dparams ?
+ * ADST_GRAD_PARAMS : 0). ws must hold
  * adst_plan_info.workspace_bytes and is clobbered. dx0 doubles as one of the
  * two adjoint buffers (for the in-place kind, the only one: the reverse
  * sweeps run in place in dx0). steps = 0 is valid: dx0 = seed, dK = 0.
@@ -240,8 +260,8 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
  * or a missing loss_aux, ADST_ERR_WORKSPACE, ADST_ERR_HIP. */
 adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
                      int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
-                     void* dx0, void* dcoeff, void* xT, double* loss_dev, void* ws,
-                     uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info);
+                     void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
+                     void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info);
 
 /* ---- Store/recompute selection for a general program (Sec. IV) --------
  * The integer program of Sec. IV-A: one binary per forwarded array (store or

@@ -22,6 +22,7 @@ ADST_F64, ADST_F32 = 0, 1
 ADST_SCHED_AUTO, ADST_SCHED_STORE_ALL, ADST_SCHED_UNIFORM, ADST_SCHED_BINOMIAL = 0, 1, 2, 3
 ADST_LOSS_HALF_SQ, ADST_LOSS_DOT_W, ADST_LOSS_HALF_SQ_DIFF, ADST_LOSS_SEED = 0, 1, 2, 3
 ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE = 0x1, 0x2, 0x4
+ADST_GRAD_COEFF, ADST_GRAD_PARAMS = 0x1, 0x2
 ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2, ADST_OP_FWDW, ADST_OP_ADJW = range(7)
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
@@ -53,10 +54,10 @@ class adst_plan_info(ctypes.Structure):
                 ("alg_bytes", ctypes.c_uint64), ("ms_fwd_sweep", ctypes.c_float),
                 ("ms_fwd_recompute", ctypes.c_float), ("ms_adj", ctypes.c_float),
                 ("ms_seed", ctypes.c_float), ("ms_total", ctypes.c_float),
-                ("reserved", ctypes.c_float)]
+                ("ms_dparams", ctypes.c_float)]
 
     def as_dict(self):
-        return {f[0]: getattr(self, f[0]) for f in self._fields_ if f[0] != "reserved"}
+        return {f[0]: getattr(self, f[0]) for f in self._fields_}
 
 
 class adst_ilp_array(ctypes.Structure):
@@ -98,8 +99,8 @@ def lib():
     L.adst_plan_actions.argtypes = [P(adst_problem), i32, u64, i32, i32, P(adst_action), i64,
                                     P(i64)]
     L.adst_forward.argtypes = [P(adst_problem), vp, vp, i32, vp, vp, u64, vp]
-    L.adst_vjp.argtypes = [P(adst_problem), vp, vp, i32, i32, vp, u64, i32, vp, vp, vp, vp, vp, u64,
-                           vp, P(adst_plan_info)]
+    L.adst_vjp.argtypes = [P(adst_problem), vp, vp, i32, i32, vp, u64, i32, vp, vp, vp, vp, vp, vp,
+                           u64, vp, P(adst_plan_info)]
     L.adst_ilp_solve.argtypes = [P(adst_ilp_array), i32, P(adst_ilp_event), i64, ctypes.c_double,
                                  P(i32), P(adst_ilp_info)]
     for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve"):
@@ -155,22 +156,22 @@ def _stream(stream):
     return int(stream)
 
 
-def adst_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
+def adst_plan(prob, steps, mem_budget_bytes, sched, grads=0):
     info = adst_plan_info()
-    _check(lib().adst_plan(ctypes.byref(prob), steps, mem_budget_bytes, sched, int(want_dcoeff),
+    _check(lib().adst_plan(ctypes.byref(prob), steps, mem_budget_bytes, sched, int(grads),
                            ctypes.byref(info)))
     return info
 
 
-def adst_plan_actions(prob, steps, mem_budget_bytes, sched, want_dcoeff=False):
+def adst_plan_actions(prob, steps, mem_budget_bytes, sched, grads=0):
     """The plan's action list as a list of (op, t, src, dst, n) tuples."""
     n = ctypes.c_int64(0)
     L = lib()
     _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
-                               int(want_dcoeff), None, 0, ctypes.byref(n)))
+                               int(grads), None, 0, ctypes.byref(n)))
     buf = (adst_action * max(n.value, 1))()
     _check(L.adst_plan_actions(ctypes.byref(prob), steps, mem_budget_bytes, sched,
-                               int(want_dcoeff), buf, n.value, ctypes.byref(n)))
+                               int(grads), buf, n.value, ctypes.byref(n)))
     return [(a.op, a.t, a.src, a.dst, a.n) for a in buf[:n.value]]
 
 
@@ -180,11 +181,11 @@ def adst_forward(prob, x0, coeff, steps, xT, ws, ws_bytes, stream=None):
 
 
 def adst_vjp(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0, dcoeff, xT,
-             loss_dev, ws, ws_bytes, stream=None, want_info=True):
+             loss_dev, dparams, ws, ws_bytes, stream=None, want_info=True):
     info = adst_plan_info() if want_info else None
     _check(lib().adst_vjp(ctypes.byref(prob), _ptr(x0), _ptr(coeff), steps, loss, _ptr(loss_aux),
                           mem_budget_bytes, sched, _ptr(dx0), _ptr(dcoeff), _ptr(xT),
-                          _ptr(loss_dev), _ptr(ws), ws_bytes, _stream(stream),
+                          _ptr(loss_dev), _ptr(dparams), _ptr(ws), ws_bytes, _stream(stream),
                           ctypes.byref(info) if info is not None else None))
     return info
 
@@ -241,23 +242,26 @@ def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
 
 def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_bytes=None,
         sched=ADST_SCHED_AUTO, want_dcoeff=False, params=None, flags=0, stream=None, ws=None,
-        want_xT=True):
+        want_xT=True, want_dparams=False):
     """Allocate outputs and workspace with torch and run adst_vjp.
 
     budget_bytes=None means unlimited (store-all). Returns a dict with dx0,
-    dK (or None), xT (None unless want_xT), loss (0-d device tensor), info
-    and the workspace."""
+    dK (or None), xT (None unless want_xT), loss (0-d device tensor),
+    dparams (device double[2], or None unless want_dparams), info and the
+    workspace."""
     import torch
     prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags)
     if budget_bytes is None:
         budget_bytes = (1 << 63)
-    info = adst_plan(prob, steps, budget_bytes, sched, want_dcoeff)
+    grads = (ADST_GRAD_COEFF if want_dcoeff else 0) | (ADST_GRAD_PARAMS if want_dparams else 0)
+    info = adst_plan(prob, steps, budget_bytes, sched, grads)
     if ws is None or ws.numel() < info.workspace_bytes:
         ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=x0.device)
     dx0 = torch.empty_like(x0)
     dK = torch.empty_like(x0) if want_dcoeff else None
     xT = torch.empty_like(x0) if want_xT else None
     L = torch.empty((), dtype=torch.float64, device=x0.device)
-    info = adst_vjp(prob, x0, coeff, steps, loss, aux, budget_bytes, sched, dx0, dK, xT, L, ws,
-                    ws.numel(), stream)
-    return {"dx0": dx0, "dK": dK, "xT": xT, "loss": L, "info": info, "ws": ws}
+    dp = torch.empty(2, dtype=torch.float64, device=x0.device) if want_dparams else None
+    info = adst_vjp(prob, x0, coeff, steps, loss, aux, budget_bytes, sched, dx0, dK, xT, L, dp,
+                    ws, ws.numel(), stream)
+    return {"dx0": dx0, "dK": dK, "xT": xT, "loss": L, "dparams": dp, "info": info, "ws": ws}

@@ -47,9 +47,10 @@ struct Checked {
   bool trace = false;
   bool fuse_fwd = false, fuse_adj = false;
   bool in_place = false;  // the Gauss-Seidel kind: pipelined sweeps, adjoint in place
+  bool want_dk = false, want_dp = false;
 };
 
-adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* out) {
+adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   if (!p) return fail(ADST_ERR_ARG, "problem is NULL");
   if (p->kind < ADST_JACOBI2D5 || p->kind > ADST_GAUSSSEIDEL2D5)
     return fail(ADST_ERR_ARG, "unknown kind " + std::to_string(p->kind));
@@ -74,15 +75,24 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
           : ((p->n[0] + 251) / 252) * ((p->n[1] + 3) / 4);
   if ((tiles + 8) * 256 >= (int64_t(1) << 32))
     return fail(ADST_ERR_UNSUPPORTED, "grid too thin in x/y for the tile shape");
-  if (want_dcoeff && p->kind != ADST_VARDIFF2D9)
+  if (grads & ~(ADST_GRAD_COEFF | ADST_GRAD_PARAMS))
+    return fail(ADST_ERR_ARG, "unknown gradient bits");
+  const bool want_dk = (grads & ADST_GRAD_COEFF) != 0;
+  const bool want_dp = (grads & ADST_GRAD_PARAMS) != 0;
+  if (want_dk && p->kind != ADST_VARDIFF2D9)
     return fail(ADST_ERR_UNSUPPORTED, "only the variable-coefficient kind has a coefficient field");
+  if (want_dp && p->kind == ADST_GAUSSSEIDEL2D5)
+    return fail(ADST_ERR_UNSUPPORTED,
+                "the constants' gradients are not built for the in-place kind");
   out->shape = {p->kind, p->dtype, (int32_t)p->n[0], (int32_t)p->n[1], (int32_t)p->n[2],
                 p->p[0], p->p[1]};
   out->npoints = n;
   out->state_bytes = uint64_t(n) * itemsize(p->dtype);
   const bool kind_reads_state = p->kind == ADST_ALLENCAHN3D7 ||
-                                (p->kind == ADST_VARDIFF2D9 && want_dcoeff);
+                                (p->kind == ADST_VARDIFF2D9 && want_dk) || want_dp;
   out->needs_state = kind_reads_state || (p->flags & ADST_FORCE_TAPE);
+  out->want_dk = want_dk;
+  out->want_dp = want_dp;
   out->trace = (p->flags & ADST_TRACE) != 0;
   const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
   out->fuse_fwd = fuse && has_forward2(p->kind);
@@ -93,7 +103,7 @@ adst_status check_problem(const adst_problem* p, int32_t want_dcoeff, Checked* o
 
 struct Layout {
   uint64_t state_stride = 0;  // aligned bytes per state buffer
-  uint64_t w0 = 0, w1 = 0, g = 0, slot0 = 0, total = 0;
+  uint64_t w0 = 0, w1 = 0, g = 0, slot0 = 0, dp = 0, total = 0;
 };
 
 // Header, two work states, the second adjoint buffer G, then the slots. The
@@ -112,13 +122,17 @@ Layout layout_for(const Checked& c, const Plan& plan) {
   L.g = L.w1 + (nwork ? L.state_stride : 0);
   L.slot0 = L.g + (c.in_place ? 0 : L.state_stride);
   L.total = L.slot0 + uint64_t(plan.slots) * L.state_stride;
+  if (c.want_dp) {  // per-block slots of the constants' gradients
+    L.dp = L.total;
+    L.total += align_up(uint64_t(dparam_partial_bytes()));
+  }
   return L;
 }
 
 // Algorithmic HBM bytes per point of one forward / adjoint step and of the
 // seed: what the step must read and write at least once.
 void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd, uint64_t* adj,
-                     uint64_t* adj_first, uint64_t* seed) {
+                     uint64_t* adj_first, uint64_t* seed, uint64_t* dparam) {
   const uint64_t s = itemsize(c.shape.dtype);
   switch (c.shape.kind) {
     case ADST_JACOBI2D5:
@@ -137,13 +151,15 @@ void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd
       break;
   }
   *seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
+  // the constants' gradient kernel reads x_{t-1} and g_t (and K)
+  *dparam = c.want_dp ? (c.shape.kind == ADST_VARDIFF2D9 ? 3 : 2) * s : 0;
 }
 
 void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,
                adst_plan_info* info) {
   const Layout L = layout_for(c, plan);
-  uint64_t fb, ab, ab1, sb;
-  per_point_bytes(c, want_dk, loss, &fb, &ab, &ab1, &sb);
+  uint64_t fb, ab, ab1, sb, db;
+  per_point_bytes(c, want_dk, loss, &fb, &ab, &ab1, &sb, &db);
   *info = adst_plan_info{};
   info->steps = plan.steps;
   info->sched = plan.sched;
@@ -183,7 +199,7 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
         break;
       case ADST_OP_ADJ:
       case ADST_OP_ADJ2:
-        per_point += first_adj ? ab1 : ab;
+        per_point += (first_adj ? ab1 : ab) + db;
         first_adj = false;
         break;
       case ADST_OP_ADJW:
@@ -198,8 +214,8 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
 }
 
 adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
-                      int32_t want_dcoeff, Checked* c, Plan* plan) {
-  adst_status st = check_problem(prob, want_dcoeff, c);
+                      int32_t grads, Checked* c, Plan* plan) {
+  adst_status st = check_problem(prob, grads, c);
   if (st != ADST_OK) return st;
   if (steps < 0) return fail(ADST_ERR_ARG, "steps must be >= 0");
   const int64_t slots_avail = (int64_t)std::min<uint64_t>(budget / c->state_bytes, INT32_MAX);
@@ -243,7 +259,7 @@ adst_status check_disjoint(const std::vector<Range>& outs, const std::vector<Ran
 // markers themselves add no gap between back-to-back kernels of a run.
 class Tracer {
  public:
-  enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, NCAT };
+  enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, DPARAM, NCAT };
   explicit Tracer(bool on) : on_(on) {}
   ~Tracer() {
     for (auto& g : segs_) {
@@ -276,7 +292,7 @@ class Tracer {
     hipError_t r = close(s);
     if (r != hipSuccess || segs_.empty()) return r;
     if ((r = hipEventSynchronize(segs_.back().stop)) != hipSuccess) return r;
-    float ms[NCAT] = {0, 0, 0, 0};
+    float ms[NCAT] = {0, 0, 0, 0, 0};
     for (const Seg& g : segs_) {
       float dt = 0.f;
       if ((r = hipEventElapsedTime(&dt, g.start, g.stop)) != hipSuccess) return r;
@@ -290,6 +306,7 @@ class Tracer {
       info->ms_fwd_recompute = ms[RECOMPUTE];
       info->ms_adj = ms[ADJ];
       info->ms_seed = ms[SEED];
+      info->ms_dparams = ms[DPARAM];
       info->ms_total = total;
     }
     return hipSuccess;
@@ -318,25 +335,25 @@ using namespace adst;
 extern "C" {
 
 adst_status adst_plan(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
-                      int32_t sched, int32_t want_dcoeff, adst_plan_info* out) {
+                      int32_t sched, int32_t grads, adst_plan_info* out) {
   if (!out) return fail(ADST_ERR_ARG, "out is NULL");
   Checked c;
   Plan plan;
-  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff, &c, &plan);
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, grads, &c, &plan);
   if (st != ADST_OK) return st;
-  fill_info(c, plan, mem_budget_bytes, want_dcoeff != 0, ADST_LOSS_HALF_SQ, out);
+  fill_info(c, plan, mem_budget_bytes, c.want_dk, ADST_LOSS_HALF_SQ, out);
   g_last_error.clear();
   return ADST_OK;
 }
 
 adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
-                              int32_t sched, int32_t want_dcoeff, adst_action* out, int64_t cap,
+                              int32_t sched, int32_t grads, adst_action* out, int64_t cap,
                               int64_t* n_out) {
   if (!n_out) return fail(ADST_ERR_ARG, "n_out is NULL");
   if (cap < 0 || (cap > 0 && !out)) return fail(ADST_ERR_ARG, "bad output capacity");
   Checked c;
   Plan plan;
-  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dcoeff, &c, &plan);
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, grads, &c, &plan);
   if (st != ADST_OK) return st;
   const int64_t n = (int64_t)plan.acts.size();
   std::copy(plan.acts.begin(), plan.acts.begin() + std::min(n, cap), out);
@@ -402,12 +419,13 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
 
 adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
                      int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
-                     void* dx0, void* dcoeff, void* xT, double* loss_dev, void* ws,
-                     uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
-  const int32_t want_dk = dcoeff != nullptr;
+                     void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
+                     void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
+  const int32_t grads = (dcoeff ? ADST_GRAD_COEFF : 0) | (dparams ? ADST_GRAD_PARAMS : 0);
+  const bool want_dk = dcoeff != nullptr;
   Checked c;
   Plan plan;
-  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, want_dk, &c, &plan);
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, grads, &c, &plan);
   if (st != ADST_OK) return st;
   if (!x0 || !dx0) return fail(ADST_ERR_ARG, "x0 and dx0 are required");
   if (prob->kind == ADST_VARDIFF2D9 && !coeff)
@@ -425,12 +443,13 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   if (dcoeff) outs.push_back(range_of("dcoeff", dcoeff, S));
   if (xT) outs.push_back(range_of("xT", xT, S));
   if (loss_dev) outs.push_back(range_of("loss_dev", loss_dev, sizeof(double)));
+  if (dparams) outs.push_back(range_of("dparams", dparams, 2 * sizeof(double)));
   std::vector<Range> ins = {range_of("x0", x0, S)};
   if (prob->kind == ADST_VARDIFF2D9) ins.push_back(range_of("coeff", coeff, S));
   if (loss != ADST_LOSS_HALF_SQ) ins.push_back(range_of("loss_aux", loss_aux, S));
   st = check_disjoint(outs, ins);
   if (st != ADST_OK) return st;
-  if (info) fill_info(c, plan, mem_budget_bytes, want_dk != 0, loss, info);
+  if (info) fill_info(c, plan, mem_budget_bytes, want_dk, loss, info);
 
   // ---- interpret the plan
   // The adjoint ping-pongs between dx0 and the workspace buffer G, one swap
@@ -443,6 +462,7 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   void* gcur = (c.in_place || plan.adj_launches % 2 == 0) ? dx0 : gws;
   void* gnext = (gcur == dx0) ? gws : dx0;
   void* const g_T = gcur;
+  double* dp_part = reinterpret_cast<double*>(wsb + L.dp);
   auto buffer = [&](int32_t id) -> void* {
     switch (id) {
       case ADST_BUF_X0: return const_cast<void*>(x0);
@@ -488,11 +508,19 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
           e = launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
         if (e == hipSuccess && steps == 0 && dcoeff)
           e = launch_fill_zero(dcoeff, (int64_t)S, stream);
+        if (e == hipSuccess && steps == 0 && dparams)
+          e = launch_fill_zero(dparams, 2 * sizeof(double), stream);
         seeded = true;
         break;
       }
       case ADST_OP_ADJ: {
         const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
+        if (dparams) {  // this step's share of the constants' gradients, from g_t
+          if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
+          e = launch_dparam_step(c.shape, xs, coeff, gcur, dp_part, a.t == steps, stream);
+          if (e != hipSuccess) return hip_fail(e, "kernel launch");
+          if ((e = tr.before(stream, Tracer::ADJ)) != hipSuccess) return hip_fail(e, "trace event");
+        }
         e = launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps, stream);
         std::swap(gcur, gnext);
         break;
@@ -505,6 +533,11 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
         e = hipErrorInvalidValue;
     }
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  }
+  if (dparams && steps > 0) {
+    if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
+    if ((e = launch_dparam_finalize(dp_part, dparams, stream)) != hipSuccess)
+      return hip_fail(e, "kernel launch");
   }
   if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");
   g_last_error.clear();

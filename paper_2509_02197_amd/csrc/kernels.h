@@ -60,6 +60,15 @@ hipError_t launch_gs_forward(const StepShape& s, const void* src, void* dst, int
 hipError_t launch_gs_adjoint(const StepShape& s, void* g, int32_t sweeps, hipStream_t stream);
 int64_t gs_kernel_launches(const StepShape& s, bool adjoint, int32_t sweeps);
 
+// Gradients of the step constants: each adjoint step adds its share
+// sum_c g_t[c] dF_c/dp (x = x_{t-1}) into per-block slots (first = the
+// step t = T, which overwrites them); finalize sums the slots into
+// dparams[0..1] (device doubles).
+int64_t dparam_partial_bytes();
+hipError_t launch_dparam_step(const StepShape& s, const void* x, const void* K, const void* g,
+                              double* partials, bool first, hipStream_t stream);
+hipError_t launch_dparam_finalize(const double* partials, double* dparams, hipStream_t stream);
+
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream);
 

@@ -700,6 +700,98 @@ __global__ __launch_bounds__(kThreads) void finalize_loss(const double* __restri
   if (tid == 0) *out = s;
 }
 
+// ------------------------------------------- gradients of the step constants
+// One adjoint step's share of dL/dp: the sum over points of g_t[c] times the
+// step's partial dF_c/dp at x_{t-1} (a constant read by every point of every
+// step is a multiply-read input whose gradient accumulates, Sec. II). The
+// partials are the sub-expressions the forward step forms, in its order:
+//   Jacobi               dF/dw  = (((x[c]+x[W])+x[E])+x[S])+x[N] on interior points
+//   Allen-Cahn           dF/dD  = lap,   dF/dC = -((x[c]*x[c])*x[c])
+//   variable coefficient dF/ddt = acc
+// Products and sums are in double. A fixed grid with a fixed point-to-thread
+// assignment adds each block's sums into its own slot, step after step in
+// the adjoint order t = T..1, so the result does not depend on the schedule.
+constexpr int kDpBlocks = 2048;
+
+// Block sums of two values, each over the 256 threads in a fixed order.
+__device__ inline void block_sum2(double& a, double& b) {
+  a = block_sum(a);
+  __syncthreads();  // block_sum's wave sums are reused
+  b = block_sum(b);
+}
+
+template <class R, int KIND>
+__global__ __launch_bounds__(kThreads) void dparam_step(const R* __restrict__ x,
+                                                        const R* __restrict__ K,
+                                                        const R* __restrict__ g,
+                                                        double* __restrict__ part, int first,
+                                                        int nx, int ny, int nz, R ca, R cd) {
+  const int tid = threadIdx.y * kBX + threadIdx.x;
+  const int64_t plane = (int64_t)nx * ny, n = plane * nz;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  double a0 = 0.0, a1 = 0.0;
+  for (int64_t q = (int64_t)blockIdx.x * kThreads + tid; q < n; q += stride) {
+    const int i = (int)(q % nx);
+    const int64_t r = q / nx;
+    const int j = (int)(r % ny), k = (int)(r / ny);
+    const double gq = (double)g[q];
+    if (KIND == ADST_JACOBI2D5) {
+      if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
+        R sum = x[q];
+        sum += x[q - 1];
+        sum += x[q + 1];
+        sum += x[q - nx];
+        sum += x[q + nx];
+        a0 += gq * (double)sum;
+      }
+    } else if (KIND == ADST_ALLENCAHN3D7) {
+      const R a = x[q];
+      R lap = (i > 0 ? x[q - 1] : R(0)) + (i < nx - 1 ? x[q + 1] : R(0));
+      lap += j > 0 ? x[q - nx] : R(0);
+      lap += j < ny - 1 ? x[q + nx] : R(0);
+      lap += k > 0 ? x[q - plane] : R(0);
+      lap += k < nz - 1 ? x[q + plane] : R(0);
+      lap = lap - R(6) * a;
+      a0 += gq * (double)lap;
+      a1 += gq * (double)(-((a * a) * a));
+    } else {  // ADST_VARDIFF2D9
+      const R xc = x[q], Kc = K[q];
+      R acc = R(0);
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) {
+        const int ii = i + kNbrDx[nn], jj = j + kNbrDy[nn];
+        if (ii < 0 || ii >= nx || jj < 0 || jj >= ny) continue;
+        const int64_t m = q + (int64_t)kNbrDy[nn] * nx + kNbrDx[nn];
+        acc += ((nn < 4 ? ca : cd) * (Kc + K[m])) * (x[m] - xc);
+      }
+      a0 += gq * (double)acc;
+    }
+  }
+  block_sum2(a0, a1);
+  if (tid == 0) {
+    double* p0 = part + blockIdx.x;
+    double* p1 = part + kDpBlocks + blockIdx.x;
+    *p0 = first ? a0 : *p0 + a0;
+    *p1 = first ? a1 : *p1 + a1;
+  }
+}
+
+// dparams[k] = the sum of the kDpBlocks slots of constant k, in a fixed order.
+__global__ __launch_bounds__(kThreads) void dparam_finalize(const double* __restrict__ part,
+                                                            double* __restrict__ out) {
+  const int tid = threadIdx.y * kBX + threadIdx.x;
+  double a0 = 0.0, a1 = 0.0;
+  for (int i = tid; i < kDpBlocks; i += kThreads) {
+    a0 += part[i];
+    a1 += part[kDpBlocks + i];
+  }
+  block_sum2(a0, a1);
+  if (tid == 0) {
+    out[0] = a0;
+    out[1] = a1;
+  }
+}
+
 // --------------------------------------------------------------- utilities
 __global__ __launch_bounds__(kThreads) void fill_zero_u32(uint32_t* __restrict__ p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * kThreads;
@@ -905,6 +997,61 @@ hipError_t launch_seed(int32_t dtype, int32_t loss, int64_t n, const void* x, co
 hipError_t launch_finalize(const double* partials, int32_t nparts, double* loss,
                            hipStream_t stream) {
   finalize_loss<<<dim3(1), dim3(kBX, kBY), 0, stream>>>(partials, nparts, loss);
+  return hipGetLastError();
+}
+
+int64_t dparam_partial_bytes() { return int64_t(2) * kDpBlocks * sizeof(double); }
+
+hipError_t launch_dparam_step(const StepShape& s, const void* x, const void* K, const void* g,
+                              double* partials, bool first, hipStream_t stream) {
+  const dim3 grid(kDpBlocks), block(kBX, kBY);
+  const int f = first ? 1 : 0;
+  if (s.dtype == ADST_F64) {
+    const double* xd = static_cast<const double*>(x);
+    const double* Kd = static_cast<const double*>(K);
+    const double* gd = static_cast<const double*>(g);
+    switch (s.kind) {
+      case ADST_JACOBI2D5:
+        dparam_step<double, ADST_JACOBI2D5><<<grid, block, 0, stream>>>(
+            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 0.0, 0.0);
+        break;
+      case ADST_ALLENCAHN3D7:
+        dparam_step<double, ADST_ALLENCAHN3D7><<<grid, block, 0, stream>>>(
+            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 0.0, 0.0);
+        break;
+      case ADST_VARDIFF2D9:
+        dparam_step<double, ADST_VARDIFF2D9><<<grid, block, 0, stream>>>(
+            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 1.0 / 3.0, 1.0 / 12.0);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
+  } else {
+    const float* xf = static_cast<const float*>(x);
+    const float* Kf = static_cast<const float*>(K);
+    const float* gf = static_cast<const float*>(g);
+    switch (s.kind) {
+      case ADST_JACOBI2D5:
+        dparam_step<float, ADST_JACOBI2D5><<<grid, block, 0, stream>>>(
+            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 0.f, 0.f);
+        break;
+      case ADST_ALLENCAHN3D7:
+        dparam_step<float, ADST_ALLENCAHN3D7><<<grid, block, 0, stream>>>(
+            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 0.f, 0.f);
+        break;
+      case ADST_VARDIFF2D9:
+        dparam_step<float, ADST_VARDIFF2D9><<<grid, block, 0, stream>>>(
+            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 1.f / 3.f, 1.f / 12.f);
+        break;
+      default:
+        return hipErrorInvalidValue;
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dparam_finalize(const double* partials, double* dparams, hipStream_t stream) {
+  dparam_finalize<<<dim3(1), dim3(kBX, kBY), 0, stream>>>(partials, dparams);
   return hipGetLastError();
 }
 

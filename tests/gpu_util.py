@@ -37,10 +37,11 @@ def host(t):
 
 
 def gpu_vjp(kind, inp, steps, loss, budget=None, sched=adst.ADST_SCHED_AUTO, want_dK=False,
-            flags=0, params=None, ws=None, keep_ws=False, want_xT=True):
+            flags=0, params=None, ws=None, keep_ws=False, want_xT=True, want_dparams=False):
     import torch
     out = adst.vjp(kind, dev(inp["x0"]), dev(inp.get("K")), steps, loss, dev(inp.get("aux")),
-                   budget, sched, want_dK, params, flags, ws=ws, want_xT=want_xT)
+                   budget, sched, want_dK, params, flags, ws=ws, want_xT=want_xT,
+                   want_dparams=want_dparams)
     torch.cuda.synchronize()
     res = {k: host(v) for k, v in out.items() if k not in ("ws", "info")}
     res["loss"] = float(res["loss"])

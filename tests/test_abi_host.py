@@ -108,12 +108,12 @@ BIG = 1 << 40
 
 def _vjp(p, **kw):
     a = dict(x0=X0, coeff=None, steps=5, loss=adst.ADST_LOSS_HALF_SQ, loss_aux=None,
-             budget=BIG, sched=0, dx0=DX0, dcoeff=None, xT=None, loss_dev=None, ws=WS,
-             ws_bytes=BIG)
+             budget=BIG, sched=0, dx0=DX0, dcoeff=None, xT=None, loss_dev=None, dparams=None,
+             ws=WS, ws_bytes=BIG)
     a.update(kw)
     return _status(adst.adst_vjp, p, a["x0"], a["coeff"], a["steps"], a["loss"], a["loss_aux"],
-                   a["budget"], a["sched"], a["dx0"], a["dcoeff"], a["xT"], a["loss_dev"], a["ws"],
-                   a["ws_bytes"], 0)
+                   a["budget"], a["sched"], a["dx0"], a["dcoeff"], a["xT"], a["loss_dev"],
+                   a["dparams"], a["ws"], a["ws_bytes"], 0)
 
 
 def test_vjp_argument_errors():
@@ -132,6 +132,28 @@ def test_vjp_argument_errors():
     pv = _p(adst.ADST_VARDIFF2D9, (8, 8, 1))
     assert _vjp(pv) == E                                       # K missing
     assert _vjp(pv, coeff=K, dcoeff=K) == E                    # dK overlaps K
+    assert _vjp(p, dparams=DX0 + 8) == E                       # dparams overlaps dx0
+    assert _vjp(p, dparams=X0) == E                            # dparams overlaps x0
+    # the constants' gradients are not built for the in-place kind
+    assert _vjp(_p(adst.ADST_GAUSSSEIDEL2D5, (8, 8, 1)), dparams=LOSS) == \
+        adst.ADST_ERR_UNSUPPORTED
+
+
+def test_gradient_mask():
+    pj = _p(adst.ADST_JACOBI2D5, (8, 8, 1))
+    assert _status(adst.adst_plan, pj, 5, 0, 0, 4) == adst.ADST_ERR_ARG
+    assert _status(adst.adst_plan, _p(adst.ADST_GAUSSSEIDEL2D5, (8, 8, 1)), 5, 0, 0,
+                   adst.ADST_GRAD_PARAMS) == adst.ADST_ERR_UNSUPPORTED
+    # the constants' partials read x_{t-1}: the linear kinds now keep a tape
+    plain = adst.adst_plan(pj, 5, BIG, 0)
+    withp = adst.adst_plan(pj, 5, BIG, 0, adst.ADST_GRAD_PARAMS)
+    assert plain.needs_state == 0 and withp.needs_state == 1 and withp.slots == 3
+    # their per-block slots (2 x 2048 doubles) sit after the checkpoint slots
+    S = 8 * 8 * 8
+    stride = -(-S // 4096) * 4096
+    assert withp.workspace_bytes == 16384 + (3 + 3) * stride + 32768
+    # bytes: every adjoint step also reads x_{t-1} and g_t for the partials
+    assert withp.alg_bytes - (16 * 5 + 16 * 5 + 16) * 64 == 16 * 5 * 64
 
 
 def test_vjp_budget_and_workspace_errors():

@@ -99,8 +99,8 @@ def test_linear_kind_elides_the_tape():
             assert nfwd == 37 and not used
     # the coefficient field's gradient makes the variable-coefficient kind read state
     p = prob(adst.ADST_VARDIFF2D9, (6, 5, 1))
-    assert adst.adst_plan(p, 10, 0, 0, want_dcoeff=False).needs_state == 0
-    assert adst.adst_plan(p, 10, 0, 0, want_dcoeff=True).needs_state == 1
+    assert adst.adst_plan(p, 10, 0, 0, grads=0).needs_state == 0
+    assert adst.adst_plan(p, 10, 0, 0, grads=adst.ADST_GRAD_COEFF).needs_state == 1
     # forcing the tape makes a linear kind use the schedule
     p = prob(adst.ADST_JACOBI2D5, (6, 5, 1), flags=adst.ADST_FORCE_TAPE)
     acts = adst.adst_plan_actions(p, 37, budget_for(3, p), adst.ADST_SCHED_BINOMIAL)
