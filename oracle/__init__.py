@@ -34,13 +34,13 @@ def _load():
     ci = ctypes.c_int
     for suf in ("f64", "f32"):
         f = getattr(lib, "oracle_forward_" + suf)
-        f.argtypes = [ci, i64p, dp, vp, vp, ci, vp]
+        f.argtypes = [ci, i64p, dp, dp, vp, vp, ci, vp]
         f.restype = ci
         f = getattr(lib, "oracle_vjp_" + suf)
-        f.argtypes = [ci, i64p, dp, vp, vp, ci, ci, vp, vp, vp, vp, dp, dp]
+        f.argtypes = [ci, i64p, dp, dp, vp, vp, ci, ci, vp, vp, vp, vp, dp, dp]
         f.restype = ci
         f = getattr(lib, "oracle_jvp_" + suf)
-        f.argtypes = [ci, i64p, dp, vp, vp, vp, vp, dp, ci, vp, vp]
+        f.argtypes = [ci, i64p, dp, dp, vp, vp, vp, vp, dp, ci, vp, vp]
         f.restype = ci
     _lib = lib
     return lib
@@ -76,6 +76,11 @@ def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
+def _lim(lim):
+    """Limiter bounds (lo, hi) as a C array, or None for no limiter."""
+    return None if lim is None else (ctypes.c_double * 2)(float(lim[0]), float(lim[1]))
+
+
 def _prep(x0, *others):
     x0 = np.ascontiguousarray(x0)
     out = [x0]
@@ -90,20 +95,20 @@ def _args(kind, x0, params):
     return n, p
 
 
-def forward(kind, x0, K=None, steps=1, params=None):
-    """x_T after ``steps`` forward steps."""
+def forward(kind, x0, K=None, steps=1, params=None, lim=None):
+    """x_T after ``steps`` forward steps (lim = limiter bounds (lo, hi))."""
     x0, K = _prep(x0, K)
     n, p = _args(kind, x0, params)
     xT = np.empty_like(x0)
     rc = getattr(_load(), "oracle_forward_" + _suffix(x0.dtype))(
-        kind, n, p, _ptr(x0), _ptr(K), steps, _ptr(xT))
+        kind, n, p, _lim(lim), _ptr(x0), _ptr(K), steps, _ptr(xT))
     if rc:
         raise ValueError("oracle_forward rejected the problem")
     return xT
 
 
 def vjp(kind, x0, K=None, steps=1, loss=HALF_SQ, aux=None, want_dK=False, params=None,
-        want_dp=False):
+        want_dp=False, lim=None):
     """Store-all reverse-mode gradient. Returns (dx0, dK or None, x_T, L), and
     with want_dp also the gradients of the two step constants (dL/dp[0],
     dL/dp[1]) as a fifth element."""
@@ -115,7 +120,7 @@ def vjp(kind, x0, K=None, steps=1, loss=HALF_SQ, aux=None, want_dK=False, params
     L = ctypes.c_double(0.0)
     dpv = (ctypes.c_double * 2)(0.0, 0.0)
     rc = getattr(_load(), "oracle_vjp_" + _suffix(x0.dtype))(
-        kind, n, p, _ptr(x0), _ptr(K), steps, loss, _ptr(aux), _ptr(dx0), _ptr(dK),
+        kind, n, p, _lim(lim), _ptr(x0), _ptr(K), steps, loss, _ptr(aux), _ptr(dx0), _ptr(dK),
         _ptr(xT), ctypes.byref(L), dpv if want_dp else None)
     if rc:
         raise ValueError("oracle_vjp rejected the problem")
@@ -124,7 +129,7 @@ def vjp(kind, x0, K=None, steps=1, loss=HALF_SQ, aux=None, want_dK=False, params
     return dx0, dK, xT, L.value
 
 
-def jvp(kind, x0, v, K=None, kappa=None, steps=1, params=None, pdot=None):
+def jvp(kind, x0, v, K=None, kappa=None, steps=1, params=None, pdot=None, lim=None):
     """Tangent-linear sweep. Returns (x_T, xdot_T) for direction (v, kappa,
     pdot), pdot the direction of the two step constants."""
     x0, v, K, kappa = _prep(x0, v, K, kappa)
@@ -133,7 +138,8 @@ def jvp(kind, x0, v, K=None, kappa=None, steps=1, params=None, pdot=None):
     xdT = np.empty_like(x0)
     pd = None if pdot is None else (ctypes.c_double * 2)(*pdot)
     rc = getattr(_load(), "oracle_jvp_" + _suffix(x0.dtype))(
-        kind, n, p, _ptr(x0), _ptr(K), _ptr(v), _ptr(kappa), pd, steps, _ptr(xT), _ptr(xdT))
+        kind, n, p, _lim(lim), _ptr(x0), _ptr(K), _ptr(v), _ptr(kappa), pd, steps, _ptr(xT),
+        _ptr(xdT))
     if rc:
         raise ValueError("oracle_jvp rejected the problem")
     return xT, xdT

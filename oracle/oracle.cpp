@@ -50,6 +50,14 @@
 //              are dropped): x' = x[c] + dt * sum_n c_n (K[c]+K[n]) (x[n]-x[c]),
 //              c_n = 1/3 for axis neighbours, 1/12 for diagonal ones;
 //              p[0] = dt.
+// Optional limiter (a branch in every step, Sec. III-B's data-dependent
+// control flow): with bounds lim = {lo, hi} every point's new value y is
+// replaced by lo if y < lo, by hi if y > hi, and kept otherwise (the ring of
+// the 2-D kinds included). Its derivative is that of the branch taken: 1
+// where lo <= y <= hi, 0 elsewhere. The reverse sweep recovers each branch
+// outcome by re-evaluating y from the stored x_{t-1} (recomputation instead
+// of a stored branch record, which the forward's fixed evaluation order
+// makes exact). Not defined for the in-place kind.
 // Evaluation order and rounding: each forward formula is evaluated exactly in
 // the order written above, left to right, in the working precision R, with no
 // contraction into fused multiply-adds (built with -ffp-contract=off).
@@ -161,6 +169,33 @@ void step_forward(int kind, const Grid& g, const double* p, const R* x,
           out[c] = x[c] + dt * acc;
         }
       }
+}
+
+// The step followed by the limiter (lim = {lo, hi}, or null for none).
+template <class R>
+void step_forward_lim(int kind, const Grid& g, const double* p, const double* lim, const R* x,
+                      const R* K, R* out) {
+  step_forward<R>(kind, g, p, x, K, out);
+  if (!lim) return;
+  const R lo = R(lim[0]), hi = R(lim[1]);
+  for (int64_t c = 0; c < g.size(); ++c) {
+    if (out[c] < lo)
+      out[c] = lo;
+    else if (out[c] > hi)
+      out[c] = hi;
+  }
+}
+
+// The branch outcome of the limiter at every point: 1 where the step's
+// unlimited value y satisfies lo <= y <= hi (the value is kept), else 0.
+template <class R>
+void limiter_mask(int kind, const Grid& g, const double* p, const double* lim, const R* x,
+                  const R* K, std::vector<R>& y, std::vector<unsigned char>& keep) {
+  y.resize(g.size());
+  keep.resize(g.size());
+  step_forward<R>(kind, g, p, x, K, y.data());
+  const R lo = R(lim[0]), hi = R(lim[1]);
+  for (int64_t c = 0; c < g.size(); ++c) keep[c] = !(y[c] < lo) && !(y[c] > hi);
 }
 
 // -------------------------------------------------------- reverse (scatter)
@@ -383,13 +418,14 @@ int check_problem(int kind, const Grid& g, const R* K) {
 }
 
 template <class R>
-int forward(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
-            int steps, R* xT) {
+int forward(int kind, const int64_t* n, const double* p, const double* lim, const R* x0,
+            const R* K, int steps, R* xT) {
   Grid g{n[0], n[1], n[2]};
   if (check_problem(kind, g, K) || steps < 0) return -1;
+  if (lim && kind == GAUSSSEIDEL2D5) return -1;
   std::vector<R> a(x0, x0 + g.size()), b(g.size());
   for (int t = 1; t <= steps; ++t) {
-    step_forward<R>(kind, g, p, a.data(), K, b.data());
+    step_forward_lim<R>(kind, g, p, lim, a.data(), K, b.data());
     a.swap(b);
   }
   std::memcpy(xT, a.data(), sizeof(R) * g.size());
@@ -397,11 +433,12 @@ int forward(int kind, const int64_t* n, const double* p, const R* x0, const R* K
 }
 
 template <class R>
-int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
+int vjp(int kind, const int64_t* n, const double* p, const double* lim, const R* x0, const R* K,
         int steps, int loss, const R* aux, R* dx0, R* dK, R* xT, double* loss_out,
         double* dp_out) {
   Grid g{n[0], n[1], n[2]};
   if (check_problem(kind, g, K) || steps < 0) return -1;
+  if (lim && kind == GAUSSSEIDEL2D5) return -1;
   if (loss < HALF_SQ || loss > SEED) return -1;
   if (loss != HALF_SQ && !aux) return -1;
   const int64_t N = g.size();
@@ -410,7 +447,7 @@ int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
   std::vector<std::vector<R>> tape(steps + 1, std::vector<R>(N));
   std::memcpy(tape[0].data(), x0, sizeof(R) * N);
   for (int t = 1; t <= steps; ++t)
-    step_forward<R>(kind, g, p, tape[t - 1].data(), K, tape[t].data());
+    step_forward_lim<R>(kind, g, p, lim, tape[t - 1].data(), K, tape[t].data());
   const std::vector<R>& xt = tape[steps];
 
   // 2. loss and seed
@@ -440,7 +477,14 @@ int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
     d0.resize(N);
     d1.resize(N);
   }
+  std::vector<R> yv;
+  std::vector<unsigned char> keep;
   for (int t = steps; t >= 1; --t) {
+    if (lim) {  // the branch taken at each point: a clamped value has no dependence
+      limiter_mask<R>(kind, g, p, lim, tape[t - 1].data(), K, yv, keep);
+      for (int64_t i = 0; i < N; ++i)
+        if (!keep[i]) gcur[i] = R(0);
+    }
     if (dp_out && kind == GAUSSSEIDEL2D5) {
       // the sweep's own reverse carries the partials (see gauss_seidel_reverse)
       gauss_seidel_sums<R>(g, p, tape[t - 1].data(), d0.data());
@@ -475,10 +519,13 @@ int vjp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
 }
 
 template <class R>
-int jvp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
+int jvp(int kind, const int64_t* n, const double* p, const double* lim, const R* x0, const R* K,
         const R* v, const R* kappa, const double* pdot, int steps, R* xT, R* xdT) {
   Grid g{n[0], n[1], n[2]};
   if (check_problem(kind, g, K) || steps < 0 || !v) return -1;
+  if (lim && kind == GAUSSSEIDEL2D5) return -1;
+  std::vector<R> yv;
+  std::vector<unsigned char> keep;
   const int64_t N = g.size();
   std::vector<R> x(x0, x0 + N), xn(N), xd(v, v + N), xdn(N), d0(N), d1(N);
   for (int t = 1; t <= steps; ++t) {
@@ -510,7 +557,12 @@ int jvp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
       for (int64_t i = 0; i < N; ++i)
         xdn[i] = (xdn[i] + R(pdot[0]) * d0[i]) + R(pdot[1]) * d1[i];
     }
-    step_forward<R>(kind, g, p, x.data(), K, xn.data());
+    if (lim) {
+      limiter_mask<R>(kind, g, p, lim, x.data(), K, yv, keep);
+      for (int64_t i = 0; i < N; ++i)
+        if (!keep[i]) xdn[i] = R(0);
+    }
+    step_forward_lim<R>(kind, g, p, lim, x.data(), K, xn.data());
     x.swap(xn);
     xd.swap(xdn);
   }
@@ -523,33 +575,34 @@ int jvp(int kind, const int64_t* n, const double* p, const R* x0, const R* K,
 
 extern "C" {
 
-int oracle_forward_f64(int kind, const int64_t* n, const double* p, const double* x0,
-                       const double* K, int steps, double* xT) {
-  return forward<double>(kind, n, p, x0, K, steps, xT);
+// lim: {lo, hi} of the limiter, or null for none.
+int oracle_forward_f64(int kind, const int64_t* n, const double* p, const double* lim,
+                       const double* x0, const double* K, int steps, double* xT) {
+  return forward<double>(kind, n, p, lim, x0, K, steps, xT);
 }
-int oracle_forward_f32(int kind, const int64_t* n, const double* p, const float* x0,
-                       const float* K, int steps, float* xT) {
-  return forward<float>(kind, n, p, x0, K, steps, xT);
+int oracle_forward_f32(int kind, const int64_t* n, const double* p, const double* lim,
+                       const float* x0, const float* K, int steps, float* xT) {
+  return forward<float>(kind, n, p, lim, x0, K, steps, xT);
 }
-int oracle_vjp_f64(int kind, const int64_t* n, const double* p, const double* x0,
-                   const double* K, int steps, int loss, const double* aux, double* dx0,
-                   double* dK, double* xT, double* loss_out, double* dp_out) {
-  return vjp<double>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
+int oracle_vjp_f64(int kind, const int64_t* n, const double* p, const double* lim,
+                   const double* x0, const double* K, int steps, int loss, const double* aux,
+                   double* dx0, double* dK, double* xT, double* loss_out, double* dp_out) {
+  return vjp<double>(kind, n, p, lim, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
 }
-int oracle_vjp_f32(int kind, const int64_t* n, const double* p, const float* x0,
-                   const float* K, int steps, int loss, const float* aux, float* dx0,
-                   float* dK, float* xT, double* loss_out, double* dp_out) {
-  return vjp<float>(kind, n, p, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
+int oracle_vjp_f32(int kind, const int64_t* n, const double* p, const double* lim,
+                   const float* x0, const float* K, int steps, int loss, const float* aux,
+                   float* dx0, float* dK, float* xT, double* loss_out, double* dp_out) {
+  return vjp<float>(kind, n, p, lim, x0, K, steps, loss, aux, dx0, dK, xT, loss_out, dp_out);
 }
-int oracle_jvp_f64(int kind, const int64_t* n, const double* p, const double* x0,
-                   const double* K, const double* v, const double* kappa, const double* pdot,
-                   int steps, double* xT, double* xdT) {
-  return jvp<double>(kind, n, p, x0, K, v, kappa, pdot, steps, xT, xdT);
+int oracle_jvp_f64(int kind, const int64_t* n, const double* p, const double* lim,
+                   const double* x0, const double* K, const double* v, const double* kappa,
+                   const double* pdot, int steps, double* xT, double* xdT) {
+  return jvp<double>(kind, n, p, lim, x0, K, v, kappa, pdot, steps, xT, xdT);
 }
-int oracle_jvp_f32(int kind, const int64_t* n, const double* p, const float* x0,
-                   const float* K, const float* v, const float* kappa, const double* pdot,
-                   int steps, float* xT, float* xdT) {
-  return jvp<float>(kind, n, p, x0, K, v, kappa, pdot, steps, xT, xdT);
+int oracle_jvp_f32(int kind, const int64_t* n, const double* p, const double* lim,
+                   const float* x0, const float* K, const float* v, const float* kappa,
+                   const double* pdot, int steps, float* xT, float* xdT) {
+  return jvp<float>(kind, n, p, lim, x0, K, v, kappa, pdot, steps, xT, xdT);
 }
 
 }  // extern "C"
