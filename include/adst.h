@@ -116,6 +116,15 @@ typedef enum {
                                 the end of the call and fill the ms_* fields of adst_plan_info */
 #define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking);
                                 results are bit-identical either way */
+#define ADST_LIMIT 0x8u      /* a limiter on every step: each new value y (ring included)
+                                becomes lim[0] if y < lim[0], lim[1] if y > lim[1], else stays
+                                y. A data-dependent branch at every point of every step
+                                (Sec. III-B): its derivative is that of the branch taken (1
+                                where y was kept, 0 where clamped), and the reverse sweep
+                                recomputes each branch outcome from x_{t-1} with the
+                                forward's own expressions, so every adjoint reads state. Not
+                                built for the in-place kind (ADST_ERR_UNSUPPORTED); steps
+                                are then not fused. */
 
 /* Which gradients besides dx0 a plan is for (the `grads` argument).
  *   ADST_GRAD_COEFF   dK, the per-point coefficient field (VARDIFF2D9 only)
@@ -137,7 +146,8 @@ typedef struct {
   int64_t n[3];   /* n[0] = nx (fastest), n[1] = ny, n[2] = nz (1 for the 2-D kinds);
                      every n[i] >= 1 and n[0]*n[1]*n[2] < 2^31 */
   double p[2];    /* step constants, see the kinds above; rounded to the working precision */
-  uint32_t flags; /* ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE */
+  double lim[2];  /* limiter bounds lo <= hi (with ADST_LIMIT; rounded likewise) */
+  uint32_t flags; /* ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE | ADST_LIMIT */
 } adst_problem;
 
 /* One action of a reverse-sweep plan. Buffers are named by small integers:

@@ -21,7 +21,7 @@ ADST_JACOBI2D5, ADST_ALLENCAHN3D7, ADST_VARDIFF2D9, ADST_GAUSSSEIDEL2D5 = 0, 1, 
 ADST_F64, ADST_F32 = 0, 1
 ADST_SCHED_AUTO, ADST_SCHED_STORE_ALL, ADST_SCHED_UNIFORM, ADST_SCHED_BINOMIAL = 0, 1, 2, 3
 ADST_LOSS_HALF_SQ, ADST_LOSS_DOT_W, ADST_LOSS_HALF_SQ_DIFF, ADST_LOSS_SEED = 0, 1, 2, 3
-ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE = 0x1, 0x2, 0x4
+ADST_FORCE_TAPE, ADST_TRACE, ADST_NO_FUSE, ADST_LIMIT = 0x1, 0x2, 0x4, 0x8
 ADST_GRAD_COEFF, ADST_GRAD_PARAMS = 0x1, 0x2
 ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2, ADST_OP_FWDW, ADST_OP_ADJW = range(7)
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
@@ -34,7 +34,8 @@ ILP_EVENTS = {"alloc": 0, "free": 1, "produce": 2, "drop": 3, "recompute": 4,
 
 class adst_problem(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n", ctypes.c_int64 * 3),
-                ("p", ctypes.c_double * 2), ("flags", ctypes.c_uint32)]
+                ("p", ctypes.c_double * 2), ("lim", ctypes.c_double * 2),
+                ("flags", ctypes.c_uint32)]
 
 
 class adst_action(ctypes.Structure):
@@ -126,8 +127,9 @@ def _check(status):
         raise AdstError(status, f"{adst_status_str(status)}: {adst_last_error()}")
 
 
-def make_problem(kind, dtype, dims, params=None, flags=0):
-    """dims = (nx, ny, nz) with nx fastest."""
+def make_problem(kind, dtype, dims, params=None, flags=0, lim=None):
+    """dims = (nx, ny, nz) with nx fastest; lim = limiter bounds (lo, hi) or
+    None (sets ADST_LIMIT)."""
     from .workloads import DEFAULT_PARAMS
     p = adst_problem()
     p.kind, p.dtype = kind, dtype
@@ -135,6 +137,9 @@ def make_problem(kind, dtype, dims, params=None, flags=0):
         p.n[i] = int(dims[i])
     pp = params if params is not None else DEFAULT_PARAMS[kind]
     p.p[0], p.p[1] = float(pp[0]), float(pp[1])
+    if lim is not None:
+        p.lim[0], p.lim[1] = float(lim[0]), float(lim[1])
+        flags |= ADST_LIMIT
     p.flags = flags
     return p
 
@@ -229,10 +234,10 @@ def _dims(shape):
     raise ValueError(f"expected a 2-D or 3-D array, got {tuple(shape)}")
 
 
-def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
+def forward(kind, x0, coeff=None, steps=1, params=None, stream=None, lim=None):
     """x_T on the device of x0 (torch tensors, row-major)."""
     import torch
-    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params)
+    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, lim=lim)
     xT = torch.empty_like(x0)
     info = adst_plan(prob, steps, 1 << 62, ADST_SCHED_STORE_ALL)
     ws = torch.empty(max(info.fwd_workspace_bytes, 1), dtype=torch.uint8, device=x0.device)
@@ -242,7 +247,7 @@ def forward(kind, x0, coeff=None, steps=1, params=None, stream=None):
 
 def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_bytes=None,
         sched=ADST_SCHED_AUTO, want_dcoeff=False, params=None, flags=0, stream=None, ws=None,
-        want_xT=True, want_dparams=False):
+        want_xT=True, want_dparams=False, lim=None):
     """Allocate outputs and workspace with torch and run adst_vjp.
 
     budget_bytes=None means unlimited (store-all). Returns a dict with dx0,
@@ -250,7 +255,7 @@ def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_
     dparams (device double[2], or None unless want_dparams), info and the
     workspace."""
     import torch
-    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags)
+    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags, lim)
     if budget_bytes is None:
         budget_bytes = (1 << 63)
     grads = (ADST_GRAD_COEFF if want_dcoeff else 0) | (ADST_GRAD_PARAMS if want_dparams else 0)

@@ -56,8 +56,13 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
     return fail(ADST_ERR_ARG, "unknown kind " + std::to_string(p->kind));
   if (p->dtype != ADST_F64 && p->dtype != ADST_F32)
     return fail(ADST_ERR_ARG, "unknown dtype " + std::to_string(p->dtype));
-  if (p->flags & ~(ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE))
+  if (p->flags & ~(ADST_FORCE_TAPE | ADST_TRACE | ADST_NO_FUSE | ADST_LIMIT))
     return fail(ADST_ERR_ARG, "unknown flag bits");
+  const bool limit = (p->flags & ADST_LIMIT) != 0;
+  if (limit && !(p->lim[0] <= p->lim[1]))
+    return fail(ADST_ERR_ARG, "limiter bounds must satisfy lim[0] <= lim[1]");
+  if (limit && p->kind == ADST_GAUSSSEIDEL2D5)
+    return fail(ADST_ERR_UNSUPPORTED, "the limiter is not built for the in-place kind");
   for (int d = 0; d < 3; ++d)
     if (p->n[d] < 1) return fail(ADST_ERR_ARG, "every extent n[i] must be >= 1");
   if (p->n[0] > INT32_MAX || p->n[1] > INT32_MAX || p->n[2] > INT32_MAX)
@@ -85,17 +90,17 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
     return fail(ADST_ERR_UNSUPPORTED,
                 "the constants' gradients are not built for the in-place kind");
   out->shape = {p->kind, p->dtype, (int32_t)p->n[0], (int32_t)p->n[1], (int32_t)p->n[2],
-                p->p[0], p->p[1]};
+                p->p[0], p->p[1], limit ? 1 : 0, p->lim[0], p->lim[1]};
   out->npoints = n;
   out->state_bytes = uint64_t(n) * itemsize(p->dtype);
   const bool kind_reads_state = p->kind == ADST_ALLENCAHN3D7 ||
-                                (p->kind == ADST_VARDIFF2D9 && want_dk) || want_dp;
+                                (p->kind == ADST_VARDIFF2D9 && want_dk) || want_dp || limit;
   out->needs_state = kind_reads_state || (p->flags & ADST_FORCE_TAPE);
   out->want_dk = want_dk;
   out->want_dp = want_dp;
   out->trace = (p->flags & ADST_TRACE) != 0;
   const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
-  out->fuse_fwd = fuse && has_forward2(p->kind);
+  out->fuse_fwd = fuse && has_forward2(p->kind) && !limit;
   out->fuse_adj = fuse && has_adjoint2(p->kind);
   out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
   return ADST_OK;
@@ -153,6 +158,8 @@ void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd
   *seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
   // the constants' gradient kernel reads x_{t-1} and g_t (and K)
   *dparam = c.want_dp ? (c.shape.kind == ADST_VARDIFF2D9 ? 3 : 2) * s : 0;
+  // the limiter's branch mask reads x_{t-1} (and K) and updates g_t in place
+  if (c.shape.limit) *dparam += (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
 }
 
 void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,
@@ -515,6 +522,10 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
       }
       case ADST_OP_ADJ: {
         const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
+        if (c.shape.limit) {  // the branch each point took at step t
+          e = launch_limit_mask(c.shape, xs, coeff, gcur, stream);
+          if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        }
         if (dparams) {  // this step's share of the constants' gradients, from g_t
           if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
           e = launch_dparam_step(c.shape, xs, coeff, gcur, dp_part, a.t == steps, stream);

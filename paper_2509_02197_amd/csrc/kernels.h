@@ -14,6 +14,8 @@ struct StepShape {
   int32_t dtype;  // adst_dtype
   int32_t nx, ny, nz;
   double p0, p1;
+  int32_t limit;  // 1: every new value is clamped to [lo, hi] (a per-point branch)
+  double lo, hi;
 };
 
 // x_t = F(x_{t-1}; K): x -> y. K only for the variable-coefficient kind.
@@ -59,6 +61,12 @@ hipError_t launch_gs_forward(const StepShape& s, const void* src, void* dst, int
                              hipStream_t stream);
 hipError_t launch_gs_adjoint(const StepShape& s, void* g, int32_t sweeps, hipStream_t stream);
 int64_t gs_kernel_launches(const StepShape& s, bool adjoint, int32_t sweeps);
+
+// The limiter's branch outcome at step t: g[c] = 0 wherever the step's
+// unlimited value at c (re-evaluated from x = x_{t-1} with the forward's own
+// expressions) lies outside [lo, hi]; g is updated in place.
+hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, void* g,
+                             hipStream_t stream);
 
 // Gradients of the step constants: each adjoint step adds its share
 // sum_c g_t[c] dF_c/dp (x = x_{t-1}) into per-block slots (first = the

@@ -149,6 +149,17 @@ __device__ inline R vardiff_fwd_at(const R* sx, const R* sk, int q, int i, int j
   return xc + dt * acc;
 }
 
+// The limiter: a new value below lo becomes lo, above hi becomes hi (the
+// branch the step takes at each point; NaN passes through unchanged).
+template <class R>
+struct Limit {
+  R lo, hi;
+};
+template <class R>
+__device__ inline R limited(R y, Limit<R> l) {
+  return y < l.lo ? l.lo : (y > l.hi ? l.hi : y);
+}
+
 // Single-step tiles: TW columns x TR rows, halo one cell (staged as one
 // 16-byte chunk on each side).
 template <class R, int TW, int TR>
@@ -181,10 +192,12 @@ __device__ inline bool jacobi_all_avg(int ia, int ib, int ja, int jb, int nx, in
   return ia >= m && ib <= nx - 1 - m && ja >= m && jb <= ny - 1 - m;
 }
 
-// Forward (ADJ = false) or adjoint (ADJ = true) Jacobi step on one tile.
-template <class R, bool ADJ>
+// Forward (ADJ = false) or adjoint (ADJ = true) Jacobi step on one tile;
+// LIM clamps the forward's new values.
+template <class R, bool ADJ, bool LIM = false>
 __device__ inline void jacobi_tile(const R* __restrict__ x, R* __restrict__ y, int nx, int ny,
-                                   int tiles_x, int ntiles, int vec, R w) {
+                                   int tiles_x, int ntiles, int vec, R w, Limit<R> lim = {}) {
+  auto out = [&](R v) { return LIM ? limited(v, lim) : v; };
   using G = Tile2<R, kJacTW, kJacTR>;
   __shared__ R s[G::LR * G::LW];
   const int b = xcd_tile(ntiles);
@@ -198,7 +211,7 @@ __device__ inline void jacobi_tile(const R* __restrict__ x, R* __restrict__ y, i
   if (jacobi_all_avg<ADJ>(i0, i0 + kJacTW - 1, j0, j0 + kJacTR - 1, nx, ny)) {
 #pragma unroll
     for (int r = 0; r < kJacTR; ++r)
-      y[(j0 + r) * nx + i] = jacobi_avg_at<R, G::LW>(s, (r + 1) * G::LW + cx, w);
+      y[(j0 + r) * nx + i] = out(jacobi_avg_at<R, G::LW>(s, (r + 1) * G::LW + cx, w));
     return;
   }
 #pragma unroll
@@ -207,7 +220,7 @@ __device__ inline void jacobi_tile(const R* __restrict__ x, R* __restrict__ y, i
     if (j >= ny) break;
     const int q = (r + 1) * G::LW + cx;
     y[j * nx + i] = ADJ ? jacobi_adj_at<R, G::LW>(s, q, i, j, nx, ny, w)
-                        : jacobi_fwd_at<R, G::LW>(s, q, i, j, nx, ny, w);
+                        : out(jacobi_fwd_at<R, G::LW>(s, q, i, j, nx, ny, w));
   }
 }
 
@@ -271,11 +284,12 @@ __device__ inline void jacobi_tile_x2(const R* __restrict__ x, R* __restrict__ y
   }
 }
 
-template <class R>
+template <class R, bool LIM>
 __global__ __launch_bounds__(kJacTW) void fwd_jacobi2d5(const R* __restrict__ x,
                                                         R* __restrict__ y, int nx, int ny,
-                                                        int tiles_x, int ntiles, int vec, R w) {
-  jacobi_tile<R, false>(x, y, nx, ny, tiles_x, ntiles, vec, w);
+                                                        int tiles_x, int ntiles, int vec, R w,
+                                                        Limit<R> lim) {
+  jacobi_tile<R, false, LIM>(x, y, nx, ny, tiles_x, ntiles, vec, w, lim);
 }
 template <class R>
 __global__ __launch_bounds__(kJacTW) void adj_jacobi2d5(const R* __restrict__ g,
@@ -363,11 +377,12 @@ __device__ inline R allencahn_point(R a, R xm, R xp, R ym, R yp, R zm, R zp, R D
   return (a + D * lap) - C * ((a * a) * a);
 }
 
-template <class R>
+template <class R, bool LIM>
 __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict__ x,
                                                              R* __restrict__ y, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
-                                                             int ntiles, R D, R C) {
+                                                             int ntiles, R D, R C, Limit<R> lim) {
+  auto out = [&](R v) { return LIM ? limited(v, lim) : v; };
   __shared__ R tile[kAcTY + 2][kAcTX + 2];
   AcTile t;
   if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;
@@ -393,12 +408,12 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
     __syncthreads();
     if (va)
       y[k * plane + t.ja * nx + t.i] =
-          allencahn_point(curA, tile[ty + 1][tx], tile[ty + 1][tx + 2], tile[ty][tx + 1],
-                          tile[ty + 2][tx + 1], belowA, aboveA, D, C);
+          out(allencahn_point(curA, tile[ty + 1][tx], tile[ty + 1][tx + 2], tile[ty][tx + 1],
+                              tile[ty + 2][tx + 1], belowA, aboveA, D, C));
     if (vb)
       y[k * plane + t.jb * nx + t.i] =
-          allencahn_point(curB, tile[ty + 5][tx], tile[ty + 5][tx + 2], tile[ty + 4][tx + 1],
-                          tile[ty + 6][tx + 1], belowB, aboveB, D, C);
+          out(allencahn_point(curB, tile[ty + 5][tx], tile[ty + 5][tx + 2], tile[ty + 4][tx + 1],
+                              tile[ty + 6][tx + 1], belowB, aboveB, D, C));
     belowA = curA;
     belowB = curB;
     curA = aboveA;
@@ -568,12 +583,12 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
 // ------------------------------------------ variable-coefficient diffusion 2-D
 constexpr int kVdTW = 256, kVdTR = 8, kVdAdjTR = 4;
 
-template <class R>
+template <class R, bool LIM>
 __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
                                                         const R* __restrict__ K,
                                                         R* __restrict__ y, int nx, int ny,
                                                         int tiles_x, int ntiles, int vec, R dt,
-                                                        R ca, R cd) {
+                                                        R ca, R cd, Limit<R> lim) {
   using G = Tile2<R, kVdTW, kVdTR>;
   __shared__ R sx[G::LR * G::LW];
   __shared__ R sk[G::LR * G::LW];
@@ -590,7 +605,8 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
   for (int r = 0; r < kVdTR; ++r) {
     const int j = j0 + r;
     if (j >= ny) break;
-    y[j * nx + i] = vardiff_fwd_at<R, G::LW>(sx, sk, (r + 1) * G::LW + cx, i, j, nx, ny, dt, ca, cd);
+    const R v = vardiff_fwd_at<R, G::LW>(sx, sk, (r + 1) * G::LW + cx, i, j, nx, ny, dt, ca, cd);
+    y[j * nx + i] = LIM ? limited(v, lim) : v;
   }
 }
 
@@ -698,6 +714,51 @@ __global__ __launch_bounds__(kThreads) void finalize_loss(const double* __restri
   for (int i = tid; i < nparts; i += kThreads) acc += partials[i];
   const double s = block_sum(acc);
   if (tid == 0) *out = s;
+}
+
+// ------------------------------------------------------- limiter branches
+// The limiter's derivative is that of the branch taken: a clamped value
+// depends on nothing, so g_t is zeroed where the step's unlimited value y
+// left [lo, hi]. y is re-evaluated from x_{t-1} (Sec. III-B: branch outcomes
+// recomputed rather than stored) through the same per-point functions the
+// forward kernels use, fed from a small local neighbourhood, so every
+// branch is decided on the bits the forward step produced.
+template <class R, int KIND>
+__global__ __launch_bounds__(kThreads) void limit_mask(const R* __restrict__ x,
+                                                       const R* __restrict__ K,
+                                                       R* __restrict__ g, int nx, int ny, int nz,
+                                                       R p0, R p1, R ca, R cd, Limit<R> lim) {
+  const int tid = threadIdx.y * kBX + threadIdx.x;
+  const int64_t plane = (int64_t)nx * ny, n = plane * nz;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t q = (int64_t)blockIdx.x * kThreads + tid; q < n; q += stride) {
+    const int i = (int)(q % nx);
+    const int64_t r = q / nx;
+    const int j = (int)(r % ny), k = (int)(r / ny);
+    R y;
+    if (KIND == ADST_ALLENCAHN3D7) {
+      y = allencahn_point(x[q], i > 0 ? x[q - 1] : R(0), i < nx - 1 ? x[q + 1] : R(0),
+                          j > 0 ? x[q - nx] : R(0), j < ny - 1 ? x[q + nx] : R(0),
+                          k > 0 ? x[q - plane] : R(0), k < nz - 1 ? x[q + plane] : R(0), p0, p1);
+    } else {
+      // 3 x 3 neighbourhood, row stride 3, centre at 4; 0 outside the grid
+      R sx[9], sk[9];
+#pragma unroll
+      for (int dy = -1; dy <= 1; ++dy)
+#pragma unroll
+        for (int dx = -1; dx <= 1; ++dx) {
+          const bool in = i + dx >= 0 && i + dx < nx && j + dy >= 0 && j + dy < ny;
+          const int64_t m = q + (int64_t)dy * nx + dx;
+          sx[(dy + 1) * 3 + dx + 1] = in ? x[m] : R(0);
+          if (KIND == ADST_VARDIFF2D9) sk[(dy + 1) * 3 + dx + 1] = in ? K[m] : R(0);
+        }
+      if (KIND == ADST_JACOBI2D5)
+        y = jacobi_fwd_at<R, 3>(sx, 4, i, j, nx, ny, p0);
+      else
+        y = vardiff_fwd_at<R, 3>(sx, sk, 4, i, j, nx, ny, p0, ca, cd);
+    }
+    if (y < lim.lo || y > lim.hi) g[q] = R(0);
+  }
 }
 
 // ------------------------------------------- gradients of the step constants
@@ -833,6 +894,8 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
   const R* x = static_cast<const R*>(xv);
   const R* K = static_cast<const R*>(Kv);
   R* y = static_cast<R*>(yv);
+  const Limit<R> lim{R(s.lo), R(s.hi)};
+  if (two && s.limit) return hipErrorInvalidValue;  // fused steps have no limiter
   switch (s.kind) {
     case ADST_JACOBI2D5: {
       if (two) {
@@ -841,8 +904,12 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
             x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
       } else {
         const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
-        fwd_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
-            x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0));
+        if (s.limit)
+          fwd_jacobi2d5<R, true><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+              x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0), lim);
+        else
+          fwd_jacobi2d5<R, false><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+              x, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x), R(s.p0), lim);
       }
       break;
     }
@@ -855,17 +922,26 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       } else {
         const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
         const int nt = tx * ty * cdiv(s.nz, kAcZC);
-        fwd_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-            x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+        if (s.limit)
+          fwd_allencahn3d7<R, true><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
+        else
+          fwd_allencahn3d7<R, false><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
       }
       break;
     }
     case ADST_VARDIFF2D9: {
       if (two) return hipErrorInvalidValue;
       const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
-      fwd_vardiff2d9<R><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-          x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
-          R(1) / R(12));
+      if (s.limit)
+        fwd_vardiff2d9<R, true><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
+            R(1) / R(12), lim);
+      else
+        fwd_vardiff2d9<R, false><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
+            R(1) / R(12), lim);
       break;
     }
     default:
@@ -998,6 +1074,40 @@ hipError_t launch_finalize(const double* partials, int32_t nparts, double* loss,
                            hipStream_t stream) {
   finalize_loss<<<dim3(1), dim3(kBX, kBY), 0, stream>>>(partials, nparts, loss);
   return hipGetLastError();
+}
+
+template <class R>
+hipError_t limit_mask_t(const StepShape& s, const void* xv, const void* Kv, void* gv,
+                        hipStream_t st) {
+  const R* x = static_cast<const R*>(xv);
+  const R* K = static_cast<const R*>(Kv);
+  R* g = static_cast<R*>(gv);
+  const int64_t n = (int64_t)s.nx * s.ny * s.nz;
+  const dim3 grid(grid_for(n, 4 * kThreads, 65536)), block(kBX, kBY);
+  const Limit<R> lim{R(s.lo), R(s.hi)};
+  switch (s.kind) {
+    case ADST_JACOBI2D5:
+      limit_mask<R, ADST_JACOBI2D5><<<grid, block, 0, st>>>(x, K, g, s.nx, s.ny, s.nz, R(s.p0),
+                                                            R(s.p1), R(0), R(0), lim);
+      break;
+    case ADST_ALLENCAHN3D7:
+      limit_mask<R, ADST_ALLENCAHN3D7><<<grid, block, 0, st>>>(x, K, g, s.nx, s.ny, s.nz,
+                                                               R(s.p0), R(s.p1), R(0), R(0), lim);
+      break;
+    case ADST_VARDIFF2D9:
+      limit_mask<R, ADST_VARDIFF2D9><<<grid, block, 0, st>>>(
+          x, K, g, s.nx, s.ny, s.nz, R(s.p0), R(s.p1), R(1) / R(3), R(1) / R(12), lim);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, void* g,
+                             hipStream_t stream) {
+  return s.dtype == ADST_F64 ? limit_mask_t<double>(s, x, K, g, stream)
+                             : limit_mask_t<float>(s, x, K, g, stream);
 }
 
 int64_t dparam_partial_bytes() { return int64_t(2) * kDpBlocks * sizeof(double); }

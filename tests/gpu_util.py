@@ -37,11 +37,12 @@ def host(t):
 
 
 def gpu_vjp(kind, inp, steps, loss, budget=None, sched=adst.ADST_SCHED_AUTO, want_dK=False,
-            flags=0, params=None, ws=None, keep_ws=False, want_xT=True, want_dparams=False):
+            flags=0, params=None, ws=None, keep_ws=False, want_xT=True, want_dparams=False,
+            lim=None):
     import torch
     out = adst.vjp(kind, dev(inp["x0"]), dev(inp.get("K")), steps, loss, dev(inp.get("aux")),
                    budget, sched, want_dK, params, flags, ws=ws, want_xT=want_xT,
-                   want_dparams=want_dparams)
+                   want_dparams=want_dparams, lim=lim)
     torch.cuda.synchronize()
     res = {k: host(v) for k, v in out.items() if k not in ("ws", "info")}
     res["loss"] = float(res["loss"])

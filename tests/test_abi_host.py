@@ -50,8 +50,8 @@ def test_status_strings():
 
 
 def test_struct_layouts_match_header():
-    # int32 x2, int64 x3, double x2, uint32 (+pad) = 56 bytes
-    assert ctypes.sizeof(adst.adst_problem) == 56
+    # int32 x2, int64 x3, double x4, uint32 (+pad) = 72 bytes
+    assert ctypes.sizeof(adst.adst_problem) == 72
     assert ctypes.sizeof(adst.adst_action) == 20
     # int32 x4, int64 x8, uint64 x6, float x6
     assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 8 * 8 + 6 * 8 + 6 * 4
@@ -137,6 +137,20 @@ def test_vjp_argument_errors():
     # the constants' gradients are not built for the in-place kind
     assert _vjp(_p(adst.ADST_GAUSSSEIDEL2D5, (8, 8, 1)), dparams=LOSS) == \
         adst.ADST_ERR_UNSUPPORTED
+
+
+def test_limiter_arguments():
+    pj = _p(adst.ADST_JACOBI2D5, (8, 8, 1))
+    assert adst.adst_plan(pj, 5, BIG, 0).needs_state == 0
+    lim = adst.make_problem(adst.ADST_JACOBI2D5, adst.ADST_F64, (8, 8, 1), lim=(0.2, 0.8))
+    info = adst.adst_plan(lim, 5, BIG, 0)
+    assert info.needs_state == 1 and info.fwd_launches == info.fwd_steps_total  # no fused steps
+    bad = adst.make_problem(adst.ADST_JACOBI2D5, adst.ADST_F64, (8, 8, 1), lim=(0.8, 0.2))
+    assert _status(adst.adst_plan, bad, 5, 0, 0) == adst.ADST_ERR_ARG
+    nan = adst.make_problem(adst.ADST_JACOBI2D5, adst.ADST_F64, (8, 8, 1), lim=(float("nan"), 1))
+    assert _status(adst.adst_plan, nan, 5, 0, 0) == adst.ADST_ERR_ARG
+    gs = adst.make_problem(adst.ADST_GAUSSSEIDEL2D5, adst.ADST_F64, (8, 8, 1), lim=(0, 1))
+    assert _status(adst.adst_plan, gs, 5, 0, 0) == adst.ADST_ERR_UNSUPPORTED
 
 
 def test_gradient_mask():

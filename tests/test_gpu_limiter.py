@@ -1,0 +1,114 @@
+"""The per-step limiter (a data-dependent branch at every point) on the GPU
+vs the CPU oracle, through the C-ABI (needs an MI355X).
+
+Bars as for the unlimited steps: forward states bit-identical (the branch
+is decided on identical bits), gradients within 1e-12 (fp64) / 1e-5 (fp32),
+every schedule bit-identical; infinite bounds reproduce the unlimited bits.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2509_02197_amd as adst
+from tests.gpu_util import NP_DTYPE, TOL, dev, gpu_vjp, rel, say
+
+pytestmark = pytest.mark.gpu
+
+J, AC, VD = adst.ADST_JACOBI2D5, adst.ADST_ALLENCAHN3D7, adst.ADST_VARDIFF2D9
+F64, F32 = adst.ADST_F64, adst.ADST_F32
+HALF_SQ, DOT_W, DIFF, SEED = (adst.ADST_LOSS_HALF_SQ, adst.ADST_LOSS_DOT_W,
+                              adst.ADST_LOSS_HALF_SQ_DIFF, adst.ADST_LOSS_SEED)
+LIM = {J: (0.35, 0.65), AC: (-0.45, 0.5), VD: (0.3, 0.7)}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    adst.lib()
+
+
+def inputs(kind, dtype, shape, seed):
+    r = np.random.Generator(np.random.PCG64(seed))
+    lo = -1.0 if kind == AC else 0.0
+    dt = NP_DTYPE[dtype]
+    return {"x0": r.uniform(lo, 1, shape).astype(dt),
+            "K": r.uniform(0.5, 1.5, shape).astype(dt) if kind == VD else None,
+            "aux": r.standard_normal(shape).astype(dt)}
+
+
+FORWARD_CASES = [(J, F64, (64, 64), 10), (J, F32, (130, 70), 5), (J, F64, (333, 517), 7),
+                 (AC, F64, (39, 45, 67), 6), (AC, F32, (17, 33, 65), 4), (VD, F32, (257, 300), 9),
+                 (VD, F64, (70, 129), 6), (J, F64, (2, 9), 4)]
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T", FORWARD_CASES)
+def test_limited_forward_bitwise(kind, dtype, shape, T):
+    say(f"limited forward kind={kind} dtype={dtype} shape={shape} T={T}")
+    inp = inputs(kind, dtype, shape, 1)
+    g = adst.forward(kind, dev(inp["x0"]), dev(inp["K"]), T, lim=LIM[kind]).cpu().numpy()
+    ref = oracle.forward(kind, inp["x0"], K=inp["K"], steps=T, lim=LIM[kind])
+    assert np.array_equal(g, ref)
+    if min(shape) > 2:  # the limiter changed the trajectory
+        assert not np.array_equal(ref, oracle.forward(kind, inp["x0"], K=inp["K"], steps=T))
+
+
+VJP_CASES = [
+    (J, F64, (64, 64), 10, HALF_SQ, False, False),
+    (J, F64, (333, 517), 7, DIFF, False, True),
+    (J, F32, (130, 70), 5, SEED, False, False),
+    (AC, F64, (39, 45, 67), 6, DOT_W, False, True),
+    (AC, F32, (17, 33, 65), 4, DIFF, False, False),
+    (VD, F32, (257, 300), 9, DIFF, True, True),
+    (VD, F64, (70, 129), 6, DOT_W, True, False),
+    (J, F64, (2, 9), 4, DOT_W, False, False),
+]
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T,loss,dK,dp", VJP_CASES)
+def test_limited_vjp_matches_oracle(kind, dtype, shape, T, loss, dK, dp):
+    say(f"limited vjp kind={kind} dtype={dtype} shape={shape} T={T} loss={loss} dK={dK} dp={dp}")
+    inp = inputs(kind, dtype, shape, 2)
+    g = gpu_vjp(kind, inp, T, loss, 2 * inp["x0"].nbytes, adst.ADST_SCHED_AUTO, dK,
+                want_dparams=dp, lim=LIM[kind])
+    assert g["info"]["needs_state"] == 1
+    ref = oracle.vjp(kind, inp["x0"], K=inp["K"], steps=T, loss=loss, aux=inp["aux"],
+                     want_dK=dK, want_dp=True, lim=LIM[kind])
+    tol = TOL[dtype]
+    assert np.array_equal(g["xT"], ref[2])
+    e = rel(g["dx0"], ref[0])
+    say(f"  dx0 rel {e:.2e}")
+    assert e <= tol
+    if dK:
+        assert rel(g["dK"], ref[1]) <= tol
+    assert abs(g["loss"] - ref[3]) <= tol * max(abs(ref[3]), 1e-300)
+    if dp:
+        for k in range(2):
+            if ref[4][k] == 0.0:
+                assert g["dparams"][k] == 0.0
+            else:
+                assert abs(g["dparams"][k] - ref[4][k]) <= tol * abs(ref[4][k])
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T,loss", [(J, F64, (90, 130), 15, HALF_SQ),
+                                                     (AC, F64, (20, 30, 70), 13, DOT_W),
+                                                     (VD, F32, (100, 130), 11, DIFF)])
+def test_limited_schedules_bitwise(kind, dtype, shape, T, loss):
+    inp = inputs(kind, dtype, shape, 3)
+    S = inp["x0"].nbytes
+    ref = gpu_vjp(kind, inp, T, loss, None, adst.ADST_SCHED_STORE_ALL, lim=LIM[kind])
+    for budget, sched in ((0, adst.ADST_SCHED_BINOMIAL), (2 * S, adst.ADST_SCHED_BINOMIAL),
+                          (3 * S, adst.ADST_SCHED_UNIFORM)):
+        g = gpu_vjp(kind, inp, T, loss, budget, sched, lim=LIM[kind])
+        assert g["info"]["recompute_steps"] > 0
+        assert np.array_equal(g["dx0"], ref["dx0"]) and g["loss"] == ref["loss"]
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T,loss", [(J, F64, (64, 70), 9, HALF_SQ),
+                                                     (AC, F64, (9, 10, 11), 5, DOT_W)])
+def test_infinite_bounds_give_the_unlimited_bits(kind, dtype, shape, T, loss):
+    inp = inputs(kind, dtype, shape, 4)
+    a = gpu_vjp(kind, inp, T, loss)
+    b = gpu_vjp(kind, inp, T, loss, lim=(-np.inf, np.inf))
+    assert np.array_equal(a["xT"], b["xT"]) and np.array_equal(a["dx0"], b["dx0"])
