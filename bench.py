@@ -48,6 +48,8 @@ def parse():
                     help="one launch per step (no temporal blocking)")
     ap.add_argument("--dparams", action="store_true",
                     help="also compute the gradients of the scalar step constants")
+    ap.add_argument("--limit", type=float, nargs=2, default=None, metavar=("LO", "HI"),
+                    help="clamp every step's new values to [LO, HI] (a per-point branch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
@@ -79,21 +81,23 @@ def traffic_for(workload, kernel, kind):
     return e["bytes_per_launch"]
 
 
-def cpu_baseline(w, inp, target_s):
+def cpu_baseline(w, inp, target_s, lim=None, want_dp=False):
     """The oracle (single-threaded store-all tape, as it stands) on the same
-    grid for as many leading steps as fit about target_s seconds."""
+    grid, with the same limiter and gradients, for as many leading steps as
+    fit about target_s seconds."""
     import oracle
     from paper_2509_02197_amd.workloads import dims_of  # noqa: F401
     x0, K, aux = inp["x0"], inp["K"], inp["aux"]
     n = x0.size
     # warm the pages once, then probe two steps to size the sample
-    oracle.vjp(w.kind, x0, K=K, steps=1, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    kw = dict(K=K, loss=w.loss, aux=aux, want_dK=w.want_dK, want_dp=want_dp, lim=lim)
+    oracle.vjp(w.kind, x0, steps=1, **kw)
     t0 = time.perf_counter()
-    oracle.vjp(w.kind, x0, K=K, steps=2, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    oracle.vjp(w.kind, x0, steps=2, **kw)
     one = (time.perf_counter() - t0) / 2
     Ts = int(max(1, min(w.steps, target_s / max(one, 1e-6))))
     t0 = time.perf_counter()
-    oracle.vjp(w.kind, x0, K=K, steps=Ts, loss=w.loss, aux=aux, want_dK=w.want_dK)
+    oracle.vjp(w.kind, x0, steps=Ts, **kw)
     dt = time.perf_counter() - t0
     return {"value": n * Ts / dt, "unit": "grid-point-steps/s", "cores": 1, "kind": "oracle",
             "sample": f"full {'x'.join(map(str, x0.shape))} grid, first {Ts} of {w.steps} steps, "
@@ -139,7 +143,7 @@ def main():
     x0 = torch.from_numpy(inp["x0"]).to(dev)
     K = torch.from_numpy(inp["K"]).to(dev) if inp["K"] is not None else None
     aux = torch.from_numpy(inp["aux"]).to(dev) if inp["aux"] is not None else None
-    prob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params, flags)
+    prob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params, flags, args.limit)
     grads = (adst.ADST_GRAD_COEFF if w.want_dK else 0) | \
         (adst.ADST_GRAD_PARAMS if args.dparams else 0)
     info = adst.adst_plan(prob, w.steps, budget, sched, grads)
@@ -175,7 +179,7 @@ def main():
 
     # ---- roofline leg: the same K calls with per-launch HIP events
     tprob = adst.make_problem(w.kind, w.dtype, dims_of(w.shape), w.params,
-                              flags | adst.ADST_TRACE)
+                              flags | adst.ADST_TRACE, args.limit)
     acc = {"ms_fwd_sweep": 0.0, "ms_fwd_recompute": 0.0, "ms_adj": 0.0, "ms_seed": 0.0,
            "ms_dparams": 0.0, "ms_total": 0.0}
     for _ in range(args.steps):
@@ -252,6 +256,7 @@ def main():
             "adj_kernels": info.adj_kernels,
             "grads": ("dx0,dK" if w.want_dK else "dx0") + (",dparams" if args.dparams else ""),
             "force_tape": bool(args.force_tape), "temporal_blocking": not args.no_fuse,
+            "limiter": args.limit,
         },
         "hbm_gbps_effective": round(info.alg_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "event_ms_per_step": ev_ms / args.steps,
@@ -268,7 +273,7 @@ def main():
         res["copy_probe_bytes"] = a.numel() * 8
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds, args.limit, args.dparams)
     print(json.dumps(res), flush=True)
 
 
