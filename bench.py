@@ -32,6 +32,28 @@ KERNELS = {  # (forward, adjoint) kernel names as rocprofv3 reports them
     2: ("fwd_vardiff2d9", "adj_vardiff2d9"),
     3: ("gs_wave<fwd>", "gs_wave<adj>"),
 }
+
+
+def kernel_name(kind, adj, n):
+    """Short name of the kernel an action of n steps launches."""
+    base = KERNELS[kind][1 if adj else 0]
+    if kind == 3 or n == 1:
+        return base
+    if n == 2:
+        return base + "_x2"
+    return f"jacobi_march<{'adj' if adj else 'fwd'},{n}>"
+
+
+def kernel_mix(kind, acts, adj):
+    """Action count per kernel name over a plan's forward or adjoint actions
+    (a pipelined run of the in-place kind counts once)."""
+    ops = (2, 4, 6) if adj else (0, 3, 5)  # ADJ, ADJ2, ADJW / FWD, FWD2, FWDW
+    mix = {}
+    for op, _t, _s, _d, n in acts:
+        if op in ops:
+            k = kernel_name(kind, adj, n)
+            mix[k] = mix.get(k, 0) + 1
+    return mix
 KERNEL_SOURCE = {0: "kernels.hip", 1: "kernels.hip", 2: "kernels.hip", 3: "gauss_seidel.hip"}
 
 
@@ -147,6 +169,7 @@ def main():
     grads = (adst.ADST_GRAD_COEFF if w.want_dK else 0) | \
         (adst.ADST_GRAD_PARAMS if args.dparams else 0)
     info = adst.adst_plan(prob, w.steps, budget, sched, grads)
+    acts = adst.adst_plan_actions(prob, w.steps, budget, sched, grads)
     ws = torch.empty(info.workspace_bytes, dtype=torch.uint8, device=dev)
     dx0 = torch.empty_like(x0)
     dK = torch.empty_like(x0) if w.want_dK else None
@@ -186,11 +209,12 @@ def main():
         ti = call(tprob)
         for k in acc:
             acc[k] += getattr(ti, k) / args.steps
-    # Roofline of the dominant kernel: its algorithmic bytes (inputs read
-    # once and outputs written once per launch; a fused two-step launch
-    # moves the same bytes as a single step; the in-place kind's pipelined
-    # runs move 2 * itemsize per point per step) over its launch time.
-    # avg_launch_ms is that time over the kernel dispatches.
+    # Roofline of the dominant phase's kernel: its algorithmic bytes (inputs
+    # read once and outputs written once per launch; a launch of n fused
+    # steps moves the same bytes as a single step; the in-place kind's
+    # pipelined runs move 2 * itemsize per point per step) over its launch
+    # time. avg_launch_ms is the phase's time over its kernel dispatches; the
+    # kernel named is the phase's most frequent one, kernel_mix the rest.
     isz = 8 if w.dtype == adst.ADST_F64 else 4
     fwd_B = {0: 2, 1: 2, 2: 3, 3: 2}[w.kind] * isz
     adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3, 3: 2}[w.kind] * isz
@@ -199,33 +223,23 @@ def main():
     fwd_units = info.fwd_steps_total if in_place else info.fwd_launches
     adj_units = info.adj_steps if in_place else info.adj_launches
     n_fwd, n_adj = info.fwd_kernels, info.adj_kernels
-    fused_fwd = 0 if in_place else info.fwd_steps_total - info.fwd_launches
-    fused_adj = 0 if in_place else info.adj_steps - info.adj_launches
     ms_fwd = acc["ms_fwd_sweep"] + acc["ms_fwd_recompute"]
     fwd_avg = ms_fwd / max(n_fwd, 1)
     adj_avg = acc["ms_adj"] / max(n_adj, 1)
-    kname = KERNELS[w.kind]
-
-    def launched(base, n, fused):
-        if fused == 0:
-            return base
-        return base + "_x2" if fused == n else base + " + " + base + "_x2"
-
     if ms_fwd >= acc["ms_adj"]:
-        kernel, ms_k, per_pt, units, nl, ns = (launched(kname[0], info.fwd_launches, fused_fwd),
-                                               ms_fwd, fwd_B, fwd_units, n_fwd,
-                                               info.fwd_steps_total)
+        mix = kernel_mix(w.kind, acts, False)
+        ms_k, per_pt, units, nl, ns = ms_fwd, fwd_B, fwd_units, n_fwd, info.fwd_steps_total
     else:
-        kernel, ms_k, per_pt, units, nl, ns = (launched(kname[1], info.adj_launches, fused_adj),
-                                               acc["ms_adj"], adj_B, adj_units, n_adj,
-                                               info.adj_steps)
+        mix = kernel_mix(w.kind, acts, True)
+        ms_k, per_pt, units, nl, ns = acc["ms_adj"], adj_B, adj_units, n_adj, info.adj_steps
+    kernel = max(mix, key=lambda k: mix[k]) if mix else "none"
     alg_total = per_pt * w.npoints * units
     avg_ms = ms_k / max(nl, 1)
     alg_bytes = alg_total / max(nl, 1)
     achieved = alg_total / (ms_k * 1e-3) / 1e9
     traffic = traffic_for(name, kernel, w.kind)
     roofline = {
-        "bound": "hbm", "kernel": kernel, "achieved": round(achieved, 1),
+        "bound": "hbm", "kernel": kernel, "kernel_mix": mix, "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
         "traffic": traffic, "alg_bytes_per_launch": alg_bytes,
         "avg_launch_ms": round(avg_ms, 5), "launches_per_step": nl,

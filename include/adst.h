@@ -114,8 +114,10 @@ typedef enum {
                                 the kind is linear, so store/recompute runs at any shape */
 #define ADST_TRACE 0x2u      /* time the launches with HIP events, synchronise the stream at
                                 the end of the call and fill the ms_* fields of adst_plan_info */
-#define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking);
-                                results are bit-identical either way */
+#define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking:
+                                otherwise up to 6 Jacobi steps or 2 Allen-Cahn forward
+                                steps share one launch); results are bit-identical either
+                                way */
 #define ADST_LIMIT 0x8u      /* a limiter on every step: each new value y (ring included)
                                 becomes lim[0] if y < lim[0], lim[1] if y > lim[1], else stays
                                 y. A data-dependent branch at every point of every step
@@ -157,11 +159,11 @@ typedef struct {
  *   ADST_OP_SEED  loss and seed g_T from x_T held in src (t = T)
  *   ADST_OP_ADJ   g_{t-1} = J_t^T g_t, reading x_{t-1} from src
  *                 (src = ADST_BUF_NONE when the step's adjoint reads no state)
- *   ADST_OP_FWD2  x_t = F(F(state in src)) (steps t-1 and t in one launch, the
- *                 intermediate x_{t-1} kept on chip; emitted only where nothing
- *                 else reads x_{t-1}), written to dst
- *   ADST_OP_ADJ2  g_{t-2} = J_{t-1}^T J_t^T g_t in one launch (state-free
- *                 adjoints only; src = ADST_BUF_NONE)
+ *   ADST_OP_FWD2  x_t = F^n(state in src), n >= 2 (steps t-n+1..t in one launch,
+ *                 the intermediate states kept on chip; emitted only where
+ *                 nothing else reads them), written to dst
+ *   ADST_OP_ADJ2  g_{t-n} = J_{t-n+1}^T ... J_t^T g_t, n >= 2, in one launch
+ *                 (state-free adjoints only; src = ADST_BUF_NONE)
  *   ADST_OP_FWDW  x_t from x_{t-n} in src by n steps of the in-place kind,
  *                 pipelined in one sequence of wavefront launches (tiles of
  *                 several steps share a launch), written to dst
@@ -169,7 +171,7 @@ typedef struct {
  *                 pipelined the same way (its adjoint reads no state)
  * Fused and pipelined actions evaluate every point with the same expression
  * as the single steps, so results are bit-identical. `n` is the number of
- * steps an action covers (1 for FWD/ADJ, 2 for FWD2/ADJ2, 0 for SEED). */
+ * steps an action covers (1 for FWD/ADJ, 0 for SEED). */
 typedef enum {
   ADST_OP_FWD = 0,
   ADST_OP_SEED = 1,
@@ -204,7 +206,7 @@ typedef struct {
   int64_t recompute_steps;  /* fwd_steps_total - T */
   int64_t adj_steps;        /* T */
   int64_t n_actions;        /* length of the action list */
-  int64_t fwd_launches;     /* forward actions (a fused pair or a pipelined run counts once) */
+  int64_t fwd_launches;     /* forward actions (a fused or a pipelined run counts once) */
   int64_t adj_launches;     /* adjoint actions (likewise) */
   int64_t fwd_kernels;      /* forward kernel dispatches the actions enqueue */
   int64_t adj_kernels;      /* adjoint kernel dispatches the actions enqueue */

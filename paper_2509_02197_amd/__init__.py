@@ -234,10 +234,10 @@ def _dims(shape):
     raise ValueError(f"expected a 2-D or 3-D array, got {tuple(shape)}")
 
 
-def forward(kind, x0, coeff=None, steps=1, params=None, stream=None, lim=None):
+def forward(kind, x0, coeff=None, steps=1, params=None, stream=None, lim=None, flags=0):
     """x_T on the device of x0 (torch tensors, row-major)."""
     import torch
-    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, lim=lim)
+    prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags, lim)
     xT = torch.empty_like(x0)
     info = adst_plan(prob, steps, 1 << 62, ADST_SCHED_STORE_ALL)
     ws = torch.empty(max(info.fwd_workspace_bytes, 1), dtype=torch.uint8, device=x0.device)

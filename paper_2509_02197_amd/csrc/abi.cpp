@@ -45,7 +45,7 @@ struct Checked {
   uint64_t state_bytes = 0;
   bool needs_state = false;
   bool trace = false;
-  bool fuse_fwd = false, fuse_adj = false;
+  int32_t fuse_fwd = 1, fuse_adj = 1;  // most steps per launch
   bool in_place = false;  // the Gauss-Seidel kind: pipelined sweeps, adjoint in place
   bool want_dk = false, want_dp = false;
 };
@@ -100,8 +100,8 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   out->want_dp = want_dp;
   out->trace = (p->flags & ADST_TRACE) != 0;
   const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
-  out->fuse_fwd = fuse && has_forward2(p->kind) && !limit;
-  out->fuse_adj = fuse && has_adjoint2(p->kind);
+  out->fuse_fwd = (fuse && !limit) ? max_fused_forward(p->kind) : 1;
+  out->fuse_adj = fuse ? max_fused_adjoint(p->kind) : 1;
   out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
   return ADST_OK;
 }
@@ -190,7 +190,7 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
   info->slot_bytes_peak = uint64_t(plan.slots) * c.state_bytes;
   info->workspace_bytes = L.total;
   info->fwd_workspace_bytes = (plan.steps >= 2 && !c.in_place) ? c.state_bytes : 0;
-  // A fused launch moves its inputs and outputs once for two steps; a
+  // A fused launch moves its inputs and outputs once for its n steps; a
   // pipelined run of the in-place kind is counted as its n steps.
   const uint64_t n = uint64_t(c.npoints);
   uint64_t per_point = sb;
@@ -403,20 +403,19 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
     g_last_error.clear();
     return ADST_OK;
   }
-  // One single step first when the count is odd, then fused pairs where the
-  // kind has them; launches alternate between xT and ws so that the last one
-  // writes xT.
-  const bool pairs = c.fuse_fwd;
-  const int32_t n_launch = pairs ? steps / 2 + steps % 2 : steps;
+  // Launches of up to fuse_fwd steps each, the shorter remainder first;
+  // they alternate between xT and ws so that the last one writes xT.
+  const int32_t d = c.fuse_fwd;
+  const int32_t n_launch = (steps + d - 1) / d;
   const void* cur = x0;
   int32_t done = 0;
   for (int32_t k = 0; k < n_launch; ++k) {
     void* dst = ((n_launch - 1 - k) % 2 == 0) ? xT : ws;
-    const bool two = pairs && !(k == 0 && steps % 2 == 1);
-    e = two ? launch_forward2(c.shape, cur, coeff, dst, stream)
-            : launch_forward(c.shape, cur, coeff, dst, stream);
+    const int32_t n = (k == 0 && steps % d != 0) ? steps % d : d;
+    e = n >= 2 ? launch_forward_n(c.shape, cur, coeff, dst, n, stream)
+               : launch_forward(c.shape, cur, coeff, dst, stream);
     if (e != hipSuccess) return hip_fail(e, "forward step");
-    done += two ? 2 : 1;
+    done += n;
     cur = dst;
   }
   if (done != steps) return fail(ADST_ERR_ARG, "internal: forward launch count");
@@ -504,7 +503,7 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
         e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
         break;
       case ADST_OP_FWD2:
-        e = launch_forward2(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+        e = launch_forward_n(c.shape, buffer(a.src), coeff, buffer(a.dst), a.n, stream);
         break;
       case ADST_OP_SEED: {
         const void* xsrc = buffer(a.src);
@@ -537,7 +536,7 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
         break;
       }
       case ADST_OP_ADJ2:
-        e = launch_adjoint2(c.shape, gcur, gnext, stream);
+        e = launch_adjoint_n(c.shape, gcur, gnext, a.n, stream);
         std::swap(gcur, gnext);
         break;
       default:

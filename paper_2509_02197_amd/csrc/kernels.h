@@ -22,17 +22,19 @@ struct StepShape {
 hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void* y,
                           hipStream_t stream);
 
-// Kinds with a fused two-step kernel (temporal blocking of depth 2).
-bool has_forward2(int32_t kind);
-bool has_adjoint2(int32_t kind);  // state-free adjoints only
+// Temporal blocking: the most steps one launch may take (1 = none). The
+// fused adjoint is for state-free adjoints only.
+int32_t max_fused_forward(int32_t kind);
+int32_t max_fused_adjoint(int32_t kind);
 
-// x_t = F(F(x_{t-2})): two forward steps, the intermediate kept on chip.
-hipError_t launch_forward2(const StepShape& s, const void* x, const void* K, void* y,
-                           hipStream_t stream);
+// x_t = F^n(x_{t-n}) in one launch (2 <= n <= max_fused_forward), the
+// intermediate states kept on chip.
+hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, void* y, int32_t n,
+                            hipStream_t stream);
 
-// g_{t-2} = J_{t-1}^T J_t^T g_t for a state-free adjoint.
-hipError_t launch_adjoint2(const StepShape& s, const void* g_next, void* g_prev,
-                           hipStream_t stream);
+// g_{t-n} = J_{t-n+1}^T ... J_t^T g_t in one launch, state-free adjoints.
+hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev, int32_t n,
+                            hipStream_t stream);
 
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
 // reads no state and dK is not asked for). dK (nullable) is accumulated:

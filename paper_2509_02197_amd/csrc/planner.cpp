@@ -55,8 +55,9 @@ int64_t best_split(int64_t l, int64_t c) {
 
 class Builder {
  public:
-  Builder(int32_t T, bool needs_state, bool fuse_fwd, bool fuse_adj)
-      : T_(T), needs_state_(needs_state), fuse_fwd_(fuse_fwd), fuse_adj_(fuse_adj) {}
+  Builder(int32_t T, bool needs_state, int32_t fuse_fwd, int32_t fuse_adj)
+      : T_(T), needs_state_(needs_state), fuse_fwd_(std::max(fuse_fwd, 1)),
+        fuse_adj_(std::max(fuse_adj, 1)) {}
 
   std::vector<adst_action> acts;
   int32_t slots_used = 0;
@@ -77,10 +78,10 @@ class Builder {
     ++nfwd;
     ++fwd_launches;
   }
-  // Steps t-1 and t in one launch; x_{t-1} is never materialised.
-  void fwd2(int32_t t, int32_t src, int32_t dst) {
-    acts.push_back({ADST_OP_FWD2, t, src, dst, 2});
-    nfwd += 2;
+  // Steps t-n+1..t in one launch; x_{t-n+1}..x_{t-1} are never materialised.
+  void fwdn(int32_t t, int32_t n, int32_t src, int32_t dst) {
+    acts.push_back({ADST_OP_FWD2, t, src, dst, n});
+    nfwd += n;
     ++fwd_launches;
   }
 
@@ -91,16 +92,16 @@ class Builder {
   // From buffer b holding x_i, compute x_{i+1}..x_j through the work buffers;
   // the last step writes final_dst instead when one is given. Returns the
   // buffer holding x_j. The intermediate states are read by nothing else, so
-  // with fusion on they are computed two steps per launch.
+  // with fusion on they are computed up to fuse_fwd_ steps per launch.
   int32_t advance(int32_t b, int32_t i, int32_t j, int32_t final_dst) {
     int32_t cur = b;
     int32_t t = i;
     while (t < j) {
-      const int32_t n = (fuse_fwd_ && j - t >= 2) ? 2 : 1;
+      const int32_t n = std::min(fuse_fwd_, j - t);
       t += n;
       const int32_t dst = (t == j && final_dst != ADST_BUF_NONE) ? final_dst : other_work(cur);
-      if (n == 2)
-        fwd2(t, cur, dst);
+      if (n >= 2)
+        fwdn(t, n, cur, dst);
       else
         fwd(t, cur, dst);
       cur = dst;
@@ -209,15 +210,16 @@ class Builder {
   }
 
   // No adjoint step reads state: one sweep straight to x_T, the seed, then
-  // the adjoint steps, two per launch when fusion is on.
+  // the adjoint steps, up to fuse_adj_ per launch.
   void elided() {
     advance(ADST_BUF_X0, 0, T_, ADST_BUF_XT);
     seed();
     int32_t t = T_;
     while (t >= 1) {
-      if (fuse_adj_ && t >= 2) {
-        acts.push_back({ADST_OP_ADJ2, t, ADST_BUF_NONE, ADST_BUF_NONE, 2});
-        t -= 2;
+      const int32_t n = std::min(fuse_adj_, t);
+      if (n >= 2) {
+        acts.push_back({ADST_OP_ADJ2, t, ADST_BUF_NONE, ADST_BUF_NONE, n});
+        t -= n;
       } else {
         acts.push_back({ADST_OP_ADJ, t, ADST_BUF_NONE, ADST_BUF_NONE, 1});
         t -= 1;
@@ -243,7 +245,7 @@ class Builder {
  private:
   int32_t T_;
   bool needs_state_;
-  bool fuse_fwd_, fuse_adj_;
+  int32_t fuse_fwd_, fuse_adj_;  // most steps per launch (1 = no fusion)
   bool seeded_ = false;
   std::vector<int32_t> free_;
 };
@@ -266,7 +268,7 @@ constexpr int64_t kMaxActions = int64_t(1) << 24;
 }  // namespace
 
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       bool fuse_fwd, bool fuse_adj, bool pipelined, Plan* out,
+                       int32_t fuse_fwd, int32_t fuse_adj, bool pipelined, Plan* out,
                        std::string* err) {
   if (steps < 0) {
     *err = "steps must be >= 0";
@@ -296,7 +298,7 @@ adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool n
     return ADST_ERR_UNSUPPORTED;
   }
 
-  Builder b(steps, needs_state, fuse_fwd, fuse_adj && !needs_state);
+  Builder b(steps, needs_state, fuse_fwd, needs_state ? 1 : fuse_adj);
   if (steps == 0) {
     b.zero_steps();
   } else if (!needs_state && pipelined) {

@@ -16,9 +16,9 @@ struct Plan {
   int32_t sched = ADST_SCHED_STORE_ALL;  // resolved
   int32_t slots = 0;                     // slots the actions use (x0 excluded)
   bool needs_state = false;
-  int64_t fwd_total = 0;     // forward steps (a fused pair counts 2)
+  int64_t fwd_total = 0;     // forward steps (a fused launch counts its n)
   int64_t adj_total = 0;     // adjoint steps
-  int64_t fwd_launches = 0;  // forward actions (a fused pair counts 1)
+  int64_t fwd_launches = 0;  // forward actions (a fused launch counts 1)
   int64_t adj_launches = 0;  // adjoint actions
   std::vector<adst_action> acts;
 };
@@ -32,14 +32,15 @@ int64_t binomial_cost(int64_t l, int64_t c);
 inline int64_t store_all_slots(int64_t T) { return T > 2 ? T - 2 : 0; }
 
 // Build the action list. slots_avail is the number of checkpoint slots the
-// budget allows (x0 excluded). sched may be AUTO. fuse_fwd lets two forward
-// steps whose intermediate state nothing reads share one launch (FWD2);
-// fuse_adj does the same for state-free adjoint steps (ADJ2). pipelined (the
-// in-place kind) turns a state-free plan into one pipelined forward run and
-// one pipelined reverse run (FWDW, ADJW). Returns ADST_OK or ADST_ERR_BUDGET
-// / ADST_ERR_ARG / ADST_ERR_UNSUPPORTED with *err filled.
+// budget allows (x0 excluded). sched may be AUTO. fuse_fwd lets up to that
+// many forward steps whose intermediate states nothing reads share one launch
+// (FWD2 with n steps; 1 = no fusion); fuse_adj does the same for state-free
+// adjoint steps (ADJ2). pipelined (the in-place kind) turns a state-free
+// plan into one pipelined forward run and one pipelined reverse run (FWDW,
+// ADJW). Returns ADST_OK or ADST_ERR_BUDGET / ADST_ERR_ARG /
+// ADST_ERR_UNSUPPORTED with *err filled.
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       bool fuse_fwd, bool fuse_adj, bool pipelined, Plan* out,
+                       int32_t fuse_fwd, int32_t fuse_adj, bool pipelined, Plan* out,
                        std::string* err);
 
 }  // namespace adst

@@ -9,10 +9,10 @@ checks what makes a plan correct, independently of how it was built:
     x_{t-1} at that moment when the step's adjoint needs state;
   * the x_T buffer is not read again after the seed (it may alias g_T);
   * checkpoint slots used stay within the allowed count;
-  * a fused forward pair (FWD2, steps t-1 and t) reads x_{t-2} and leaves
-    x_{t-1} nowhere, so any later use of x_{t-1} fails the checks above;
-    a fused adjoint pair (ADJ2, steps t and t-1) only appears for
-    state-free adjoints;
+  * a fused forward run (FWD2, steps t-n+1..t, n >= 2) reads x_{t-n} and
+    leaves x_{t-n+1}..x_{t-1} nowhere, so any later use of them fails the
+    checks above; a fused adjoint run (ADJ2, steps t..t-n+1) only appears
+    for state-free adjoints;
   * a pipelined forward run (FWDW, steps t-n+1..t) reads x_{t-n} and leaves
     only x_t behind; a pipelined reverse run (ADJW, steps t..t-n+1) is
     state-free;
@@ -32,8 +32,10 @@ def replay(actions, T, needs_state, max_slots):
     slots = set()
     for k, (op, t, src, dst, n) in enumerate(actions):
         if op in (FWD, FWD2, FWDW):
-            if op != FWDW:
-                assert n == (1 if op == FWD else 2), f"action {k}: step count {n}"
+            if op == FWD:
+                assert n == 1, f"action {k}: step count {n}"
+            elif op == FWD2:
+                assert n >= 2, f"action {k}: step count {n}"
             assert n >= 1
             assert not (seeded and src == XT), f"action {k}: reads x_T buffer after the seed"
             assert holds.get(src) == t - n, f"action {k}: FWD {t} reads buffer {src} holding {holds.get(src)}"
@@ -63,10 +65,10 @@ def replay(actions, T, needs_state, max_slots):
                 assert src == NONE
             next_adj -= 1
         elif op == ADJ2:
-            assert n == 2
+            assert n >= 2
             assert seeded and not needs_state and src == NONE
-            assert t == next_adj and t >= 2, f"fused adjoint {t} out of order"
-            next_adj -= 2
+            assert t == next_adj and t >= n, f"fused adjoint {t} out of order"
+            next_adj -= n
         elif op == ADJW:
             assert seeded and not needs_state and src == NONE
             assert t == next_adj and 1 <= n <= t, f"pipelined adjoint {t}/{n} out of order"

@@ -237,14 +237,25 @@ def test_fused_plans_replay_with_the_same_step_counts(kind, flags, sched, slots)
         assert info.fwd_steps_total == infon.fwd_steps_total == nf
         assert info.fwd_launches <= infon.fwd_launches == infon.fwd_steps_total
         assert info.adj_launches <= infon.adj_launches == T
+        depth = 6 if kind == adst.ADST_JACOBI2D5 else 2 if kind == AC else 1
+        assert all(a[4] <= depth for a in fused if a[0] == adst.ADST_OP_FWD2)
+        assert all(a[4] <= depth for a in fused if a[0] == adst.ADST_OP_ADJ2)
 
 
 def test_elided_jacobi_fuses_everything():
+    """Jacobi steps go up to six per launch, forward and adjoint; the
+    remainder takes the last forward launch and the last adjoint launch."""
     p = prob(adst.ADST_JACOBI2D5, (6, 5, 1))
     info = adst.adst_plan(p, 100, 0, adst.ADST_SCHED_AUTO)
-    assert info.fwd_launches == 50 and info.adj_launches == 50
+    assert info.fwd_launches == 17 and info.adj_launches == 17
+    acts = adst.adst_plan_actions(p, 100, 0, adst.ADST_SCHED_AUTO)
+    assert [a[4] for a in acts if a[0] == adst.ADST_OP_FWD2] == [6] * 16 + [4]
+    assert [a[4] for a in acts if a[0] == adst.ADST_OP_ADJ2] == [6] * 16 + [4]
     info = adst.adst_plan(p, 7, 0, adst.ADST_SCHED_AUTO)
-    assert info.fwd_launches == 4 and info.adj_launches == 4
+    assert info.fwd_launches == 2 and info.adj_launches == 2
+    acts = adst.adst_plan_actions(p, 7, 0, adst.ADST_SCHED_AUTO)
+    assert [a[0] for a in acts] == [adst.ADST_OP_FWD2, adst.ADST_OP_FWD, adst.ADST_OP_SEED,
+                                    adst.ADST_OP_ADJ2, adst.ADST_OP_ADJ]
     # Allen-Cahn fuses forward chains; its adjoint reads state, so it does not
     info = adst.adst_plan(prob(), 30, budget_for(4), adst.ADST_SCHED_BINOMIAL)
     assert info.fwd_launches < info.fwd_steps_total and info.adj_launches == 30
