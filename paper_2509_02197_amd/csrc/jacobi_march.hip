@@ -1,0 +1,310 @@
+// Temporal blocking of the Jacobi kind on gfx950: n = 3..kJacMaxFuse steps,
+// forward or gather adjoint, in one launch with the intermediate time levels
+// in registers.
+//
+// The step (adst.h, ADST_JACOBI2D5): interior points take
+//     x'[c] = w * ((((x[c] + x[W]) + x[E]) + x[S]) + x[N]),
+// the ring is copied; the adjoint is its transpose in gather form,
+//     interior m: g'[m] = w * (g[m] + sum of gi over the neighbours of m)
+//     ring m:     g'[m] = g[m] + w * (sum of gi over the neighbours of m)
+// with gi = g on interior points and 0 on the ring, the neighbours summed in
+// the order W, E, S, N. A point two or more cells from the edge sees only
+// interior neighbours, so there the adjoint is the same plain average as the
+// forward. Both are linear in the carried state, so their adjoints read no
+// forward state (Sec. IV) and n steps of either compose without any stored
+// value in between.
+//
+// Layout. A workgroup is one wave of 64 lanes owning a strip of 64 * V
+// columns (V elements, 16 bytes, per lane) and a chunk of rows. It marches
+// along the rows carrying the last three rows of each of the n time levels:
+// when input row q arrives, level k evaluates row q - k from level k - 1's
+// rows q - k - 1, q - k, q - k + 1. East/west neighbours of a lane's first
+// and last element come from the adjacent lanes by DPP whole-wave shifts.
+// Each level is valid on one column fewer at each side of the strip and one
+// row fewer at each end of the chunk, so strips overlap by H >= n columns
+// (whole vectors) and a chunk reads n rows beyond each of its ends. Every
+// point evaluates the single-step expressions above, so any split of the
+// steps into launches gives the same bits.
+//
+// Memory. Each input row is loaded kAhead rows before it enters the
+// pipeline, into registers that nothing touches until then (its validity
+// mask is applied on entry), so the loads stay in flight behind the
+// arithmetic. Rows beyond the ones a chunk needs are never fetched from new
+// addresses. Odd chunks march downward, so the rows two neighbouring chunks
+// share are read by both at about the same time and the second read hits
+// the L2 cache they share (their blocks go to the same XCD).
+//
+// Boundary. Blocks of kUnroll consecutive input rows whose evaluated rows all
+// lie two or more cells from the top and bottom edge, in a strip two or more
+// cells from the side edges, take the plain average; the others evaluate the
+// ring logic as selects on per-lane column flags. The first and last strip
+// (the side edges) take short chunks, and every XCD gets an equal share of
+// them, so their slower blocks do not become the launch's tail.
+
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "adst.h"
+#include "kernels.h"
+
+namespace adst {
+namespace {
+
+constexpr int kLanes = 64;
+constexpr int kRows = 48;      // rows per chunk of an interior strip
+constexpr int kEdgeRows = 8;   // rows per chunk of the first and last strip
+constexpr int kAhead = 6;      // input rows loaded ahead of the pipeline
+constexpr int kUnroll = 6;     // input rows per straight-line block
+constexpr int kXcds = 8;       // workgroup i runs on XCD i mod 8
+static_assert(kUnroll % kAhead == 0 && kUnroll % 3 == 0, "register slots must stay static");
+
+// Whole-wave lane shifts: lane i receives lane i-1's value (lane 0: 0) or
+// lane i+1's (lane 63: 0).
+__device__ inline uint32_t shr1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x138, 0xf, 0xf, true);
+}
+__device__ inline uint32_t shl1(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x130, 0xf, 0xf, true);
+}
+__device__ inline float from_prev(float v) { return __uint_as_float(shr1(__float_as_uint(v))); }
+__device__ inline float from_next(float v) { return __uint_as_float(shl1(__float_as_uint(v))); }
+__device__ inline double from_prev(double v) {
+  const uint64_t a = __double_as_longlong(v);
+  return __longlong_as_double(
+      (long long)(((uint64_t)shr1((uint32_t)(a >> 32)) << 32) | shr1((uint32_t)a)));
+}
+__device__ inline double from_next(double v) {
+  const uint64_t a = __double_as_longlong(v);
+  return __longlong_as_double(
+      (long long)(((uint64_t)shl1((uint32_t)(a >> 32)) << 32) | shl1((uint32_t)a)));
+}
+
+template <class R, int K>
+struct Geom {
+  static constexpr int V = 16 / sizeof(R);
+  static constexpr int H = ((K + V - 1) / V) * V;  // column overlap, whole vectors
+  static constexpr int OW = kLanes * V - 2 * H;    // output columns per strip
+};
+
+// Work list: the chunks of the first and last strip (E of them) and of the
+// interior strips (I). XCD x takes edge chunks [x*pe, (x+1)*pe) and interior
+// chunks [x*pi, (x+1)*pi), edge chunks first.
+struct MarchGrid {
+  int ns, nedge, ce, ci, pe, pi;
+};
+
+template <class R, int K, bool ADJ, bool VEC>
+__global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, R* __restrict__ y,
+                                                       int nx, int ny, MarchGrid g, R w) {
+  using G = Geom<R, K>;
+  constexpr int V = G::V, H = G::H, OW = G::OW, P = kAhead, U = kUnroll;
+  typedef R vec_t __attribute__((ext_vector_type(V)));
+  const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
+  int strip, chunk, rpc;
+  if (slot < g.pe) {
+    const int t = xcd * g.pe + slot;
+    if (t >= g.nedge * g.ce) return;
+    strip = (t / g.ce == 0) ? 0 : g.ns - 1;
+    chunk = t % g.ce;
+    rpc = kEdgeRows;
+  } else {
+    const int t = xcd * g.pi + (slot - g.pe);
+    if (t >= (g.ns - g.nedge) * g.ci) return;
+    strip = 1 + t / g.ci;
+    chunk = t % g.ci;
+    rpc = kRows;
+  }
+  const int lane = threadIdx.x;
+  const int s0 = strip * OW;
+  const int c0 = s0 - H + lane * V;  // first column of this lane
+  const int r0 = chunk * rpc, r1 = min(r0 + rpc, ny);
+  const int nit = (r1 - r0) + 2 * K;  // input rows through the pipeline
+  const int lo_need = max(r0 - K, 0), hi_need = min(r1 + K - 1, ny - 1);
+
+  // Per-lane column facts of the V columns.
+  auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
+  bool cok[V], cI[V], cW[V], cE[V], cF[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    const int c = c0 + e;
+    cok[e] = c >= 0 && c < nx;
+    cI[e] = cin(c);
+    cW[e] = cin(c - 1);
+    cE[e] = cin(c + 1);
+    cF[e] = c >= 2 && c <= nx - 3;
+  }
+  const bool strip_in = s0 - H >= 2 && s0 - H + kLanes * V <= nx - 2;
+  const bool st_lane = lane * V >= H && lane * V < H + OW;
+
+  // Raw load of input row `row` (clamped to the rows the chunk needs, and
+  // to the grid, so every address is in bounds); masked on entry.
+  auto load = [&](int row, R* out) {
+    const int rr = min(max(row, lo_need), hi_need);
+    const R* src = x + (int64_t)rr * nx;
+    if constexpr (VEC) {
+      const int cc = min(max(c0, 0), nx - V);
+      const vec_t t = *reinterpret_cast<const vec_t*>(src + cc);
+#pragma unroll
+      for (int e = 0; e < V; ++e) out[e] = t[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) out[e] = src[min(max(c0 + e, 0), nx - 1)];
+    }
+  };
+
+  auto march = [&](auto dir_t) {
+    constexpr int DIR = decltype(dir_t)::value;  // +1 upward, -1 downward
+    const int ifirst = DIR > 0 ? r0 - K : r1 - 1 + K;  // row of input index 0
+    // Level k's row of pipeline index p (row ifirst + DIR*p) sits in slot p mod 3.
+    R lv[K][3][V];
+    R pf[P][V];
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int s3 = 0; s3 < 3; ++s3)
+#pragma unroll
+        for (int e = 0; e < V; ++e) lv[k][s3][e] = R(0);
+#pragma unroll
+    for (int u = 0; u < P; ++u) load(ifirst + DIR * u, pf[u]);
+
+    auto block = [&](int base, auto fast_t) {
+      constexpr bool FAST = decltype(fast_t)::value;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int rr = base + u;
+        {  // input row rr enters level 0; the row P ahead is requested
+          const int row = ifirst + DIR * rr;
+          const bool rok = row >= 0 && row < ny;
+#pragma unroll
+          for (int e = 0; e < V; ++e) lv[0][u % 3][e] = (rok && cok[e]) ? pf[u % P][e] : R(0);
+          load(row + DIR * P, pf[u % P]);
+        }
+#pragma unroll
+        for (int k = 1; k <= K; ++k) {
+          const int j = ifirst + DIR * (rr - k);  // row level k evaluates now
+          constexpr int off = 3 * (K + 2);
+          const int sOld = (u - k - 1 + off) % 3, sc = (u - k + off) % 3,
+                    sNew = (u - k + 1 + off) % 3;
+          const R* a = lv[k - 1][sc];
+          const R* S = lv[k - 1][DIR > 0 ? sOld : sNew];
+          const R* N = lv[k - 1][DIR > 0 ? sNew : sOld];
+          const R wl = from_prev(a[V - 1]), er = from_next(a[0]);
+          R o[V];
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
+            const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
+            const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
+            if constexpr (FAST) {
+              o[e] = f;
+            } else {
+              const bool rj = j >= 1 && j <= ny - 2, rS = j >= 2 && j <= ny - 1,
+                         rN = j >= 0 && j <= ny - 3, rF = j >= 2 && j <= ny - 3;
+              if constexpr (!ADJ) {
+                o[e] = (cI[e] && rj) ? f : a[e];
+              } else {
+                R sum = (cW[e] && rj) ? Wn : R(0);
+                sum += (cE[e] && rj) ? En : R(0);
+                sum += (cI[e] && rS) ? S[e] : R(0);
+                sum += (cI[e] && rN) ? N[e] : R(0);
+                const R gr = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
+                o[e] = (cF[e] && rF) ? f : gr;
+              }
+            }
+          }
+          if (k < K) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) lv[k][sc][e] = o[e];
+          } else if (j >= r0 && j < r1 && st_lane) {
+            R* dst = y + (int64_t)j * nx;
+            if constexpr (VEC) {
+              if (c0 + V <= nx) {
+                vec_t t;
+#pragma unroll
+                for (int e = 0; e < V; ++e) t[e] = o[e];
+                *reinterpret_cast<vec_t*>(dst + c0) = t;
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < V; ++e)
+                if (c0 + e < nx) dst[c0 + e] = o[e];
+            }
+          }
+        }
+      }
+    };
+
+    // A block of U input rows evaluates rows ifirst + DIR*[base - K, base + U - 1];
+    // blocks [fa, fb) have all of them in [2, ny - 3].
+    int fa, fb;
+    if (DIR > 0) {
+      fa = 2 + K - ifirst;
+      fb = ny - 1 - ifirst - U;
+    } else {
+      fa = ifirst + K - (ny - 3);
+      fb = ifirst - U;
+    }
+    fa = ((max(fa, 0) + U - 1) / U) * U;
+    if (!strip_in) fa = fb = 0;
+    int base = 0;
+    for (; base < nit && base < fa; base += U) block(base, std::false_type{});
+    for (; base < nit && base < fb; base += U) block(base, std::true_type{});
+    for (; base < nit; base += U) block(base, std::false_type{});
+  };
+  if (chunk & 1)
+    march(std::integral_constant<int, -1>{});
+  else
+    march(std::integral_constant<int, 1>{});
+}
+
+template <class R, int K, bool ADJ>
+hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
+  using G = Geom<R, K>;
+  MarchGrid g;
+  g.ns = (s.nx + G::OW - 1) / G::OW;
+  g.nedge = g.ns >= 2 ? 2 : 1;
+  g.ce = (s.ny + kEdgeRows - 1) / kEdgeRows;
+  g.ci = (s.ny + kRows - 1) / kRows;
+  const int64_t E = int64_t(g.nedge) * g.ce, I = int64_t(g.ns - g.nedge) * g.ci;
+  g.pe = (int)((E + kXcds - 1) / kXcds);
+  g.pi = (int)((I + kXcds - 1) / kXcds);
+  const int64_t blocks = int64_t(kXcds) * (g.pe + g.pi);
+  if (blocks <= 0 || blocks > INT32_MAX) return hipErrorInvalidValue;
+  const bool vec = s.nx % G::V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(y) & 15u) == 0;
+  if (vec)
+    jacobi_march<R, K, ADJ, true><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
+        x, y, s.nx, s.ny, g, R(s.p0));
+  else
+    jacobi_march<R, K, ADJ, false><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
+        x, y, s.nx, s.ny, g, R(s.p0));
+  return hipGetLastError();
+}
+
+template <class R, bool ADJ>
+hipError_t march_n(const StepShape& s, const void* xv, void* yv, int n, hipStream_t st) {
+  const R* x = static_cast<const R*>(xv);
+  R* y = static_cast<R*>(yv);
+  switch (n) {
+    case 3: return march_launch<R, 3, ADJ>(s, x, y, st);
+    case 4: return march_launch<R, 4, ADJ>(s, x, y, st);
+    case 5: return march_launch<R, 5, ADJ>(s, x, y, st);
+    case 6: return march_launch<R, 6, ADJ>(s, x, y, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32_t n, bool adjoint,
+                               hipStream_t stream) {
+  if (s.kind != ADST_JACOBI2D5 || n < 3 || n > kJacMaxFuse) return hipErrorInvalidValue;
+  if (s.dtype == ADST_F64)
+    return adjoint ? march_n<double, true>(s, x, y, n, stream)
+                   : march_n<double, false>(s, x, y, n, stream);
+  return adjoint ? march_n<float, true>(s, x, y, n, stream)
+                 : march_n<float, false>(s, x, y, n, stream);
+}
+
+}  // namespace adst

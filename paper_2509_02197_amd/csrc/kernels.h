@@ -24,6 +24,7 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 
 // Temporal blocking: the most steps one launch may take (1 = none). The
 // fused adjoint is for state-free adjoints only.
+constexpr int32_t kJacMaxFuse = 6;
 int32_t max_fused_forward(int32_t kind);
 int32_t max_fused_adjoint(int32_t kind);
 
@@ -35,6 +36,11 @@ hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, vo
 // g_{t-n} = J_{t-n+1}^T ... J_t^T g_t in one launch, state-free adjoints.
 hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev, int32_t n,
                             hipStream_t stream);
+
+// Jacobi only, 3 <= n <= kJacMaxFuse: n forward steps (adjoint = false) or
+// n adjoint steps in one launch (jacobi_march.hip).
+hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32_t n, bool adjoint,
+                               hipStream_t stream);
 
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
 // reads no state and dK is not asked for). dK (nullable) is accumulated:

@@ -284,186 +284,6 @@ __device__ inline void jacobi_tile_x2(const R* __restrict__ x, R* __restrict__ y
   }
 }
 
-// ------------------------------------ Jacobi, up to kJacMaxFuse steps per launch
-// Temporal blocking without LDS: one wave owns a strip of 64*V columns (V = 2
-// doubles or 4 floats per lane, one 16-byte vector) and marches down a chunk
-// of rows, carrying K time levels in a register pipeline. At input row r the
-// wave computes level k at row r-k from level k-1's rows r-k-1..r-k+1, so
-// every point is read once from memory and written once after K steps. The
-// east/west neighbours of a lane's edge elements come from the adjacent
-// lanes by DPP whole-wave shifts; each level loses one valid column at each
-// side of the strip and one row at each end of the chunk, so strips overlap
-// by H >= K columns and chunks read K extra rows above and below. Every
-// point is evaluated with the single-step kernels' expressions (the plain
-// average where all neighbours are interior; the ring logic as selects on
-// per-lane column flags and wave-uniform row flags), so any split of the
-// steps into launches gives the same bits.
-constexpr int kJacMaxFuse = 6;
-constexpr int kJmRows = 48;      // rows per chunk of an interior strip
-constexpr int kJmEdgeRows = 12;  // rows per chunk of the first and last strip, whose
-                                 // boundary path costs about three times as much
-constexpr int kJmAhead = 6;      // input rows in flight ahead of the pipeline
-
-__device__ inline uint32_t jm_shr1(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x138, 0xf, 0xf, false);
-}
-__device__ inline uint32_t jm_shl1(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x130, 0xf, 0xf, false);
-}
-// lane i receives lane i-1's value (lane 0: 0) / lane i+1's (lane 63: 0)
-__device__ inline float jm_from_prev(float v) { return __uint_as_float(jm_shr1(__float_as_uint(v))); }
-__device__ inline float jm_from_next(float v) { return __uint_as_float(jm_shl1(__float_as_uint(v))); }
-__device__ inline double jm_from_prev(double v) {
-  const uint64_t a = __double_as_longlong(v);
-  return __longlong_as_double(
-      (long long)(((uint64_t)jm_shr1((uint32_t)(a >> 32)) << 32) | jm_shr1((uint32_t)a)));
-}
-__device__ inline double jm_from_next(double v) {
-  const uint64_t a = __double_as_longlong(v);
-  return __longlong_as_double(
-      (long long)(((uint64_t)jm_shl1((uint32_t)(a >> 32)) << 32) | jm_shl1((uint32_t)a)));
-}
-
-template <class R, int K>
-struct JmGeom {
-  static constexpr int V = 16 / sizeof(R);
-  static constexpr int H = ((K + V - 1) / V) * V;  // column overlap, whole vectors
-  static constexpr int OW = kBX * V - 2 * H;       // output columns per strip
-};
-
-template <class R, int K, bool ADJ>
-__global__ __launch_bounds__(kBX) void jacobi_march(const R* __restrict__ x, R* __restrict__ y,
-                                                    int nx, int ny, int nstrips, int nedge,
-                                                    int ce, int ci, int nblocks, int vec, R w) {
-  using G = JmGeom<R, K>;
-  constexpr int V = G::V, H = G::H, OW = G::OW, P = kJmAhead;
-  static_assert(P % 3 == 0, "the unrolled row loop keeps level slots static");
-  typedef R vec_t __attribute__((ext_vector_type(V)));
-  int b = xcd_tile(nblocks);
-  if (b >= nblocks) return;
-  // blocks of the edge strips come first (chunks of kJmEdgeRows), then the
-  // interior strips (chunks of kJmRows); chunks of one strip are consecutive
-  int strip, chunk, rpc;
-  if (b < nedge * ce) {
-    strip = (b / ce == 0) ? 0 : nstrips - 1;
-    chunk = b % ce;
-    rpc = kJmEdgeRows;
-  } else {
-    b -= nedge * ce;
-    strip = 1 + b / ci;
-    chunk = b % ci;
-    rpc = kJmRows;
-  }
-  const int lane = threadIdx.x;
-  const int s0 = strip * OW;
-  const int c0 = s0 - H + lane * V;
-  const int r0 = chunk * rpc, r1 = min(r0 + rpc, ny);
-  const int ifirst = r0 - K;
-  const int nit = (r1 - ifirst) + K;
-  auto load = [&](int row, R* out) {
-    const bool rok = row >= 0 && row < ny;
-    const int rr = min(max(row, 0), ny - 1);
-    if (vec) {
-      const bool ok = rok && c0 >= 0 && c0 + V <= nx;
-      const int cc = min(max(c0, 0), nx - V);
-      const vec_t t = *reinterpret_cast<const vec_t*>(x + (int64_t)rr * nx + cc);
-#pragma unroll
-      for (int e = 0; e < V; ++e) out[e] = ok ? t[e] : R(0);
-    } else {
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        const int c = c0 + e;
-        const R v = x[(int64_t)rr * nx + min(max(c, 0), nx - 1)];
-        out[e] = (rok && c >= 0 && c < nx) ? v : R(0);
-      }
-    }
-  };
-  auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
-  bool cI[V], cW[V], cE[V], cF[V];  // per-lane column flags of the V columns
-#pragma unroll
-  for (int e = 0; e < V; ++e) {
-    const int c = c0 + e;
-    cI[e] = cin(c);
-    cW[e] = cin(c - 1);
-    cE[e] = cin(c + 1);
-    cF[e] = c >= 2 && c <= nx - 3;
-  }
-  const bool strip_in = s0 - H >= 2 && s0 - H + kBX * V <= nx - 2;
-  const bool st_lane = lane * V >= H && lane * V < H + OW;  // owns output columns
-  R lv[K][3][V];  // levels 0..K-1, the last three rows of each (slot = row mod 3)
-  R pf[P][V];     // input rows loaded ahead
-#pragma unroll
-  for (int k = 0; k < K; ++k)
-#pragma unroll
-    for (int s3 = 0; s3 < 3; ++s3)
-#pragma unroll
-      for (int e = 0; e < V; ++e) lv[k][s3][e] = R(0);
-#pragma unroll
-  for (int u = 0; u < P; ++u) load(ifirst + u, pf[u]);
-  for (int base = 0; base < nit; base += P) {
-#pragma unroll
-    for (int u = 0; u < P; ++u) {
-      const int rr = base + u;
-#pragma unroll
-      for (int e = 0; e < V; ++e) lv[0][u % 3][e] = pf[u][e];
-      load(ifirst + rr + P, pf[u]);
-#pragma unroll
-      for (int k = 1; k <= K; ++k) {
-        const int j = ifirst + rr - k;  // row of level k evaluated now
-        constexpr int off = 3 * (K + 1);
-        const int sm = (u - k - 1 + off) % 3, sc = (u - k + off) % 3, sp = (u - k + 1 + off) % 3;
-        const R* a = lv[k - 1][sc];
-        const R* S = lv[k - 1][sm];
-        const R* N = lv[k - 1][sp];
-        R Wn[V], En[V], f[V], o[V];
-        const R wl = jm_from_prev(a[V - 1]), er = jm_from_next(a[0]);
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          Wn[e] = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
-          En[e] = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
-          f[e] = w * ((((a[e] + Wn[e]) + En[e]) + S[e]) + N[e]);
-        }
-        if (strip_in && j >= 2 && j <= ny - 3) {  // wave-uniform: plain average
-#pragma unroll
-          for (int e = 0; e < V; ++e) o[e] = f[e];
-        } else {
-          const bool rj = j >= 1 && j <= ny - 2, rS = j >= 2 && j <= ny - 1,
-                     rN = j >= 0 && j <= ny - 3, rF = j >= 2 && j <= ny - 3;
-#pragma unroll
-          for (int e = 0; e < V; ++e) {
-            if (!ADJ) {
-              o[e] = (cI[e] && rj) ? f[e] : a[e];
-            } else {  // the gather adjoint of the single-step kernel, as selects
-              R sum = (cW[e] && rj) ? Wn[e] : R(0);
-              sum += (cE[e] && rj) ? En[e] : R(0);
-              sum += (cI[e] && rS) ? S[e] : R(0);
-              sum += (cI[e] && rN) ? N[e] : R(0);
-              const R g = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
-              o[e] = (cF[e] && rF) ? f[e] : g;
-            }
-          }
-        }
-        if (k < K) {
-#pragma unroll
-          for (int e = 0; e < V; ++e) lv[k][sc][e] = o[e];
-        } else if (j >= r0 && j < r1 && st_lane) {
-          R* dst = y + (int64_t)j * nx;
-          if (vec && c0 + V <= nx) {
-            vec_t t;
-#pragma unroll
-            for (int e = 0; e < V; ++e) t[e] = o[e];
-            *reinterpret_cast<vec_t*>(dst + c0) = t;
-          } else {
-#pragma unroll
-            for (int e = 0; e < V; ++e)
-              if (c0 + e < nx) dst[c0 + e] = o[e];
-          }
-        }
-      }
-    }
-  }
-}
-
 template <class R, bool LIM>
 __global__ __launch_bounds__(kJacTW) void fwd_jacobi2d5(const R* __restrict__ x,
                                                         R* __restrict__ y, int nx, int ny,
@@ -1175,32 +995,6 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
   return hipGetLastError();
 }
 
-// K (3..kJacMaxFuse) Jacobi steps, forward or adjoint, in one launch.
-template <class R, int K, bool ADJ>
-void jacobi_march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
-  using G = JmGeom<R, K>;
-  const int ns = cdiv(s.nx, G::OW);
-  const int nedge = ns >= 2 ? 2 : 1;
-  const int ce = cdiv(s.ny, kJmEdgeRows), ci = cdiv(s.ny, kJmRows);
-  const int nb = nedge * ce + (ns - nedge) * ci;
-  jacobi_march<R, K, ADJ><<<dim3(xcd_grid(nb)), dim3(kBX), 0, st>>>(
-      x, y, s.nx, s.ny, ns, nedge, ce, ci, nb, vec_ok<R>(s.nx, x, y), R(s.p0));
-}
-
-template <class R, bool ADJ>
-hipError_t jacobi_steps_t(const StepShape& s, const void* xv, void* yv, int n, hipStream_t st) {
-  const R* x = static_cast<const R*>(xv);
-  R* y = static_cast<R*>(yv);
-  switch (n) {
-    case 3: jacobi_march_launch<R, 3, ADJ>(s, x, y, st); break;
-    case 4: jacobi_march_launch<R, 4, ADJ>(s, x, y, st); break;
-    case 5: jacobi_march_launch<R, 5, ADJ>(s, x, y, st); break;
-    case 6: jacobi_march_launch<R, 6, ADJ>(s, x, y, st); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
 template <class R>
 hipError_t adjoint2_t(const StepShape& s, const void* gv, void* gpv, hipStream_t st) {
   const R* g = static_cast<const R*>(gv);
@@ -1257,8 +1051,7 @@ hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, vo
   if (n == 2)
     return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, true, stream)
                                : forward_t<float>(s, x, K, y, true, stream);
-  return s.dtype == ADST_F64 ? jacobi_steps_t<double, false>(s, x, y, n, stream)
-                             : jacobi_steps_t<float, false>(s, x, y, n, stream);
+  return launch_jacobi_march(s, x, y, n, false, stream);
 }
 
 hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev, int32_t n,
@@ -1267,8 +1060,7 @@ hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev
   if (n == 2)
     return s.dtype == ADST_F64 ? adjoint2_t<double>(s, g_next, g_prev, stream)
                                : adjoint2_t<float>(s, g_next, g_prev, stream);
-  return s.dtype == ADST_F64 ? jacobi_steps_t<double, true>(s, g_next, g_prev, n, stream)
-                             : jacobi_steps_t<float, true>(s, g_next, g_prev, n, stream);
+  return launch_jacobi_march(s, g_next, g_prev, n, true, stream);
 }
 
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
