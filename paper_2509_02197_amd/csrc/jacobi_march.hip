@@ -5,14 +5,13 @@
 // The step (adst.h, ADST_JACOBI2D5): interior points take
 //     x'[c] = w * ((((x[c] + x[W]) + x[E]) + x[S]) + x[N]),
 // the ring is copied; the adjoint is its transpose in gather form,
-//     interior m: g'[m] = w * (g[m] + sum of gi over the neighbours of m)
-//     ring m:     g'[m] = g[m] + w * (sum of gi over the neighbours of m)
-// with gi = g on interior points and 0 on the ring, the neighbours summed in
-// the order W, E, S, N. A point two or more cells from the edge sees only
-// interior neighbours, so there the adjoint is the same plain average as the
-// forward. Both are linear in the carried state, so their adjoints read no
-// forward state (Sec. IV) and n steps of either compose without any stored
-// value in between.
+//     interior m: g'[m] = w * (g[m] + (((gi[W] + gi[E]) + gi[S]) + gi[N]))
+//     ring m:     g'[m] = g[m] + w * (((gi[W] + gi[E]) + gi[S]) + gi[N])
+// with gi = g on interior points and 0 on the ring (and outside the grid).
+// A point two or more cells from the edge sees only interior neighbours, so
+// there both take their unmasked form. The step is linear in the carried
+// state, so its adjoint reads no forward state (Sec. IV) and n steps of
+// either compose without any stored value in between.
 //
 // Layout. A workgroup is one wave of 64 lanes owning a strip of 64 * V
 // columns (V elements, 16 bytes, per lane) and a chunk of rows. It marches
@@ -36,7 +35,7 @@
 //
 // Boundary. Blocks of kUnroll consecutive input rows whose evaluated rows all
 // lie two or more cells from the top and bottom edge, in a strip two or more
-// cells from the side edges, take the plain average; the others evaluate the
+// cells from the side edges, take the unmasked forms; the others evaluate the
 // ring logic as selects on per-lane column flags. The first and last strip
 // (the side edges) take short chunks, and every XCD gets an equal share of
 // them, so their slower blocks do not become the launch's tail.
@@ -124,7 +123,7 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
 
   // Per-lane column facts of the V columns.
   auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
-  bool cok[V], cI[V], cW[V], cE[V], cF[V];
+  bool cok[V], cI[V], cW[V], cE[V];
 #pragma unroll
   for (int e = 0; e < V; ++e) {
     const int c = c0 + e;
@@ -132,7 +131,6 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
     cI[e] = cin(c);
     cW[e] = cin(c - 1);
     cE[e] = cin(c + 1);
-    cF[e] = c >= 2 && c <= nx - 3;
   }
   const bool strip_in = s0 - H >= 2 && s0 - H + kLanes * V <= nx - 2;
   const bool st_lane = lane * V >= H && lane * V < H + OW;
@@ -195,22 +193,24 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
           for (int e = 0; e < V; ++e) {
             const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
             const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
-            const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
-            if constexpr (FAST) {
-              o[e] = f;
+            if constexpr (!ADJ) {
+              const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
+              if constexpr (FAST) {
+                o[e] = f;
+              } else {
+                const bool rj = j >= 1 && j <= ny - 2;
+                o[e] = (cI[e] && rj) ? f : a[e];
+              }
+            } else if constexpr (FAST) {
+              o[e] = w * (a[e] + (((Wn + En) + S[e]) + N[e]));
             } else {
               const bool rj = j >= 1 && j <= ny - 2, rS = j >= 2 && j <= ny - 1,
-                         rN = j >= 0 && j <= ny - 3, rF = j >= 2 && j <= ny - 3;
-              if constexpr (!ADJ) {
-                o[e] = (cI[e] && rj) ? f : a[e];
-              } else {
-                R sum = (cW[e] && rj) ? Wn : R(0);
-                sum += (cE[e] && rj) ? En : R(0);
-                sum += (cI[e] && rS) ? S[e] : R(0);
-                sum += (cI[e] && rN) ? N[e] : R(0);
-                const R gr = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
-                o[e] = (cF[e] && rF) ? f : gr;
-              }
+                         rN = j >= 0 && j <= ny - 3;
+              R sum = (cW[e] && rj) ? Wn : R(0);
+              sum += (cE[e] && rj) ? En : R(0);
+              sum += (cI[e] && rS) ? S[e] : R(0);
+              sum += (cI[e] && rN) ? N[e] : R(0);
+              o[e] = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
             }
           }
           if (k < K) {

@@ -82,8 +82,7 @@ __device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int
 // kernels call the same functions, so a fused launch is bit-identical to two
 // single launches.
 
-// w*((((v[c]+v[W])+v[E])+v[S])+v[N]): the forward step at an interior point,
-// and also the adjoint step at a point whose neighbours are all interior.
+// w*((((v[c]+v[W])+v[E])+v[S])+v[N]): the forward step at an interior point.
 template <class R, int LW>
 __device__ inline R jacobi_avg_at(const R* s, int q, R w) {
   R sum = s[q];
@@ -105,10 +104,27 @@ __device__ inline R jacobi_fwd_at(const R* s, int q, int i, int j, int nx, int n
 // Jacobi adjoint (gather): with gi(p) = g[p] on interior p and 0 elsewhere,
 //   interior m: g'[m] = w * (g[m] + sum_{p in nbr(m)} gi(p))
 //   ring m:     g'[m] = g[m] + w * sum_{p in nbr(m)} gi(p)
-// Points two or more cells from the edge see only interior neighbours.
+// the neighbours summed in the order W, E, S, N. Points two or more cells
+// from the edge see only interior neighbours: w*(g[m] + (((W+E)+S)+N)).
+template <class R, int LW>
+__device__ inline R jacobi_adj_inner_at(const R* s, int q, R w) {
+  R sum = s[q - 1];
+  sum += s[q + 1];
+  sum += s[q - LW];
+  sum += s[q + LW];
+  return w * (s[q] + sum);
+}
+
+// The value of a point whose stencil reads only interior points: the
+// forward's average, or the adjoint's inner form.
+template <class R, int LW, bool ADJ>
+__device__ inline R jacobi_inner_at(const R* s, int q, R w) {
+  return ADJ ? jacobi_adj_inner_at<R, LW>(s, q, w) : jacobi_avg_at<R, LW>(s, q, w);
+}
+
 template <class R, int LW>
 __device__ inline R jacobi_adj_at(const R* s, int q, int i, int j, int nx, int ny, R w) {
-  if (i >= 2 && i <= nx - 3 && j >= 2 && j <= ny - 3) return jacobi_avg_at<R, LW>(s, q, w);
+  if (i >= 2 && i <= nx - 3 && j >= 2 && j <= ny - 3) return jacobi_adj_inner_at<R, LW>(s, q, w);
   const R c = s[q];
   auto interior = [&](int a, int b) { return a > 0 && a < nx - 1 && b > 0 && b < ny - 1; };
   R sum = interior(i - 1, j) ? s[q - 1] : R(0);
@@ -211,7 +227,7 @@ __device__ inline void jacobi_tile(const R* __restrict__ x, R* __restrict__ y, i
   if (jacobi_all_avg<ADJ>(i0, i0 + kJacTW - 1, j0, j0 + kJacTR - 1, nx, ny)) {
 #pragma unroll
     for (int r = 0; r < kJacTR; ++r)
-      y[(j0 + r) * nx + i] = out(jacobi_avg_at<R, G::LW>(s, (r + 1) * G::LW + cx, w));
+      y[(j0 + r) * nx + i] = out(jacobi_inner_at<R, G::LW, ADJ>(s, (r + 1) * G::LW + cx, w));
     return;
   }
 #pragma unroll
@@ -247,7 +263,8 @@ __device__ inline void jacobi_tile_x2(const R* __restrict__ x, R* __restrict__ y
   if (act) {
     if (avg) {
 #pragma unroll
-      for (int r = 1; r <= kX2TR + 2; ++r) v[r - 1] = jacobi_avg_at<R, G::LW>(s, r * G::LW + c, w);
+      for (int r = 1; r <= kX2TR + 2; ++r)
+        v[r - 1] = jacobi_inner_at<R, G::LW, ADJ>(s, r * G::LW + c, w);
     } else {
 #pragma unroll
       for (int r = 1; r <= kX2TR + 2; ++r) {
@@ -271,7 +288,7 @@ __device__ inline void jacobi_tile_x2(const R* __restrict__ x, R* __restrict__ y
   if (avg) {
 #pragma unroll
     for (int r = 0; r < kX2TR; ++r)
-      y[(j0 + r) * nx + i] = jacobi_avg_at<R, G::LW>(s, (r + 2) * G::LW + cx, w);
+      y[(j0 + r) * nx + i] = jacobi_inner_at<R, G::LW, ADJ>(s, (r + 2) * G::LW + cx, w);
     return;
   }
 #pragma unroll
