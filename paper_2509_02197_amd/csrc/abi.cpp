@@ -101,7 +101,7 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   out->trace = (p->flags & ADST_TRACE) != 0;
   const bool fuse = (p->flags & ADST_NO_FUSE) == 0;
   out->fuse_fwd = (fuse && !limit) ? max_fused_forward(p->kind) : 1;
-  out->fuse_adj = fuse ? max_fused_adjoint(p->kind) : 1;
+  out->fuse_adj = fuse ? max_fused_adjoint(p->kind, p->n[0]) : 1;
   out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
   return ADST_OK;
 }

@@ -36,9 +36,10 @@
 // Boundary. Blocks of kUnroll consecutive input rows whose evaluated rows all
 // lie two or more cells from the top and bottom edge, in a strip two or more
 // cells from the side edges, take the unmasked forms; the others evaluate the
-// ring logic as selects on per-lane column flags. The first and last strip
-// (the side edges) take short chunks, and every XCD gets an equal share of
-// them, so their slower blocks do not become the launch's tail.
+// ring logic. A strip's first and last chunk are short, so the slower blocks
+// near the top and bottom edge do not make their waves the launch's tail;
+// the first and last strip (the side edges) take short chunks throughout,
+// and every XCD gets an equal share of them.
 
 #include <hip/hip_runtime.h>
 
@@ -52,11 +53,15 @@ namespace {
 
 constexpr int kLanes = 64;
 constexpr int kRows = 48;      // rows per chunk of an interior strip
-constexpr int kEdgeRows = 8;   // rows per chunk of the first and last strip
-constexpr int kAhead = 6;      // input rows loaded ahead of the pipeline
+constexpr int kEdgeRows = 12;  // rows per chunk of the first and last strip
+constexpr int kEndRows = 6;    // rows of a strip's first and last chunk, whose
+                               // blocks near the grid's top and bottom edge
+                               // take the slower general path
+constexpr int kAhead = 3;      // input rows loaded ahead of the pipeline
 constexpr int kUnroll = 6;     // input rows per straight-line block
 constexpr int kXcds = 8;       // workgroup i runs on XCD i mod 8
 static_assert(kUnroll % kAhead == 0 && kUnroll % 3 == 0, "register slots must stay static");
+static_assert(2 * kEndRows <= kRows && kEdgeRows <= kRows && kRows <= 64, "chunk sizes");
 
 // Whole-wave lane shifts: lane i receives lane i-1's value (lane 0: 0) or
 // lane i+1's (lane 63: 0).
@@ -100,40 +105,66 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
   constexpr int V = G::V, H = G::H, OW = G::OW, P = kAhead, U = kUnroll;
   typedef R vec_t __attribute__((ext_vector_type(V)));
   const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
-  int strip, chunk, rpc;
+  int strip, chunk, nch, mid;
   if (slot < g.pe) {
     const int t = xcd * g.pe + slot;
     if (t >= g.nedge * g.ce) return;
     strip = (t / g.ce == 0) ? 0 : g.ns - 1;
     chunk = t % g.ce;
-    rpc = kEdgeRows;
+    nch = g.ce;
+    mid = kEdgeRows;
   } else {
     const int t = xcd * g.pi + (slot - g.pe);
     if (t >= (g.ns - g.nedge) * g.ci) return;
     strip = 1 + t / g.ci;
     chunk = t % g.ci;
-    rpc = kRows;
+    nch = g.ci;
+    mid = kRows;
   }
   const int lane = threadIdx.x;
   const int s0 = strip * OW;
   const int c0 = s0 - H + lane * V;  // first column of this lane
-  const int r0 = chunk * rpc, r1 = min(r0 + rpc, ny);
+  // rows [r0, r1): kEndRows at each end of the strip, mid rows between
+  int r0, r1;
+  if (nch == 1) {
+    r0 = 0;
+    r1 = ny;
+  } else if (chunk == 0) {
+    r0 = 0;
+    r1 = kEndRows;
+  } else if (chunk == nch - 1) {
+    r0 = ny - kEndRows;
+    r1 = ny;
+  } else {
+    r0 = kEndRows + (chunk - 1) * mid;
+    r1 = min(r0 + mid, ny - kEndRows);
+  }
   const int nit = (r1 - r0) + 2 * K;  // input rows through the pipeline
   const int lo_need = max(r0 - K, 0), hi_need = min(r1 + K - 1, ny - 1);
 
   // Per-lane column facts of the V columns.
   auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
-  bool cok[V], cI[V], cW[V], cE[V];
+  bool cok[V], cI[V];
+  int side[V];  // 0: column 0, 1: column nx-1, -1: neither
 #pragma unroll
   for (int e = 0; e < V; ++e) {
     const int c = c0 + e;
     cok[e] = c >= 0 && c < nx;
     cI[e] = cin(c);
-    cW[e] = cin(c - 1);
-    cE[e] = cin(c + 1);
+    side[e] = c == 0 ? 0 : (c == nx - 1 ? 1 : -1);
   }
   const bool strip_in = s0 - H >= 2 && s0 - H + kLanes * V <= nx - 2;
   const bool st_lane = lane * V >= H && lane * V < H + OW;
+  // This lane's ring column, if any (a lane holds at most one: nx > V), and
+  // its element; with 16-byte rows, column 0 is a lane's first element and
+  // column nx-1 its last.
+  int rside = -1, relem = 0;
+#pragma unroll
+  for (int e = 0; e < V; ++e)
+    if (side[e] >= 0) {
+      rside = side[e];
+      relem = e;
+    }
 
   // Raw load of input row `row` (clamped to the rows the chunk needs, and
   // to the grid, so every address is in bounds); masked on entry.
@@ -151,12 +182,33 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
     }
   };
 
-  auto march = [&](auto dir_t) {
+  // The adjoint's pipeline holds gi: every ring cell and every cell outside
+  // the grid holds +0 there, so each interior point's masked neighbour sum
+  // is the plain sum of the pipeline's values (the terms a mask would drop
+  // are +0 already). The ring's own values, g + w*sum, read no other ring
+  // value and are kept beside the pipeline: ring_lo and ring_hi hold the
+  // bottom and top ring rows at the highest level that has evaluated them
+  // (one level reaches a given row per input row), and the one interior
+  // neighbour a ring-column cell has is recorded at every level in LDS, from
+  // which the ring columns of the chunk's rows are summed after the march.
+  // Rows of the record: every row a level may evaluate, [r0 - K - U, r1 + K + U).
+  constexpr int NR = kRows + 2 * (K + U);
+  __shared__ R nbr[ADJ ? 2 * K * NR + kLanes : 1];
+  // LDS index of row j's record at level k: nbr_lane + (k-1)*NR + j, or the
+  // lane's scratch cell when it has no ring column
+  const bool has_ring = rside >= 0;
+  const int nbr_lane = rside * K * NR + (K + U) - r0;
+  enum { kFast = 0, kCols = 1, kGeneral = 2 };
+  // mid_t: the mode of the blocks away from the top and bottom edge.
+  auto march = [&](auto dir_t, auto mid_t) {
     constexpr int DIR = decltype(dir_t)::value;  // +1 upward, -1 downward
     const int ifirst = DIR > 0 ? r0 - K : r1 - 1 + K;  // row of input index 0
     // Level k's row of pipeline index p (row ifirst + DIR*p) sits in slot p mod 3.
     R lv[K][3][V];
     R pf[P][V];
+    R ring_lo[V], ring_hi[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) ring_lo[e] = ring_hi[e] = R(0);
 #pragma unroll
     for (int k = 0; k < K; ++k)
 #pragma unroll
@@ -166,16 +218,37 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
 #pragma unroll
     for (int u = 0; u < P; ++u) load(ifirst + DIR * u, pf[u]);
 
-    auto block = [&](int base, auto fast_t) {
-      constexpr bool FAST = decltype(fast_t)::value;
+    // kFast: rows in [2, ny-3], strip in columns [2, nx-3]: unmasked forms.
+    // kCols: rows in [2, ny-3], strip touching the side edges.
+    // kGeneral: anything (rows near or beyond the top and bottom edge).
+    auto block = [&](int base, auto mode_t) {
+      constexpr int MODE = decltype(mode_t)::value;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int rr = base + u;
         {  // input row rr enters level 0; the row P ahead is requested
           const int row = ifirst + DIR * rr;
-          const bool rok = row >= 0 && row < ny;
+          if constexpr (MODE == kFast) {
 #pragma unroll
-          for (int e = 0; e < V; ++e) lv[0][u % 3][e] = (rok && cok[e]) ? pf[u % P][e] : R(0);
+            for (int e = 0; e < V; ++e) lv[0][u % 3][e] = pf[u % P][e];
+          } else if constexpr (!ADJ) {
+            const bool rok = row >= 0 && row < ny;
+#pragma unroll
+            for (int e = 0; e < V; ++e)
+              lv[0][u % 3][e] = (rok && cok[e]) ? pf[u % P][e] : R(0);
+          } else {
+            if constexpr (MODE == kGeneral) {
+#pragma unroll
+              for (int e = 0; e < V; ++e) {
+                const R v = cok[e] ? pf[u % P][e] : R(0);
+                ring_lo[e] = row == 0 ? v : ring_lo[e];
+                ring_hi[e] = row == ny - 1 ? v : ring_hi[e];
+              }
+            }
+            const bool rin = MODE == kCols || (row >= 1 && row <= ny - 2);
+#pragma unroll
+            for (int e = 0; e < V; ++e) lv[0][u % 3][e] = (rin && cI[e]) ? pf[u % P][e] : R(0);
+          }
           load(row + DIR * P, pf[u % P]);
         }
 #pragma unroll
@@ -188,35 +261,65 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
           const R* S = lv[k - 1][DIR > 0 ? sOld : sNew];
           const R* N = lv[k - 1][DIR > 0 ? sNew : sOld];
           const R wl = from_prev(a[V - 1]), er = from_next(a[0]);
+          const bool rj = MODE != kGeneral || (j >= 1 && j <= ny - 2);  // uniform
           R o[V];
+          if constexpr (!ADJ) {
 #pragma unroll
-          for (int e = 0; e < V; ++e) {
-            const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
-            const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
-            if constexpr (!ADJ) {
+            for (int e = 0; e < V; ++e) {
+              const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
+              const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
               const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
-              if constexpr (FAST) {
+              if constexpr (MODE == kFast)
                 o[e] = f;
-              } else {
-                const bool rj = j >= 1 && j <= ny - 2;
+              else
                 o[e] = (cI[e] && rj) ? f : a[e];
+            }
+          } else {
+            R sum[V], Ws[V], Es[V];
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              Ws[e] = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
+              Es[e] = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
+              sum[e] = ((Ws[e] + Es[e]) + S[e]) + N[e];
+            }
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              if constexpr (MODE == kFast)
+                o[e] = w * (a[e] + sum[e]);
+              else
+                o[e] = (cI[e] && rj) ? w * (a[e] + sum[e]) : R(0);
+            }
+            if constexpr (MODE != kFast) {
+              // record the ring cell's interior neighbour (E of column 0, W
+              // of column nx-1) for rows of this chunk; other lanes write
+              // their own scratch cell
+              R nb;
+              if constexpr (VEC) {
+                nb = rside == 0 ? Es[0] : Ws[V - 1];
+              } else {
+                nb = R(0);
+#pragma unroll
+                for (int e = 0; e < V; ++e) nb = relem == e ? (rside == 0 ? Es[e] : Ws[e]) : nb;
               }
-            } else if constexpr (FAST) {
-              o[e] = w * (a[e] + (((Wn + En) + S[e]) + N[e]));
-            } else {
-              const bool rj = j >= 1 && j <= ny - 2, rS = j >= 2 && j <= ny - 1,
-                         rN = j >= 0 && j <= ny - 3;
-              R sum = (cW[e] && rj) ? Wn : R(0);
-              sum += (cE[e] && rj) ? En : R(0);
-              sum += (cI[e] && rS) ? S[e] : R(0);
-              sum += (cI[e] && rN) ? N[e] : R(0);
-              o[e] = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
+              nbr[has_ring ? nbr_lane + (k - 1) * NR + j : 2 * K * NR + lane] = nb;
+            }
+            if constexpr (MODE == kGeneral) {
+#pragma unroll
+              for (int e = 0; e < V; ++e) {
+                ring_lo[e] = j == 0 ? (cok[e] ? ring_lo[e] + w * sum[e] : R(0)) : ring_lo[e];
+                ring_hi[e] = j == ny - 1 ? (cok[e] ? ring_hi[e] + w * sum[e] : R(0)) : ring_hi[e];
+              }
             }
           }
           if (k < K) {
 #pragma unroll
             for (int e = 0; e < V; ++e) lv[k][sc][e] = o[e];
           } else if (j >= r0 && j < r1 && st_lane) {
+            if constexpr (ADJ && MODE == kGeneral) {  // ring rows
+#pragma unroll
+              for (int e = 0; e < V; ++e)
+                o[e] = j == 0 ? ring_lo[e] : (j == ny - 1 ? ring_hi[e] : o[e]);
+            }
             R* dst = y + (int64_t)j * nx;
             if constexpr (VEC) {
               if (c0 + V <= nx) {
@@ -246,26 +349,68 @@ __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, 
       fb = ifirst - U;
     }
     fa = ((max(fa, 0) + U - 1) / U) * U;
-    if (!strip_in) fa = fb = 0;
+    using General = std::integral_constant<int, kGeneral>;
     int base = 0;
-    for (; base < nit && base < fa; base += U) block(base, std::false_type{});
-    for (; base < nit && base < fb; base += U) block(base, std::true_type{});
-    for (; base < nit; base += U) block(base, std::false_type{});
+    for (; base < nit && base < fa; base += U) block(base, General{});
+    for (; base < nit && base < fb; base += U) block(base, mid_t);
+    for (; base < nit; base += U) block(base, General{});
   };
+  // Each combination gets its own straight code path, chosen before any
+  // state is live.
+  using Up = std::integral_constant<int, 1>;
+  using Down = std::integral_constant<int, -1>;
+  using Fast = std::integral_constant<int, kFast>;
+  using Cols = std::integral_constant<int, ADJ ? kCols : kGeneral>;
+  if (strip_in) {
+    if (chunk & 1)
+      march(Down{}, Fast{});
+    else
+      march(Up{}, Fast{});
+    return;
+  }
   if (chunk & 1)
-    march(std::integral_constant<int, -1>{});
+    march(Down{}, Cols{});
   else
-    march(std::integral_constant<int, 1>{});
+    march(Up{}, Cols{});
+  if constexpr (ADJ) {
+    // The ring columns of this chunk's interior rows, one row per lane:
+    // g_n = g_0 + w*(((0 + E) + 0) + 0) level by level on the left,
+    // g_0 + w*(((W + 0) + 0) + 0) on the right, E and W the recorded
+    // neighbours. All earlier stores and LDS writes complete first.
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    const int jr = r0 + lane;
+    if (lane < kRows && jr < r1 && jr >= 1 && jr <= ny - 2) {
+#pragma unroll
+      for (int sd = 0; sd < 2; ++sd) {
+        const int col = sd == 0 ? 0 : nx - 1;
+        if (col < s0 || col >= s0 + OW) continue;  // not this strip's output column
+        const int64_t q = (int64_t)jr * nx + col;
+        R g = x[q];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          const R v = nbr[(sd * K + k) * NR + (K + U) + lane];
+          const R sum = sd == 0 ? ((R(0) + v) + R(0)) + R(0) : ((v + R(0)) + R(0)) + R(0);
+          g = g + w * sum;
+        }
+        y[q] = g;
+      }
+    }
+  }
 }
 
 template <class R, int K, bool ADJ>
 hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
   using G = Geom<R, K>;
+  if (ADJ && s.nx <= G::V) return hipErrorInvalidValue;  // a lane would hold both ring columns
   MarchGrid g;
   g.ns = (s.nx + G::OW - 1) / G::OW;
   g.nedge = g.ns >= 2 ? 2 : 1;
-  g.ce = (s.ny + kEdgeRows - 1) / kEdgeRows;
-  g.ci = (s.ny + kRows - 1) / kRows;
+  auto chunks = [&](int mid) {
+    return s.ny > 2 * kEndRows ? 2 + (s.ny - 2 * kEndRows + mid - 1) / mid : 1;
+  };
+  g.ce = chunks(kEdgeRows);
+  g.ci = chunks(kRows);
   const int64_t E = int64_t(g.nedge) * g.ce, I = int64_t(g.ns - g.nedge) * g.ci;
   g.pe = (int)((E + kXcds - 1) / kXcds);
   g.pi = (int)((I + kXcds - 1) / kXcds);

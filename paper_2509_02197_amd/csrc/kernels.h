@@ -26,7 +26,7 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 // fused adjoint is for state-free adjoints only.
 constexpr int32_t kJacMaxFuse = 6;
 int32_t max_fused_forward(int32_t kind);
-int32_t max_fused_adjoint(int32_t kind);
+int32_t max_fused_adjoint(int32_t kind, int64_t nx);
 
 // x_t = F^n(x_{t-n}) in one launch (2 <= n <= max_fused_forward), the
 // intermediate states kept on chip.

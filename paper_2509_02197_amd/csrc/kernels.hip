@@ -1060,7 +1060,12 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 int32_t max_fused_forward(int32_t kind) {
   return kind == ADST_JACOBI2D5 ? kJacMaxFuse : kind == ADST_ALLENCAHN3D7 ? 2 : 1;
 }
-int32_t max_fused_adjoint(int32_t kind) { return kind == ADST_JACOBI2D5 ? kJacMaxFuse : 1; }
+// The marching adjoint needs rows wider than one lane's 16 bytes; narrower
+// grids take the fused pair.
+int32_t max_fused_adjoint(int32_t kind, int64_t nx) {
+  if (kind != ADST_JACOBI2D5) return 1;
+  return nx > 4 ? kJacMaxFuse : 2;
+}
 
 hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, void* y, int32_t n,
                             hipStream_t stream) {
@@ -1073,7 +1078,7 @@ hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, vo
 
 hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev, int32_t n,
                             hipStream_t stream) {
-  if (n < 2 || n > max_fused_adjoint(s.kind)) return hipErrorInvalidValue;
+  if (n < 2 || n > max_fused_adjoint(s.kind, s.nx)) return hipErrorInvalidValue;
   if (n == 2)
     return s.dtype == ADST_F64 ? adjoint2_t<double>(s, g_next, g_prev, stream)
                                : adjoint2_t<float>(s, g_next, g_prev, stream);

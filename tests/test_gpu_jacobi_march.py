@@ -74,7 +74,8 @@ def test_fused_adjoint_bitwise(dtype, shape):
         say(f"march adjoint dtype={dtype} shape={shape} T={T}")
         a = gpu_vjp(J, inp, T, adst.ADST_LOSS_DOT_W)
         b = gpu_vjp(J, inp, T, adst.ADST_LOSS_DOT_W, flags=adst.ADST_NO_FUSE)
-        assert a["info"]["adj_launches"] == -(-T // 6)
+        depth = 6 if shape[1] > 4 else 2  # the marching adjoint needs nx > 16 bytes
+        assert a["info"]["adj_launches"] == -(-T // depth)
         assert np.array_equal(a["dx0"], b["dx0"]), T
         assert np.array_equal(a["xT"], b["xT"]), T
         dx0, _, xT, _ = oracle.vjp(J, inp["x0"], steps=T, loss=adst.ADST_LOSS_DOT_W,
