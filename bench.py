@@ -54,7 +54,13 @@ def kernel_mix(kind, acts, adj):
             k = kernel_name(kind, adj, n)
             mix[k] = mix.get(k, 0) + 1
     return mix
-KERNEL_SOURCE = {0: "kernels.hip", 1: "kernels.hip", 2: "kernels.hip", 3: "gauss_seidel.hip"}
+def kernel_source(kernel):
+    """The source file holding a kernel (by its short name)."""
+    if kernel.startswith("jacobi_march"):
+        return "jacobi_march.hip"
+    if kernel.startswith("gs_wave"):
+        return "gauss_seidel.hip"
+    return "kernels.hip"
 
 
 def parse():
@@ -81,24 +87,24 @@ def parse():
     return ap.parse_args()
 
 
-def source_sha(kind):
-    """Hash of the source file holding the kind's kernels."""
+def source_sha(kernel):
+    """Hash of the source file holding the kernel."""
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2509_02197_amd", "csrc", KERNEL_SOURCE[kind]), "rb") as fh:
+    with open(os.path.join(ROOT, "paper_2509_02197_amd", "csrc", kernel_source(kernel)), "rb") as fh:
         h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_for(workload, kernel, kind):
+def traffic_for(workload, kernel):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
-    or None when none exists for this kernel source."""
+    or None when none exists for this kernel's current source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         table = json.load(f)
     e = table.get(f"{workload}:{kernel}")
-    if not e or e.get("src_sha") != source_sha(kind):
+    if not e or e.get("src_sha") != source_sha(kernel):
         return None
     return e["bytes_per_launch"]
 
@@ -237,7 +243,7 @@ def main():
     avg_ms = ms_k / max(nl, 1)
     alg_bytes = alg_total / max(nl, 1)
     achieved = alg_total / (ms_k * 1e-3) / 1e9
-    traffic = traffic_for(name, kernel, w.kind)
+    traffic = traffic_for(name, kernel)
     roofline = {
         "bound": "hbm", "kernel": kernel, "kernel_mix": mix, "achieved": round(achieved, 1),
         "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),

@@ -717,7 +717,7 @@ __global__ __launch_bounds__(kThreads) void seed_loss(const R* x, const R* __res
       term = (double)a * (double)xv;
     }
     if (xcopy) xcopy[i] = xv;
-    g[i] = gv;
+    if (g) g[i] = gv;
     acc += term;
   }
   const double s = block_sum(acc);
@@ -1028,7 +1028,9 @@ hipError_t seed_t(int32_t loss, int64_t n, const void* xv, const void* auxv, voi
                   void* xcopyv, double* partials, hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
   const R* aux = static_cast<const R*>(auxv);
-  R* g = static_cast<R*>(gv);
+  // g_T = x_T for the half square: when x_T already sits in g_T's buffer,
+  // only the loss is computed
+  R* g = (loss == ADST_LOSS_HALF_SQ && gv == xv) ? nullptr : static_cast<R*>(gv);
   R* xcopy = static_cast<R*>(xcopyv);
   const dim3 block(kBX, kBY);
   const dim3 grid(seed_partials(n));

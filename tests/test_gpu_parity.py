@@ -226,3 +226,19 @@ def test_fused_launches_match_single_steps_bitwise(kind, dtype, shape, T, loss, 
             assert np.array_equal(a[key], b[key]), key
     assert a["loss"] == b["loss"]
     check_against_oracle(kind, dtype, inp, T, loss, dK, a)
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T", [
+    (J, F64, (130, 257), 9), (J, F32, (64, 64), 1), (AC, F64, (20, 17, 33), 5),
+    (VD, F32, (70, 129), 4), (J, F64, (7, 9), 0),
+])
+def test_half_square_without_xT_output(kind, dtype, shape, T):
+    """Without an x_T output, x_T is written straight into g_T's buffer and
+    the half-square seed only reduces the loss there: the same bits as with
+    the output."""
+    say(f"half-square seed without xT kind={kind} dtype={dtype} shape={shape} T={T}")
+    inp = inputs(kind, dtype, shape, 12)
+    a = gpu_vjp(kind, inp, T, HALF_SQ, want_xT=True)
+    b = gpu_vjp(kind, inp, T, HALF_SQ, want_xT=False)
+    assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
+    check_against_oracle(kind, dtype, inp, T, HALF_SQ, False, a)
