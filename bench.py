@@ -224,6 +224,9 @@ def main():
     isz = 8 if w.dtype == adst.ADST_F64 else 4
     fwd_B = {0: 2, 1: 2, 2: 3, 3: 2}[w.kind] * isz
     adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3, 3: 2}[w.kind] * isz
+    if args.dparams and (w.kind == adst.ADST_JACOBI2D5 or
+                         (w.kind == adst.ADST_VARDIFF2D9 and not w.want_dK)):
+        adj_B += isz  # the fused constants' gradients also read x_{t-1}
     in_place = w.kind == adst.ADST_GAUSSSEIDEL2D5
     # units of fwd_B * npoints moved per call: one per launch, or one per step
     fwd_units = info.fwd_steps_total if in_place else info.fwd_launches
@@ -255,11 +258,8 @@ def main():
         "adj_avg_ms": round(adj_avg, 5),
         "adj_gbps": round(adj_B * w.npoints * adj_units / max(acc["ms_adj"], 1e-9) / 1e6, 1),
     }
-    if args.dparams:  # the constants' gradient kernel: reads x_{t-1}, g_t (and K) per step
-        dp_B = (3 if w.kind == adst.ADST_VARDIFF2D9 else 2) * isz
-        roofline["dparam_ms"] = round(acc["ms_dparams"], 4)
-        roofline["dparam_gbps"] = round(dp_B * w.npoints * info.adj_steps /
-                                        max(acc["ms_dparams"], 1e-9) / 1e6, 1)
+    if args.dparams:  # the final sum of the constants' per-workgroup slots
+        roofline["dparam_finalize_ms"] = round(acc["ms_dparams"], 4)
 
     res = {
         "metric": METRIC, "value": value, "unit": "grid-point-steps/s", "n_gpus": 1,

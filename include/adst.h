@@ -221,7 +221,8 @@ typedef struct {
   float ms_adj;             /*   ... of the adjoint steps */
   float ms_seed;            /*   ... of the loss/seed and its final reduction */
   float ms_total;           /*   first launch start to last launch end */
-  float ms_dparams;         /*   ... of the constants' gradient kernels */
+  float ms_dparams;         /*   ... of the constants' gradient sum (the final reduction; the
+                               per-step shares run inside the adjoint launches) */
 } adst_plan_info;
 
 /* Plan a forward+VJP call without touching the GPU (host only).

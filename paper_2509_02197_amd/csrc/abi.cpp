@@ -129,7 +129,7 @@ Layout layout_for(const Checked& c, const Plan& plan) {
   L.total = L.slot0 + uint64_t(plan.slots) * L.state_stride;
   if (c.want_dp) {  // per-block slots of the constants' gradients
     L.dp = L.total;
-    L.total += align_up(uint64_t(dparam_partial_bytes()));
+    L.total += align_up(uint64_t(dparam_partial_bytes(c.shape)));
   }
   return L;
 }
@@ -156,8 +156,11 @@ void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd
       break;
   }
   *seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
-  // the constants' gradient kernel reads x_{t-1} and g_t (and K)
-  *dparam = c.want_dp ? (c.shape.kind == ADST_VARDIFF2D9 ? 3 : 2) * s : 0;
+  // the constants' gradients, fused into the adjoint, add the reads of
+  // x_{t-1} the adjoint does not already make
+  *dparam = 0;
+  if (c.want_dp && (c.shape.kind == ADST_JACOBI2D5 || (c.shape.kind == ADST_VARDIFF2D9 && !want_dk)))
+    *dparam = s;
   // the limiter's branch mask reads x_{t-1} (and K) and updates g_t in place
   if (c.shape.limit) *dparam += (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
 }
@@ -525,13 +528,10 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
           e = launch_limit_mask(c.shape, xs, coeff, gcur, stream);
           if (e != hipSuccess) return hip_fail(e, "kernel launch");
         }
-        if (dparams) {  // this step's share of the constants' gradients, from g_t
-          if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
-          e = launch_dparam_step(c.shape, xs, coeff, gcur, dp_part, a.t == steps, stream);
-          if (e != hipSuccess) return hip_fail(e, "kernel launch");
-          if ((e = tr.before(stream, Tracer::ADJ)) != hipSuccess) return hip_fail(e, "trace event");
-        }
-        e = launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps, stream);
+        // with dparams, the launch also adds this step's share of the
+        // constants' gradients, from g_t and x_{t-1}
+        e = launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps,
+                           dparams ? dp_part : nullptr, a.t == steps, stream);
         std::swap(gcur, gnext);
         break;
       }
@@ -546,7 +546,7 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   }
   if (dparams && steps > 0) {
     if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
-    if ((e = launch_dparam_finalize(dp_part, dparams, stream)) != hipSuccess)
+    if ((e = launch_dparam_finalize(c.shape, dp_part, dparams, stream)) != hipSuccess)
       return hip_fail(e, "kernel launch");
   }
   if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");

@@ -43,10 +43,15 @@ hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32
                                hipStream_t stream);
 
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
-// reads no state and dK is not asked for). dK (nullable) is accumulated:
-// dK = (dk_first ? 0 : dK) + contribution of step t.
+// reads no state and neither dK nor the constants' gradients are asked for).
+// dK (nullable) is accumulated: dK = (dk_first ? 0 : dK) + contribution of
+// step t. dp_part (nullable; dparam_partial_bytes(s) bytes) receives step
+// t's share of the constants' gradients: sum_c g_t[c] dF_c/dp (x = x_{t-1}),
+// added per workgroup into its slot (dp_first = the step t = T, which
+// overwrites the slots).
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
-                          void* g_prev, void* dK, bool dk_first, hipStream_t stream);
+                          void* g_prev, void* dK, bool dk_first, double* dp_part, bool dp_first,
+                          hipStream_t stream);
 
 // Number of per-block loss partials launch_seed writes for n points.
 int32_t seed_partials(int64_t n);
@@ -76,14 +81,14 @@ int64_t gs_kernel_launches(const StepShape& s, bool adjoint, int32_t sweeps);
 hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, void* g,
                              hipStream_t stream);
 
-// Gradients of the step constants: each adjoint step adds its share
-// sum_c g_t[c] dF_c/dp (x = x_{t-1}) into per-block slots (first = the
-// step t = T, which overwrites them); finalize sums the slots into
+// Gradients of the step constants: the adjoint launches add their steps'
+// shares into per-workgroup slots (launch_adjoint's dp_part; one slot per
+// adjoint tile and constant); finalize sums the slots in a fixed order into
 // dparams[0..1] (device doubles).
-int64_t dparam_partial_bytes();
-hipError_t launch_dparam_step(const StepShape& s, const void* x, const void* K, const void* g,
-                              double* partials, bool first, hipStream_t stream);
-hipError_t launch_dparam_finalize(const double* partials, double* dparams, hipStream_t stream);
+int64_t dparam_slots(const StepShape& s);
+int64_t dparam_partial_bytes(const StepShape& s);
+hipError_t launch_dparam_finalize(const StepShape& s, const double* partials, double* dparams,
+                                  hipStream_t stream);
 
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream);

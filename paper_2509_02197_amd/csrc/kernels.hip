@@ -77,6 +77,55 @@ __device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int
   }
 }
 
+// ------------------------------------------------------- block reductions
+// Sum over the 256 threads of a block: a wave64 butterfly, then the four
+// wave sums in a fixed order. Valid in thread 0.
+__device__ inline double block_sum(double v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  __shared__ double wave_sum[kThreads / 64];
+  const int tid = threadIdx.y * kBX + threadIdx.x;
+  if ((tid & 63) == 0) wave_sum[tid >> 6] = v;
+  __syncthreads();
+  return ((wave_sum[0] + wave_sum[1]) + wave_sum[2]) + wave_sum[3];
+}
+
+// Block sums of two values, each over the 256 threads in a fixed order.
+__device__ inline void block_sum2(double& a, double& b) {
+  a = block_sum(a);
+  __syncthreads();  // block_sum's wave sums are reused
+  b = block_sum(b);
+}
+
+// Gradients of the step constants, fused into the adjoint kernels: one
+// adjoint step's share of dL/dp is the sum over points of g_t[c] times the
+// step's partial dF_c/dp at x_{t-1} (a constant read by every point of every
+// step is a multiply-read input whose gradient accumulates, Sec. II). The
+// partials are the sub-expressions the forward step forms, in its order:
+//   Jacobi               dF/dw  = (((x[c]+x[W])+x[E])+x[S])+x[N] on interior points
+//   Allen-Cahn           dF/dD  = lap,   dF/dC = -((x[c]*x[c])*x[c])
+//   variable coefficient dF/ddt = acc
+// Products and sums are in double. Each workgroup (one tile of the adjoint
+// launch, whose tiling depends only on the grid) sums its points in a fixed
+// order and adds the result into its own slot, step after step in the
+// adjoint order t = T..1 (first: the step t = T overwrites), so the result
+// does not depend on the schedule. part holds nslots slots per constant.
+struct DpOut {
+  double* part;
+  int nslots, first;
+};
+
+// All threads of the block call this (it synchronises).
+__device__ inline void dp_commit(DpOut dp, int slot, double a0, double a1) {
+  block_sum2(a0, a1);
+  if (threadIdx.x == 0 && threadIdx.y == 0) {
+    double* p0 = dp.part + slot;
+    double* p1 = dp.part + dp.nslots + slot;
+    *p0 = dp.first ? a0 : *p0 + a0;
+    *p1 = dp.first ? a1 : *p1 + a1;
+  }
+}
+
 // Point updates read from an LDS array with row stride LW; q is the flat
 // index of the point, (i, j) its grid coordinates. Single-step and fused
 // kernels call the same functions, so a fused launch is bit-identical to two
@@ -314,6 +363,50 @@ __global__ __launch_bounds__(kJacTW) void adj_jacobi2d5(const R* __restrict__ g,
                                                         int tiles_x, int ntiles, int vec, R w) {
   jacobi_tile<R, true>(g, gp, nx, ny, tiles_x, ntiles, vec, w);
 }
+// Adjoint step with its share of dL/dw: the tile of x_{t-1} is staged beside
+// g's (tiles of kJacDpTR rows, so two staged arrays leave room for as many
+// workgroups per CU as one array of kJacTR rows). Threads past the grid's
+// last column take part in the block sum.
+constexpr int kJacDpTR = 4;
+template <class R>
+__global__ __launch_bounds__(kJacTW) void adj_jacobi2d5_dp(const R* __restrict__ x,
+                                                           const R* __restrict__ g,
+                                                           R* __restrict__ gp, int nx, int ny,
+                                                           int tiles_x, int ntiles, int vec, R w,
+                                                           DpOut dp) {
+  using G = Tile2<R, kJacTW, kJacDpTR>;
+  __shared__ R sg[G::LR * G::LW];
+  __shared__ R sx[G::LR * G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;  // the whole block
+  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacDpTR;
+  stage_rows<R, kJacTW, G::LR, G::LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
+  stage_rows<R, kJacTW, G::LR, G::LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
+  __syncthreads();
+  const int i = i0 + (int)threadIdx.x;
+  const int cx = G::V + (int)threadIdx.x;
+  const bool avg = jacobi_all_avg<true>(i0, i0 + kJacTW - 1, j0, j0 + kJacDpTR - 1, nx, ny);
+  double a0 = 0.0;
+  if (i < nx) {
+#pragma unroll
+    for (int r = 0; r < kJacDpTR; ++r) {
+      const int j = j0 + r;
+      if (j >= ny) break;
+      const int q = (r + 1) * G::LW + cx;
+      gp[j * nx + i] = avg ? jacobi_adj_inner_at<R, G::LW>(sg, q, w)
+                           : jacobi_adj_at<R, G::LW>(sg, q, i, j, nx, ny, w);
+      if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
+        R sum = sx[q];
+        sum += sx[q - 1];
+        sum += sx[q + 1];
+        sum += sx[q - G::LW];
+        sum += sx[q + G::LW];
+        a0 += (double)sg[q] * (double)sum;
+      }
+    }
+  }
+  dp_commit(dp, b, a0, 0.0);
+}
 template <class R>
 __global__ __launch_bounds__(kX2Threads) void fwd_jacobi2d5_x2(const R* __restrict__ x,
                                                                R* __restrict__ y, int nx, int ny,
@@ -338,13 +431,14 @@ __global__ __launch_bounds__(kX2Threads) void adj_jacobi2d5_x2(const R* __restri
 constexpr int kAcTX = 64, kAcTY = 8, kAcZC = 32;
 
 struct AcTile {
-  int i, ja, jb, by, bx, z0, z1;
+  int b, i, ja, jb, by, bx, z0, z1;
 };
 
 __device__ inline bool ac_tile(int nx, int ny, int nz, int tiles_x, int tiles_y, int ntiles,
                                AcTile* t) {
   int b = xcd_tile(ntiles);
   if (b >= ntiles) return false;
+  t->b = b;
   t->bx = b % tiles_x;
   b /= tiles_x;
   t->by = b % tiles_y;
@@ -543,18 +637,23 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_x2(const R* __restr
 // fused), dx'[c]/dx[m] = D for each in-grid face neighbour c of m. The
 // Laplacian with zero ghosts is symmetric, so the gather reads g at m's own
 // neighbours:  g'[m] = (k0 - k1*x[m]^2) * g[m] + D * sum_nbr g.
-template <class R>
+// DP: also this step's share of dL/dD and dL/dC (see DpOut), from x_{t-1}
+// staged the same way as g (its plane in LDS, the planes below and above in
+// registers).
+template <class R, bool DP>
 __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict__ x,
                                                              const R* __restrict__ g,
                                                              R* __restrict__ gp, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
-                                                             int ntiles, R D, R k0, R k1) {
+                                                             int ntiles, R D, R k0, R k1,
+                                                             DpOut dp) {
   __shared__ R tile[kAcTY + 2][kAcTX + 2];
+  __shared__ R tilex[DP ? kAcTY + 2 : 1][DP ? kAcTX + 2 : 1];
   AcTile t;
-  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;
+  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;  // the whole block
   const int plane = nx * ny;
-  auto ld = [&](int k, int j, int i) -> R {
-    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? g[k * plane + j * nx + i]
+  auto ld = [&](const R* a, int k, int j, int i) -> R {
+    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? a[k * plane + j * nx + i]
                                                                       : R(0);
   };
   const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
@@ -562,18 +661,49 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   ac_halo_cell(tid, &hly, &hlx);
   const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
   const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
-  R belowA = ld(t.z0 - 1, t.ja, t.i), belowB = ld(t.z0 - 1, t.jb, t.i);
-  R curA = ld(t.z0, t.ja, t.i), curB = ld(t.z0, t.jb, t.i);
+  R belowA = ld(g, t.z0 - 1, t.ja, t.i), belowB = ld(g, t.z0 - 1, t.jb, t.i);
+  R curA = ld(g, t.z0, t.ja, t.i), curB = ld(g, t.z0, t.jb, t.i);
+  R xbelowA = R(0), xbelowB = R(0), xcurA = R(0), xcurB = R(0);
+  if (DP) {
+    xbelowA = ld(x, t.z0 - 1, t.ja, t.i);
+    xbelowB = ld(x, t.z0 - 1, t.jb, t.i);
+    xcurA = ld(x, t.z0, t.ja, t.i);
+    xcurB = ld(x, t.z0, t.jb, t.i);
+  }
+  double a0 = 0.0, a1 = 0.0;
   for (int k = t.z0; k < t.z1; ++k) {
-    const R aboveA = ld(k + 1, t.ja, t.i), aboveB = ld(k + 1, t.jb, t.i);
-    const R halo = hly >= 0 ? ld(k, hj, hi) : R(0);
-    const R xa = va ? x[k * plane + t.ja * nx + t.i] : R(0);
-    const R xb = vb ? x[k * plane + t.jb * nx + t.i] : R(0);
+    const R aboveA = ld(g, k + 1, t.ja, t.i), aboveB = ld(g, k + 1, t.jb, t.i);
+    const R halo = hly >= 0 ? ld(g, k, hj, hi) : R(0);
+    R xa, xb, xaboveA = R(0), xaboveB = R(0), xhalo = R(0);
+    if (DP) {
+      xa = xcurA;
+      xb = xcurB;
+      xaboveA = ld(x, k + 1, t.ja, t.i);
+      xaboveB = ld(x, k + 1, t.jb, t.i);
+      xhalo = hly >= 0 ? ld(x, k, hj, hi) : R(0);
+    } else {
+      xa = va ? x[k * plane + t.ja * nx + t.i] : R(0);
+      xb = vb ? x[k * plane + t.jb * nx + t.i] : R(0);
+    }
     __syncthreads();
     tile[ty + 1][tx + 1] = curA;
     tile[ty + 5][tx + 1] = curB;
     if (hly >= 0) tile[hly][hlx] = halo;
+    if (DP) {
+      tilex[ty + 1][tx + 1] = xcurA;
+      tilex[ty + 5][tx + 1] = xcurB;
+      if (hly >= 0) tilex[hly][hlx] = xhalo;
+    }
     __syncthreads();
+    // lap of x at row r of this thread (r = 1: A, r = 5: B), the forward's order
+    auto lapx = [&](int r, R xzm, R xzp, R a) {
+      R lap = tilex[ty + r][tx] + tilex[ty + r][tx + 2];
+      lap += tilex[ty + r - 1][tx + 1];
+      lap += tilex[ty + r + 1][tx + 1];
+      lap += xzm;
+      lap += xzp;
+      return lap - R(6) * a;
+    };
     if (va) {
       R s = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
       s += tile[ty][tx + 1];
@@ -581,6 +711,10 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
       s += belowA;
       s += aboveA;
       gp[k * plane + t.ja * nx + t.i] = (k0 - k1 * (xa * xa)) * curA + D * s;
+      if (DP) {
+        a0 += (double)curA * (double)lapx(1, xbelowA, xaboveA, xa);
+        a1 += (double)curA * (double)(-((xa * xa) * xa));
+      }
     }
     if (vb) {
       R s = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
@@ -589,11 +723,25 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
       s += belowB;
       s += aboveB;
       gp[k * plane + t.jb * nx + t.i] = (k0 - k1 * (xb * xb)) * curB + D * s;
+      if (DP) {
+        a0 += (double)curB * (double)lapx(5, xbelowB, xaboveB, xb);
+        a1 += (double)curB * (double)(-((xb * xb) * xb));
+      }
     }
     belowA = curA;
     belowB = curB;
     curA = aboveA;
     curB = aboveB;
+    if (DP) {
+      xbelowA = xcurA;
+      xbelowB = xcurB;
+      xcurA = xaboveA;
+      xcurB = xaboveB;
+    }
+  }
+  if (DP) {
+    __syncthreads();
+    dp_commit(dp, t.b, a0, a1);
   }
 }
 
@@ -630,67 +778,63 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
 // Adjoint (the operator is symmetric in x):
 //   g'[m] = g[m] + dt * sum_n (c_n*(K[m]+K[n]))*(g[n]-g[m])
 //   dK[m] += dt * sum_n (c_n*(x[n]-x[m]))*(g[m]-g[n])      (x = x_{t-1})
-// the second line being the coefficient-field gradient of step t, fused.
-template <class R, bool WANT_DK, int TR>
+// the second line being the coefficient-field gradient of step t, fused;
+// DP adds this step's share of dL/ddt (see DpOut), sum_m g[m] * acc[m] with
+// the forward's acc. Threads past the grid's last column take part in the
+// block sum.
+template <class R, bool WANT_DK, int TR, bool DP>
 __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
                                                         const R* __restrict__ K,
                                                         const R* __restrict__ g,
                                                         R* __restrict__ gp, R* __restrict__ dK,
                                                         int dk_first, int nx, int ny,
                                                         int tiles_x, int ntiles, int vec, R dt,
-                                                        R ca, R cd) {
+                                                        R ca, R cd, DpOut dp) {
+  constexpr bool XS = WANT_DK || DP;  // x_{t-1} staged
   using G = Tile2<R, kVdTW, TR>;
   constexpr int LW = G::LW;
   __shared__ R sg[G::LR * LW];
   __shared__ R sk[G::LR * LW];
-  __shared__ R sx[WANT_DK ? G::LR * LW : 1];
+  __shared__ R sx[XS ? G::LR * LW : 1];
   const int b = xcd_tile(ntiles);
-  if (b >= ntiles) return;
+  if (b >= ntiles) return;  // the whole block
   const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * TR;
   stage_rows<R, kVdTW, G::LR, LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
   stage_rows<R, kVdTW, G::LR, LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
-  if (WANT_DK) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
+  if (XS) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
   __syncthreads();
   const int i = i0 + (int)threadIdx.x;
-  if (i >= nx) return;
   const int cx = G::V + (int)threadIdx.x;
   const bool xin = i > 0 && i < nx - 1;
+  double a0 = 0.0;
+  if (i < nx) {
 #pragma unroll 2
-  for (int r = 0; r < TR; ++r) {
-    const int j = j0 + r;
-    if (j >= ny) break;
-    const int q = (r + 1) * LW + cx;
-    const R gc = sg[q], Kc = sk[q];
-    const R xc = WANT_DK ? sx[q] : R(0);
-    R ag = R(0), ak = R(0);
-    const bool inner = xin && j > 0 && j < ny - 1;
+    for (int r = 0; r < TR; ++r) {
+      const int j = j0 + r;
+      if (j >= ny) break;
+      const int q = (r + 1) * LW + cx;
+      const R gc = sg[q], Kc = sk[q];
+      const R xc = XS ? sx[q] : R(0);
+      R ag = R(0), ak = R(0), acc = R(0);
+      const bool inner = xin && j > 0 && j < ny - 1;
 #pragma unroll
-    for (int n = 0; n < 8; ++n) {
-      const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
-      if (!inner && (a < 0 || a >= nx || bb < 0 || bb >= ny)) continue;
-      const int m = q + kNbrDy[n] * LW + kNbrDx[n];
-      const R cn = n < 4 ? ca : cd;
-      const R gn = sg[m];
-      ag += (cn * (Kc + sk[m])) * (gn - gc);
-      if (WANT_DK) ak += (cn * (sx[m] - xc)) * (gc - gn);
+      for (int n = 0; n < 8; ++n) {
+        const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
+        if (!inner && (a < 0 || a >= nx || bb < 0 || bb >= ny)) continue;
+        const int m = q + kNbrDy[n] * LW + kNbrDx[n];
+        const R cn = n < 4 ? ca : cd;
+        const R gn = sg[m];
+        ag += (cn * (Kc + sk[m])) * (gn - gc);
+        if (WANT_DK) ak += (cn * (sx[m] - xc)) * (gc - gn);
+        if (DP) acc += (cn * (Kc + sk[m])) * (sx[m] - xc);
+      }
+      const int o = j * nx + i;
+      gp[o] = gc + dt * ag;
+      if (WANT_DK) dK[o] = (dk_first ? R(0) : dK[o]) + dt * ak;
+      if (DP) a0 += (double)gc * (double)acc;
     }
-    const int o = j * nx + i;
-    gp[o] = gc + dt * ag;
-    if (WANT_DK) dK[o] = (dk_first ? R(0) : dK[o]) + dt * ak;
   }
-}
-
-// --------------------------------------------------------------- loss, seed
-// Sum over the 256 threads of a block: a wave64 butterfly, then the four
-// wave sums in a fixed order. Valid in thread 0.
-__device__ inline double block_sum(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  __shared__ double wave_sum[kThreads / 64];
-  const int tid = threadIdx.y * kBX + threadIdx.x;
-  if ((tid & 63) == 0) wave_sum[tid >> 6] = v;
-  __syncthreads();
-  return ((wave_sum[0] + wave_sum[1]) + wave_sum[2]) + wave_sum[3];
+  if (DP) dp_commit(dp, b, a0, 0.0);
 }
 
 template <class R, int LOSS>
@@ -779,89 +923,15 @@ __global__ __launch_bounds__(kThreads) void limit_mask(const R* __restrict__ x,
 }
 
 // ------------------------------------------- gradients of the step constants
-// One adjoint step's share of dL/dp: the sum over points of g_t[c] times the
-// step's partial dF_c/dp at x_{t-1} (a constant read by every point of every
-// step is a multiply-read input whose gradient accumulates, Sec. II). The
-// partials are the sub-expressions the forward step forms, in its order:
-//   Jacobi               dF/dw  = (((x[c]+x[W])+x[E])+x[S])+x[N] on interior points
-//   Allen-Cahn           dF/dD  = lap,   dF/dC = -((x[c]*x[c])*x[c])
-//   variable coefficient dF/ddt = acc
-// Products and sums are in double. A fixed grid with a fixed point-to-thread
-// assignment adds each block's sums into its own slot, step after step in
-// the adjoint order t = T..1, so the result does not depend on the schedule.
-constexpr int kDpBlocks = 2048;
-
-// Block sums of two values, each over the 256 threads in a fixed order.
-__device__ inline void block_sum2(double& a, double& b) {
-  a = block_sum(a);
-  __syncthreads();  // block_sum's wave sums are reused
-  b = block_sum(b);
-}
-
-template <class R, int KIND>
-__global__ __launch_bounds__(kThreads) void dparam_step(const R* __restrict__ x,
-                                                        const R* __restrict__ K,
-                                                        const R* __restrict__ g,
-                                                        double* __restrict__ part, int first,
-                                                        int nx, int ny, int nz, R ca, R cd) {
-  const int tid = threadIdx.y * kBX + threadIdx.x;
-  const int64_t plane = (int64_t)nx * ny, n = plane * nz;
-  const int64_t stride = (int64_t)gridDim.x * kThreads;
-  double a0 = 0.0, a1 = 0.0;
-  for (int64_t q = (int64_t)blockIdx.x * kThreads + tid; q < n; q += stride) {
-    const int i = (int)(q % nx);
-    const int64_t r = q / nx;
-    const int j = (int)(r % ny), k = (int)(r / ny);
-    const double gq = (double)g[q];
-    if (KIND == ADST_JACOBI2D5) {
-      if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
-        R sum = x[q];
-        sum += x[q - 1];
-        sum += x[q + 1];
-        sum += x[q - nx];
-        sum += x[q + nx];
-        a0 += gq * (double)sum;
-      }
-    } else if (KIND == ADST_ALLENCAHN3D7) {
-      const R a = x[q];
-      R lap = (i > 0 ? x[q - 1] : R(0)) + (i < nx - 1 ? x[q + 1] : R(0));
-      lap += j > 0 ? x[q - nx] : R(0);
-      lap += j < ny - 1 ? x[q + nx] : R(0);
-      lap += k > 0 ? x[q - plane] : R(0);
-      lap += k < nz - 1 ? x[q + plane] : R(0);
-      lap = lap - R(6) * a;
-      a0 += gq * (double)lap;
-      a1 += gq * (double)(-((a * a) * a));
-    } else {  // ADST_VARDIFF2D9
-      const R xc = x[q], Kc = K[q];
-      R acc = R(0);
-#pragma unroll
-      for (int nn = 0; nn < 8; ++nn) {
-        const int ii = i + kNbrDx[nn], jj = j + kNbrDy[nn];
-        if (ii < 0 || ii >= nx || jj < 0 || jj >= ny) continue;
-        const int64_t m = q + (int64_t)kNbrDy[nn] * nx + kNbrDx[nn];
-        acc += ((nn < 4 ? ca : cd) * (Kc + K[m])) * (x[m] - xc);
-      }
-      a0 += gq * (double)acc;
-    }
-  }
-  block_sum2(a0, a1);
-  if (tid == 0) {
-    double* p0 = part + blockIdx.x;
-    double* p1 = part + kDpBlocks + blockIdx.x;
-    *p0 = first ? a0 : *p0 + a0;
-    *p1 = first ? a1 : *p1 + a1;
-  }
-}
-
-// dparams[k] = the sum of the kDpBlocks slots of constant k, in a fixed order.
+// dparams[k] = the sum of the nslots slots of constant k, in a fixed order.
 __global__ __launch_bounds__(kThreads) void dparam_finalize(const double* __restrict__ part,
+                                                            int nslots,
                                                             double* __restrict__ out) {
   const int tid = threadIdx.y * kBX + threadIdx.x;
   double a0 = 0.0, a1 = 0.0;
-  for (int i = tid; i < kDpBlocks; i += kThreads) {
+  for (int i = tid; i < nslots; i += kThreads) {
     a0 += part[i];
-    a1 += part[kDpBlocks + i];
+    a1 += part[nslots + i];
   }
   block_sum2(a0, a1);
   if (tid == 0) {
@@ -969,17 +1039,24 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
 
 template <class R>
 hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const void* gv,
-                     void* gpv, void* dKv, bool dk_first, hipStream_t st) {
+                     void* gpv, void* dKv, bool dk_first, double* dp_part, bool dp_first,
+                     hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
   const R* K = static_cast<const R*>(Kv);
   const R* g = static_cast<const R*>(gv);
   R* gp = static_cast<R*>(gpv);
   R* dK = static_cast<R*>(dKv);
+  const DpOut dp{dp_part, (int)dparam_slots(s), dp_first ? 1 : 0};
   switch (s.kind) {
     case ADST_JACOBI2D5: {
       const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
-      adj_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
-          g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
+      if (dp_part)
+        adj_jacobi2d5_dp<R><<<dim3(xcd_grid(tx * cdiv(s.ny, kJacDpTR))), dim3(kJacTW), 0, st>>>(
+            x, g, gp, s.nx, s.ny, tx, tx * cdiv(s.ny, kJacDpTR), vec_ok<R>(s.nx, g, x), R(s.p0),
+            dp);
+      else
+        adj_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+            g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
       break;
     }
     case ADST_ALLENCAHN3D7: {
@@ -987,22 +1064,35 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
       const R k0 = R(1) + D * R(-6), k1 = R(3) * C;
       const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
       const int nt = tx * ty * cdiv(s.nz, kAcZC);
-      adj_allencahn3d7<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-          x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1);
+      if (dp_part)
+        adj_allencahn3d7<R, true><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+            x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1, dp);
+      else
+        adj_allencahn3d7<R, false><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+            x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1, dp);
       break;
     }
     case ADST_VARDIFF2D9: {
       const int tx = cdiv(s.nx, kVdTW);
-      if (dK) {
-        const int nt = tx * cdiv(s.ny, kVdAdjTR);
-        adj_vardiff2d9<R, true, kVdAdjTR><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K, x),
-            R(s.p0), R(1) / R(3), R(1) / R(12));
+      const R dt = R(s.p0), ca = R(1) / R(3), cd = R(1) / R(12);
+      const int nt4 = tx * cdiv(s.ny, kVdAdjTR);
+      if (dK && dp_part) {
+        adj_vardiff2d9<R, true, kVdAdjTR, true><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
+            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt,
+            ca, cd, dp);
+      } else if (dK) {
+        adj_vardiff2d9<R, true, kVdAdjTR, false><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
+            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt,
+            ca, cd, dp);
+      } else if (dp_part) {
+        adj_vardiff2d9<R, false, kVdAdjTR, true><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
+            x, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt, ca, cd,
+            dp);
       } else {
         const int nt = tx * cdiv(s.ny, kVdTR);
-        adj_vardiff2d9<R, false, kVdTR><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-            nullptr, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K),
-            R(s.p0), R(1) / R(3), R(1) / R(12));
+        adj_vardiff2d9<R, false, kVdTR, false><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
+            nullptr, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K), dt, ca,
+            cd, dp);
       }
       break;
     }
@@ -1088,10 +1178,13 @@ hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev
 }
 
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
-                          void* g_prev, void* dK, bool dk_first, hipStream_t stream) {
+                          void* g_prev, void* dK, bool dk_first, double* dp_part, bool dp_first,
+                          hipStream_t stream) {
+  if (dp_part && (s.kind < ADST_JACOBI2D5 || s.kind > ADST_VARDIFF2D9 || !x))
+    return hipErrorInvalidValue;
   return s.dtype == ADST_F64
-             ? adjoint_t<double>(s, x, K, g_next, g_prev, dK, dk_first, stream)
-             : adjoint_t<float>(s, x, K, g_next, g_prev, dK, dk_first, stream);
+             ? adjoint_t<double>(s, x, K, g_next, g_prev, dK, dk_first, dp_part, dp_first, stream)
+             : adjoint_t<float>(s, x, K, g_next, g_prev, dK, dk_first, dp_part, dp_first, stream);
 }
 
 int32_t seed_partials(int64_t n) { return grid_for(n, 8 * kThreads, kMaxSeedPartials); }
@@ -1142,58 +1235,21 @@ hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, v
                              : limit_mask_t<float>(s, x, K, g, stream);
 }
 
-int64_t dparam_partial_bytes() { return int64_t(2) * kDpBlocks * sizeof(double); }
-
-hipError_t launch_dparam_step(const StepShape& s, const void* x, const void* K, const void* g,
-                              double* partials, bool first, hipStream_t stream) {
-  const dim3 grid(kDpBlocks), block(kBX, kBY);
-  const int f = first ? 1 : 0;
-  if (s.dtype == ADST_F64) {
-    const double* xd = static_cast<const double*>(x);
-    const double* Kd = static_cast<const double*>(K);
-    const double* gd = static_cast<const double*>(g);
-    switch (s.kind) {
-      case ADST_JACOBI2D5:
-        dparam_step<double, ADST_JACOBI2D5><<<grid, block, 0, stream>>>(
-            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 0.0, 0.0);
-        break;
-      case ADST_ALLENCAHN3D7:
-        dparam_step<double, ADST_ALLENCAHN3D7><<<grid, block, 0, stream>>>(
-            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 0.0, 0.0);
-        break;
-      case ADST_VARDIFF2D9:
-        dparam_step<double, ADST_VARDIFF2D9><<<grid, block, 0, stream>>>(
-            xd, Kd, gd, partials, f, s.nx, s.ny, s.nz, 1.0 / 3.0, 1.0 / 12.0);
-        break;
-      default:
-        return hipErrorInvalidValue;
-    }
-  } else {
-    const float* xf = static_cast<const float*>(x);
-    const float* Kf = static_cast<const float*>(K);
-    const float* gf = static_cast<const float*>(g);
-    switch (s.kind) {
-      case ADST_JACOBI2D5:
-        dparam_step<float, ADST_JACOBI2D5><<<grid, block, 0, stream>>>(
-            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 0.f, 0.f);
-        break;
-      case ADST_ALLENCAHN3D7:
-        dparam_step<float, ADST_ALLENCAHN3D7><<<grid, block, 0, stream>>>(
-            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 0.f, 0.f);
-        break;
-      case ADST_VARDIFF2D9:
-        dparam_step<float, ADST_VARDIFF2D9><<<grid, block, 0, stream>>>(
-            xf, Kf, gf, partials, f, s.nx, s.ny, s.nz, 1.f / 3.f, 1.f / 12.f);
-        break;
-      default:
-        return hipErrorInvalidValue;
-    }
+int64_t dparam_slots(const StepShape& s) {
+  switch (s.kind) {
+    case ADST_JACOBI2D5: return int64_t(cdiv(s.nx, kJacTW)) * cdiv(s.ny, kJacDpTR);
+    case ADST_ALLENCAHN3D7:
+      return int64_t(cdiv(s.nx, kAcTX)) * cdiv(s.ny, kAcTY) * cdiv(s.nz, kAcZC);
+    case ADST_VARDIFF2D9: return int64_t(cdiv(s.nx, kVdTW)) * cdiv(s.ny, kVdAdjTR);
+    default: return 0;
   }
-  return hipGetLastError();
 }
 
-hipError_t launch_dparam_finalize(const double* partials, double* dparams, hipStream_t stream) {
-  dparam_finalize<<<dim3(1), dim3(kBX, kBY), 0, stream>>>(partials, dparams);
+int64_t dparam_partial_bytes(const StepShape& s) { return 2 * dparam_slots(s) * int64_t(sizeof(double)); }
+
+hipError_t launch_dparam_finalize(const StepShape& s, const double* partials, double* dparams,
+                                  hipStream_t stream) {
+  dparam_finalize<<<dim3(1), dim3(kBX, kBY), 0, stream>>>(partials, (int)dparam_slots(s), dparams);
   return hipGetLastError();
 }
 

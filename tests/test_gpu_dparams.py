@@ -83,7 +83,8 @@ def test_dparams_match_oracle(kind, dtype, shape, T, loss, dK, slots):
 
 @pytest.mark.parametrize("kind,dtype,shape,T,loss,dK", [
     (J, F64, (90, 130), 15, HALF_SQ, False), (AC, F64, (20, 30, 70), 13, DOT_W, False),
-    (VD, F32, (100, 130), 17, DIFF, True)])
+    (AC, F32, (70, 20, 30), 7, HALF_SQ, False), (VD, F32, (100, 130), 17, DIFF, True),
+    (VD, F64, (70, 600), 9, DOT_W, False)])
 def test_dparams_bitwise_across_schedules(kind, dtype, shape, T, loss, dK):
     say(f"dparams schedules kind={kind} shape={shape} T={T}")
     inp = inputs(kind, dtype, shape, 2)
