@@ -17,6 +17,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "adst.h"
 #include "kernels.h"
 
@@ -766,13 +768,58 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
   const int i = i0 + (int)threadIdx.x;
   if (i >= nx) return;
   const int cx = G::V + (int)threadIdx.x;
-#pragma unroll 4
-  for (int r = 0; r < kVdTR; ++r) {
-    const int j = j0 + r;
-    if (j >= ny) break;
-    const R v = vardiff_fwd_at<R, G::LW>(sx, sk, (r + 1) * G::LW + cx, i, j, nx, ny, dt, ca, cd);
-    y[j * nx + i] = LIM ? limited(v, lim) : v;
-  }
+  // A 3 x 3 window of x and K slides down the thread's column: each row
+  // enters once (three LDS reads of each array) and serves three outputs.
+  // Window rows 0, 1, 2 are grid rows j-1, j, j+1; columns i-1, i, i+1. The
+  // neighbours are visited in the forward's order (kNbrDx, kNbrDy).
+  R xw[3][3], kw[3][3];
+  auto enter = [&](int slot, int lr) {
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      xw[slot][c] = sx[lr * G::LW + cx - 1 + c];
+      kw[slot][c] = sk[lr * G::LW + cx - 1 + c];
+    }
+  };
+  enter(0, 0);
+  enter(1, 1);
+  // tiles whose points all have eight in-grid neighbours skip the bounds
+  // tests (a workgroup-uniform branch)
+  const bool all_in = i0 >= 1 && i0 + kVdTW <= nx - 1 && j0 >= 1 && j0 + kVdTR <= ny - 1;
+  auto rows = [&](auto all_in_t) {
+    constexpr bool ALL_IN = decltype(all_in_t)::value;
+    const bool xin = i > 0 && i < nx - 1;
+#pragma unroll
+    for (int r = 0; r < kVdTR; ++r) {
+      const int j = j0 + r;
+      if (!ALL_IN && j >= ny) break;
+      enter(2, r + 2);
+      const R xc = xw[1][1], Kc = kw[1][1];
+      R acc = R(0);
+      const bool inner = ALL_IN || (xin && j > 0 && j < ny - 1);
+#pragma unroll
+      for (int n = 0; n < 8; ++n) {
+        if (!ALL_IN && !inner) {
+          const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
+          if (a < 0 || a >= nx || bb < 0 || bb >= ny) continue;
+        }
+        const int wr = 1 + kNbrDy[n], wc = 1 + kNbrDx[n];
+        acc += ((n < 4 ? ca : cd) * (Kc + kw[wr][wc])) * (xw[wr][wc] - xc);
+      }
+      const R v = xc + dt * acc;
+      y[j * nx + i] = LIM ? limited(v, lim) : v;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        xw[0][c] = xw[1][c];
+        kw[0][c] = kw[1][c];
+        xw[1][c] = xw[2][c];
+        kw[1][c] = kw[2][c];
+      }
+    }
+  };
+  if (all_in)
+    rows(std::true_type{});
+  else
+    rows(std::false_type{});
 }
 
 // Adjoint (the operator is symmetric in x):
@@ -808,31 +855,67 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   const bool xin = i > 0 && i < nx - 1;
   double a0 = 0.0;
   if (i < nx) {
-#pragma unroll 2
+    // 3 x 3 windows of g, K (and x) slide down the thread's column, as in
+    // the forward: rows j-1, j, j+1, columns i-1, i, i+1.
+    R gw[3][3], kw[3][3], xw[XS ? 3 : 1][3];
+    auto enter = [&](int slot, int lr) {
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        gw[slot][c] = sg[lr * LW + cx - 1 + c];
+        kw[slot][c] = sk[lr * LW + cx - 1 + c];
+        if (XS) xw[XS ? slot : 0][c] = sx[lr * LW + cx - 1 + c];
+      }
+    };
+    enter(0, 0);
+    enter(1, 1);
+    const bool all_in = i0 >= 1 && i0 + kVdTW <= nx - 1 && j0 >= 1 && j0 + TR <= ny - 1;
+    auto rows = [&](auto all_in_t) {
+    constexpr bool ALL_IN = decltype(all_in_t)::value;
+    // rolled with both dK and the constants' sums, to keep four waves per SIMD
+    constexpr int kRowUnroll = (WANT_DK && DP) ? 1 : TR;
+#pragma unroll kRowUnroll
     for (int r = 0; r < TR; ++r) {
       const int j = j0 + r;
-      if (j >= ny) break;
-      const int q = (r + 1) * LW + cx;
-      const R gc = sg[q], Kc = sk[q];
-      const R xc = XS ? sx[q] : R(0);
+      if (!ALL_IN && j >= ny) break;
+      enter(2, r + 2);
+      const R gc = gw[1][1], Kc = kw[1][1];
+      const R xc = XS ? xw[XS ? 1 : 0][1] : R(0);
       R ag = R(0), ak = R(0), acc = R(0);
-      const bool inner = xin && j > 0 && j < ny - 1;
+      const bool inner = ALL_IN || (xin && j > 0 && j < ny - 1);
 #pragma unroll
       for (int n = 0; n < 8; ++n) {
-        const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
-        if (!inner && (a < 0 || a >= nx || bb < 0 || bb >= ny)) continue;
-        const int m = q + kNbrDy[n] * LW + kNbrDx[n];
+        if (!ALL_IN && !inner) {
+          const int a = i + kNbrDx[n], bb = j + kNbrDy[n];
+          if (a < 0 || a >= nx || bb < 0 || bb >= ny) continue;
+        }
+        const int wr = 1 + kNbrDy[n], wc = 1 + kNbrDx[n];
         const R cn = n < 4 ? ca : cd;
-        const R gn = sg[m];
-        ag += (cn * (Kc + sk[m])) * (gn - gc);
-        if (WANT_DK) ak += (cn * (sx[m] - xc)) * (gc - gn);
-        if (DP) acc += (cn * (Kc + sk[m])) * (sx[m] - xc);
+        const R gn = gw[wr][wc];
+        ag += (cn * (Kc + kw[wr][wc])) * (gn - gc);
+        if (WANT_DK) ak += (cn * (xw[XS ? wr : 0][wc] - xc)) * (gc - gn);
+        if (DP) acc += (cn * (Kc + kw[wr][wc])) * (xw[XS ? wr : 0][wc] - xc);
       }
       const int o = j * nx + i;
       gp[o] = gc + dt * ag;
       if (WANT_DK) dK[o] = (dk_first ? R(0) : dK[o]) + dt * ak;
       if (DP) a0 += (double)gc * (double)acc;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        gw[0][c] = gw[1][c];
+        kw[0][c] = kw[1][c];
+        gw[1][c] = gw[2][c];
+        kw[1][c] = kw[2][c];
+        if (XS) {
+          xw[0][c] = xw[XS ? 1 : 0][c];
+          xw[XS ? 1 : 0][c] = xw[XS ? 2 : 0][c];
+        }
+      }
     }
+    };
+    if (all_in)
+      rows(std::true_type{});
+    else
+      rows(std::false_type{});
   }
   if (DP) dp_commit(dp, b, a0, 0.0);
 }
