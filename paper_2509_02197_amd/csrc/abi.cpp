@@ -524,7 +524,9 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
       }
       case ADST_OP_ADJ: {
         const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
-        if (c.shape.limit) {  // the branch each point took at step t
+        if (c.shape.limit && !adjoint_applies_limit(c.shape, dparams != nullptr)) {
+          // the branch each point took at step t (otherwise applied by the
+          // adjoint launch itself)
           e = launch_limit_mask(c.shape, xs, coeff, gcur, stream);
           if (e != hipSuccess) return hip_fail(e, "kernel launch");
         }

@@ -98,47 +98,72 @@ struct MarchGrid {
   int ns, nedge, ce, ci, pe, pi;
 };
 
+// This workgroup's strip and chunk of rows [r0, r1); false when the
+// workgroup has no work (the grid is rounded up to whole XCD shares).
+__device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* chunk, int* r0,
+                                  int* r1) {
+  const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
+  int nch, mid;
+  if (slot < g.pe) {
+    const int t = xcd * g.pe + slot;
+    if (t >= g.nedge * g.ce) return false;
+    *strip = (t / g.ce == 0) ? 0 : g.ns - 1;
+    *chunk = t % g.ce;
+    nch = g.ce;
+    mid = kEdgeRows;
+  } else {
+    const int t = xcd * g.pi + (slot - g.pe);
+    if (t >= (g.ns - g.nedge) * g.ci) return false;
+    *strip = 1 + t / g.ci;
+    *chunk = t % g.ci;
+    nch = g.ci;
+    mid = kRows;
+  }
+  // kEndRows at each end of the strip, mid rows between
+  const int c = *chunk;
+  if (nch == 1) {
+    *r0 = 0;
+    *r1 = ny;
+  } else if (c == 0) {
+    *r0 = 0;
+    *r1 = kEndRows;
+  } else if (c == nch - 1) {
+    *r0 = ny - kEndRows;
+    *r1 = ny;
+  } else {
+    *r0 = kEndRows + (c - 1) * mid;
+    *r1 = min(*r0 + mid, ny - kEndRows);
+  }
+  return true;
+}
+
+// The work list for strips of ow output columns; false if it is too long.
+inline bool make_grid(int nx, int ny, int ow, MarchGrid* g, int64_t* blocks) {
+  g->ns = (nx + ow - 1) / ow;
+  g->nedge = g->ns >= 2 ? 2 : 1;
+  auto chunks = [&](int mid) {
+    return ny > 2 * kEndRows ? 2 + (ny - 2 * kEndRows + mid - 1) / mid : 1;
+  };
+  g->ce = chunks(kEdgeRows);
+  g->ci = chunks(kRows);
+  const int64_t E = int64_t(g->nedge) * g->ce, I = int64_t(g->ns - g->nedge) * g->ci;
+  g->pe = (int)((E + kXcds - 1) / kXcds);
+  g->pi = (int)((I + kXcds - 1) / kXcds);
+  *blocks = int64_t(kXcds) * (g->pe + g->pi);
+  return *blocks > 0 && *blocks <= INT32_MAX;
+}
+
 template <class R, int K, bool ADJ, bool VEC>
 __global__ __launch_bounds__(kLanes) void jacobi_march(const R* __restrict__ x, R* __restrict__ y,
                                                        int nx, int ny, MarchGrid g, R w) {
   using G = Geom<R, K>;
   constexpr int V = G::V, H = G::H, OW = G::OW, P = kAhead, U = kUnroll;
   typedef R vec_t __attribute__((ext_vector_type(V)));
-  const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
-  int strip, chunk, nch, mid;
-  if (slot < g.pe) {
-    const int t = xcd * g.pe + slot;
-    if (t >= g.nedge * g.ce) return;
-    strip = (t / g.ce == 0) ? 0 : g.ns - 1;
-    chunk = t % g.ce;
-    nch = g.ce;
-    mid = kEdgeRows;
-  } else {
-    const int t = xcd * g.pi + (slot - g.pe);
-    if (t >= (g.ns - g.nedge) * g.ci) return;
-    strip = 1 + t / g.ci;
-    chunk = t % g.ci;
-    nch = g.ci;
-    mid = kRows;
-  }
+  int strip, chunk, r0, r1;
+  if (!march_item(g, ny, &strip, &chunk, &r0, &r1)) return;
   const int lane = threadIdx.x;
   const int s0 = strip * OW;
   const int c0 = s0 - H + lane * V;  // first column of this lane
-  // rows [r0, r1): kEndRows at each end of the strip, mid rows between
-  int r0, r1;
-  if (nch == 1) {
-    r0 = 0;
-    r1 = ny;
-  } else if (chunk == 0) {
-    r0 = 0;
-    r1 = kEndRows;
-  } else if (chunk == nch - 1) {
-    r0 = ny - kEndRows;
-    r1 = ny;
-  } else {
-    r0 = kEndRows + (chunk - 1) * mid;
-    r1 = min(r0 + mid, ny - kEndRows);
-  }
   const int nit = (r1 - r0) + 2 * K;  // input rows through the pipeline
   const int lo_need = max(r0 - K, 0), hi_need = min(r1 + K - 1, ny - 1);
 
@@ -404,18 +429,8 @@ hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
   using G = Geom<R, K>;
   if (ADJ && s.nx <= G::V) return hipErrorInvalidValue;  // a lane would hold both ring columns
   MarchGrid g;
-  g.ns = (s.nx + G::OW - 1) / G::OW;
-  g.nedge = g.ns >= 2 ? 2 : 1;
-  auto chunks = [&](int mid) {
-    return s.ny > 2 * kEndRows ? 2 + (s.ny - 2 * kEndRows + mid - 1) / mid : 1;
-  };
-  g.ce = chunks(kEdgeRows);
-  g.ci = chunks(kRows);
-  const int64_t E = int64_t(g.nedge) * g.ce, I = int64_t(g.ns - g.nedge) * g.ci;
-  g.pe = (int)((E + kXcds - 1) / kXcds);
-  g.pi = (int)((I + kXcds - 1) / kXcds);
-  const int64_t blocks = int64_t(kXcds) * (g.pe + g.pi);
-  if (blocks <= 0 || blocks > INT32_MAX) return hipErrorInvalidValue;
+  int64_t blocks;
+  if (!make_grid(s.nx, s.ny, G::OW, &g, &blocks)) return hipErrorInvalidValue;
   const bool vec = s.nx % G::V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(y) & 15u) == 0;
   if (vec)
@@ -424,6 +439,207 @@ hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
   else
     jacobi_march<R, K, ADJ, false><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
         x, y, s.nx, s.ny, g, R(s.p0));
+  return hipGetLastError();
+}
+
+// ------------------------------------------- the limiter's adjoint, fused
+// One Jacobi adjoint step under the limiter: g_t is masked by the branch
+// each point took at step t (its unlimited value re-evaluated from x_{t-1}
+// with the forward's expression; 0 where it left [lo, hi]) and the masked g
+// is transposed with the single-step adjoint's expressions, in one pass
+// that reads x and g once and writes g' once. A wave marches down a strip
+// carrying three rows of x, the g rows waiting for their mask and three
+// masked g rows: when input row p arrives, row p-1 is masked (its x
+// neighbourhood is complete) and row p-2 transposed. The mask reads x one
+// column beyond the masked g, so strips overlap by V >= 2 columns.
+template <class R, bool VEC>
+__global__ __launch_bounds__(kLanes) void jacobi_lim_adjoint(const R* __restrict__ x,
+                                                             const R* __restrict__ g,
+                                                             R* __restrict__ gp, int nx, int ny,
+                                                             MarchGrid grid, R w, R lo, R hi) {
+  // six rows of each array in flight: the pass is lighter than the n-step
+  // march and registers allow it
+  constexpr int V = 16 / sizeof(R), H = V, OW = kLanes * V - 2 * H, P = 6, U = kUnroll;
+  static_assert(H >= 2, "the mask reaches two columns beyond an output");
+  static_assert(U % P == 0, "register slots must stay static");
+  typedef R vec_t __attribute__((ext_vector_type(V)));
+  int strip, chunk, r0, r1;
+  if (!march_item(grid, ny, &strip, &chunk, &r0, &r1)) return;
+  const int lane = threadIdx.x;
+  const int s0 = strip * OW;
+  const int c0 = s0 - H + lane * V;
+  const int nit = (r1 - r0) + 4;  // input rows r0-2 .. r1+1
+  const int lo_need = max(r0 - 2, 0), hi_need = min(r1 + 1, ny - 1);
+  auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
+  bool cok[V], cI[V], cW[V], cE[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    const int c = c0 + e;
+    cok[e] = c >= 0 && c < nx;
+    cI[e] = cin(c);
+    cW[e] = cin(c - 1);
+    cE[e] = cin(c + 1);
+  }
+  const bool strip_in = s0 - H >= 2 && s0 - H + kLanes * V <= nx - 2;
+  const bool st_lane = lane * V >= H && lane * V < H + OW;
+  auto load = [&](const R* a, int row, R* out) {
+    const int rr = min(max(row, lo_need), hi_need);
+    const R* src = a + (int64_t)rr * nx;
+    if constexpr (VEC) {
+      const int cc = min(max(c0, 0), nx - V);
+      const vec_t t = *reinterpret_cast<const vec_t*>(src + cc);
+#pragma unroll
+      for (int e = 0; e < V; ++e) out[e] = t[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) out[e] = src[min(max(c0 + e, 0), nx - 1)];
+    }
+  };
+  enum { kFast = 0, kGeneral = 2 };
+  auto march = [&](auto dir_t, auto mid_t) {
+    constexpr int DIR = decltype(dir_t)::value;
+    const int ifirst = DIR > 0 ? r0 - 2 : r1 + 1;  // row of input index 0
+    // slot p mod 3 holds pipeline index p (row ifirst + DIR*p)
+    R xw[3][V], gr[3][V], mg[3][V];
+    R px[P][V], pg[P][V];
+#pragma unroll
+    for (int s3 = 0; s3 < 3; ++s3)
+#pragma unroll
+      for (int e = 0; e < V; ++e) xw[s3][e] = gr[s3][e] = mg[s3][e] = R(0);
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      load(x, ifirst + DIR * u, px[u]);
+      load(g, ifirst + DIR * u, pg[u]);
+    }
+    auto block = [&](int base, auto mode_t) {
+      constexpr int MODE = decltype(mode_t)::value;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int rr = base + u;
+        {  // input row rr enters; the rows P ahead are requested
+          const int row = ifirst + DIR * rr;
+          const bool rok = row >= 0 && row < ny;
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const bool ok = MODE == kFast || (rok && cok[e]);
+            xw[u % 3][e] = ok ? px[u % P][e] : R(0);
+            gr[u % 3][e] = ok ? pg[u % P][e] : R(0);
+          }
+          load(x, row + DIR * P, px[u % P]);
+          load(g, row + DIR * P, pg[u % P]);
+        }
+        {  // mask row index rr-1 from x rows rr-2 .. rr
+          const int m = ifirst + DIR * (rr - 1);
+          constexpr int off = 6;
+          const int sOld = (u - 2 + off) % 3, sc = (u - 1 + off) % 3, sNew = u % 3;
+          const R* a = xw[sc];
+          const R* S = xw[DIR > 0 ? sOld : sNew];
+          const R* N = xw[DIR > 0 ? sNew : sOld];
+          const R wl = from_prev(a[V - 1]), er = from_next(a[0]);
+          const bool rm = m >= 1 && m <= ny - 2;
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
+            const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
+            const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
+            const R yv = (MODE == kFast || (cI[e] && rm)) ? f : a[e];
+            mg[sc][e] = (yv < lo || yv > hi) ? R(0) : gr[sc][e];
+          }
+        }
+        {  // transpose row index rr-2 from masked rows rr-3 .. rr-1
+          const int j = ifirst + DIR * (rr - 2);
+          constexpr int off = 6;
+          const int sOld = (u - 3 + off) % 3, sc = (u - 2 + off) % 3, sNew = (u - 1 + off) % 3;
+          const R* a = mg[sc];
+          const R* S = mg[DIR > 0 ? sOld : sNew];
+          const R* N = mg[DIR > 0 ? sNew : sOld];
+          const R wl = from_prev(a[V - 1]), er = from_next(a[0]);
+          const bool rj = j >= 1 && j <= ny - 2, rS = j >= 2 && j <= ny - 1,
+                     rN = j >= 0 && j <= ny - 3;
+          R o[V];
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
+            const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
+            if constexpr (MODE == kFast) {
+              o[e] = w * (a[e] + (((Wn + En) + S[e]) + N[e]));
+            } else {
+              R sum = (cW[e] && rj) ? Wn : R(0);
+              sum += (cE[e] && rj) ? En : R(0);
+              sum += (cI[e] && rS) ? S[e] : R(0);
+              sum += (cI[e] && rN) ? N[e] : R(0);
+              o[e] = (cI[e] && rj) ? w * (a[e] + sum) : a[e] + w * sum;
+            }
+          }
+          if (j >= r0 && j < r1 && st_lane) {
+            R* dst = gp + (int64_t)j * nx;
+            if constexpr (VEC) {
+              if (c0 + V <= nx) {
+                vec_t t;
+#pragma unroll
+                for (int e = 0; e < V; ++e) t[e] = o[e];
+                *reinterpret_cast<vec_t*>(dst + c0) = t;
+              }
+            } else {
+#pragma unroll
+              for (int e = 0; e < V; ++e)
+                if (c0 + e < nx) dst[c0 + e] = o[e];
+            }
+          }
+        }
+      }
+    };
+    // A block of U input rows touches rows ifirst + DIR*[base - 4, base + U - 1];
+    // blocks [fa, fb) have all of them in [2, ny - 3].
+    constexpr int R4 = 4;
+    int fa, fb;
+    if (DIR > 0) {
+      fa = 2 + R4 - ifirst;
+      fb = ny - 1 - ifirst - U;
+    } else {
+      fa = ifirst + R4 - (ny - 3);
+      fb = ifirst - U;
+    }
+    fa = ((max(fa, 0) + U - 1) / U) * U;
+    using General = std::integral_constant<int, kGeneral>;
+    int base = 0;
+    for (; base < nit && base < fa; base += U) block(base, General{});
+    for (; base < nit && base < fb; base += U) block(base, mid_t);
+    for (; base < nit; base += U) block(base, General{});
+  };
+  using Up = std::integral_constant<int, 1>;
+  using Down = std::integral_constant<int, -1>;
+  using Fast = std::integral_constant<int, kFast>;
+  using General = std::integral_constant<int, kGeneral>;
+  if (strip_in) {
+    if (chunk & 1)
+      march(Down{}, Fast{});
+    else
+      march(Up{}, Fast{});
+  } else {
+    if (chunk & 1)
+      march(Down{}, General{});
+    else
+      march(Up{}, General{});
+  }
+}
+
+template <class R>
+hipError_t lim_adjoint_launch(const StepShape& s, const R* x, const R* g, R* gp,
+                              hipStream_t st) {
+  constexpr int V = 16 / sizeof(R), OW = kLanes * V - 2 * V;
+  MarchGrid grid;
+  int64_t blocks;
+  if (!make_grid(s.nx, s.ny, OW, &grid, &blocks)) return hipErrorInvalidValue;
+  const bool vec = s.nx % V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(g) & 15u) == 0 &&
+                   (reinterpret_cast<uintptr_t>(gp) & 15u) == 0;
+  if (vec)
+    jacobi_lim_adjoint<R, true><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
+        x, g, gp, s.nx, s.ny, grid, R(s.p0), R(s.lo), R(s.hi));
+  else
+    jacobi_lim_adjoint<R, false><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
+        x, g, gp, s.nx, s.ny, grid, R(s.p0), R(s.lo), R(s.hi));
   return hipGetLastError();
 }
 
@@ -441,6 +657,17 @@ hipError_t march_n(const StepShape& s, const void* xv, void* yv, int n, hipStrea
 }
 
 }  // namespace
+
+hipError_t launch_jacobi_lim_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
+                                     hipStream_t stream) {
+  if (s.kind != ADST_JACOBI2D5 || !s.limit || !x) return hipErrorInvalidValue;
+  if (s.dtype == ADST_F64)
+    return lim_adjoint_launch<double>(s, static_cast<const double*>(x),
+                                      static_cast<const double*>(g), static_cast<double*>(gp),
+                                      stream);
+  return lim_adjoint_launch<float>(s, static_cast<const float*>(x), static_cast<const float*>(g),
+                                   static_cast<float*>(gp), stream);
+}
 
 hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32_t n, bool adjoint,
                                hipStream_t stream) {

@@ -42,6 +42,12 @@ hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev
 hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32_t n, bool adjoint,
                                hipStream_t stream);
 
+// Jacobi under the limiter: one adjoint step with the branch mask of step t
+// (from x = x_{t-1}) applied on the fly, g_prev = J_t^T (mask_t * g_next),
+// in one pass (jacobi_march.hip).
+hipError_t launch_jacobi_lim_adjoint(const StepShape& s, const void* x, const void* g_next,
+                                     void* g_prev, hipStream_t stream);
+
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
 // reads no state and neither dK nor the constants' gradients are asked for).
 // dK (nullable) is accumulated: dK = (dk_first ? 0 : dK) + contribution of
@@ -52,6 +58,10 @@ hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
                           void* g_prev, void* dK, bool dk_first, double* dp_part, bool dp_first,
                           hipStream_t stream);
+
+// With the limiter on, whether launch_adjoint applies the branch mask itself
+// (reading x = x_{t-1}); otherwise launch_limit_mask must run first.
+bool adjoint_applies_limit(const StepShape& s, bool dparams);
 
 // Number of per-block loss partials launch_seed writes for n points.
 int32_t seed_partials(int64_t n);

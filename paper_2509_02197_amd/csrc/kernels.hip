@@ -1260,11 +1260,17 @@ hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev
   return launch_jacobi_march(s, g_next, g_prev, n, true, stream);
 }
 
+bool adjoint_applies_limit(const StepShape& s, bool dparams) {
+  return s.limit && s.kind == ADST_JACOBI2D5 && !dparams;
+}
+
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
                           void* g_prev, void* dK, bool dk_first, double* dp_part, bool dp_first,
                           hipStream_t stream) {
   if (dp_part && (s.kind < ADST_JACOBI2D5 || s.kind > ADST_VARDIFF2D9 || !x))
     return hipErrorInvalidValue;
+  if (adjoint_applies_limit(s, dp_part != nullptr))
+    return launch_jacobi_lim_adjoint(s, x, g_next, g_prev, stream);
   return s.dtype == ADST_F64
              ? adjoint_t<double>(s, x, K, g_next, g_prev, dK, dk_first, dp_part, dp_first, stream)
              : adjoint_t<float>(s, x, K, g_next, g_prev, dK, dk_first, dp_part, dp_first, stream);
