@@ -112,3 +112,42 @@ def test_infinite_bounds_give_the_unlimited_bits(kind, dtype, shape, T, loss):
     a = gpu_vjp(kind, inp, T, loss)
     b = gpu_vjp(kind, inp, T, loss, lim=(-np.inf, np.inf))
     assert np.array_equal(a["xT"], b["xT"]) and np.array_equal(a["dx0"], b["dx0"])
+
+
+# The Jacobi adjoint under the limiter alone masks and transposes in one
+# register-marching pass; asking for the constants' gradients as well takes
+# the separate mask pass and the tiled adjoint. Both must give the same
+# dx0 bits. Shapes put the column strips (124 output columns in fp64, 248
+# in fp32), the row chunks and the element path (odd widths) against the
+# ring, plus grids narrower than a strip and a few rows tall.
+FUSED_LIM_SHAPES = [
+    (F64, (50, 124)), (F64, (49, 125)), (F64, (97, 248)), (F64, (3, 300)), (F64, (300, 3)),
+    (F64, (5, 4)), (F64, (61, 351)), (F32, (50, 248)), (F32, (13, 249)), (F32, (100, 497)),
+    (F32, (7, 5)),
+]
+
+
+@pytest.mark.parametrize("dtype,shape", FUSED_LIM_SHAPES)
+def test_fused_limiter_adjoint_matches_two_pass(dtype, shape):
+    say(f"fused limiter adjoint dtype={dtype} shape={shape}")
+    inp = inputs(J, dtype, shape, 5)
+    T, loss = 6, DOT_W
+    a = gpu_vjp(J, inp, T, loss, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL, lim=LIM[J])
+    b = gpu_vjp(J, inp, T, loss, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL, lim=LIM[J],
+                want_dparams=True)
+    assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
+    ref = oracle.vjp(J, inp["x0"], steps=T, loss=loss, aux=inp["aux"], lim=LIM[J])
+    assert rel(a["dx0"], ref[0]) <= TOL[dtype]
+
+
+def test_fused_limiter_adjoint_full_grid():
+    """4096^2 f64, the benchmark's limiter leg: the one-pass masked adjoint
+    and the two-pass one give the same bits."""
+    say("fused limiter adjoint 4096x4096 T=8")
+    inp = inputs(J, F64, (4096, 4096), 6)
+    S = inp["x0"].nbytes
+    a = gpu_vjp(J, inp, 8, HALF_SQ, 2 * S, adst.ADST_SCHED_BINOMIAL, lim=(0.3, 0.7),
+                want_xT=False)
+    b = gpu_vjp(J, inp, 8, HALF_SQ, 2 * S, adst.ADST_SCHED_BINOMIAL, lim=(0.3, 0.7),
+                want_xT=False, want_dparams=True)
+    assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
