@@ -30,8 +30,9 @@
 // mask is applied on entry), so the loads stay in flight behind the
 // arithmetic. Rows beyond the ones a chunk needs are never fetched from new
 // addresses. Odd chunks march downward, so the rows two neighbouring chunks
-// share are read by both at about the same time and the second read hits
-// the L2 cache they share (their blocks go to the same XCD).
+// share are read by both at about the same time and the second read can hit
+// the L2 cache they share (their blocks go to the same XCD); measured, this
+// cut the fetched bytes from 1.46x to 1.24x the state's size.
 //
 // Boundary. Blocks of kUnroll consecutive input rows whose evaluated rows all
 // lie two or more cells from the top and bottom edge, in a strip two or more
@@ -40,6 +41,9 @@
 // near the top and bottom edge do not make their waves the launch's tail;
 // the first and last strip (the side edges) take short chunks throughout,
 // and every XCD gets an equal share of them.
+//
+// The same layout carries the limiter's one-step adjoint (jacobi_lim_adjoint
+// below), which masks g by the branch outcome and transposes it in one pass.
 
 #include <hip/hip_runtime.h>
 
