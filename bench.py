@@ -39,6 +39,8 @@ def kernel_name(kind, adj, n):
     base = KERNELS[kind][1 if adj else 0]
     if kind == 3 or n == 1:
         return base
+    if kind == 1:
+        return f"{base}_n<{n}>"
     if n == 2:
         return base + "_x2"
     return f"jacobi_march<{'adj' if adj else 'fwd'},{n}>"
@@ -132,6 +134,31 @@ def cpu_baseline(w, inp, target_s, lim=None, want_dp=False):
             "sample": f"full {'x'.join(map(str, x0.shape))} grid, first {Ts} of {w.steps} steps, "
                       f"store-all tape, single thread, {dt:.1f} s",
             "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
+
+
+def copy_ceiling(torch, dev, stream, state_bytes):
+    """Bandwidth of a plain device-to-device copy (hipMemcpyAsync), bytes read
+    plus bytes written over the event-timed copy: at one state's size (the
+    buffers a launch streams; at 128 MiB a pair of them fits the 256 MB
+    Infinity Cache) and at 2 GiB, far beyond it."""
+    out = {"kernel": "hipMemcpyAsync device-to-device"}
+    for key, nbytes in (("state_size", min(state_bytes, 2 << 30)), ("2GiB", 2 << 30)):
+        a = torch.empty(nbytes // 8, dtype=torch.float64, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        reps = 10
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[key] = {"bytes": 2 * a.numel() * 8, "ms": round(ms, 5),
+                    "GB/s": round(2 * a.numel() * 8 / (ms * 1e-3) / 1e9, 1)}
+        del a, b
+    return out
 
 
 def _cpu_model():
@@ -284,6 +311,7 @@ def main():
         "phase_ms": {k: round(v, 4) for k, v in acc.items()},
         "roofline": roofline,
     }
+    res["copy_ceiling"] = copy_ceiling(torch, dev, stream, w.npoints * isz)
     if args.copy_probe_mib:
         del ws
         a = torch.empty(args.copy_probe_mib << 17, dtype=torch.float64, device=dev).fill_(1.0)

@@ -25,6 +25,7 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 // Temporal blocking: the most steps one launch may take (1 = none). The
 // fused adjoint is for state-free adjoints only.
 constexpr int32_t kJacMaxFuse = 6;
+constexpr int32_t kAcMaxFuse = 3;
 int32_t max_fused_forward(int32_t kind);
 int32_t max_fused_adjoint(int32_t kind, int64_t nx);
 

@@ -511,9 +511,11 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
   const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
   R belowA = ld(t.z0 - 1, t.ja, t.i), belowB = ld(t.z0 - 1, t.jb, t.i);
   R curA = ld(t.z0, t.ja, t.i), curB = ld(t.z0, t.jb, t.i);
+  R halo = hly >= 0 ? ld(t.z0, hj, hi) : R(0);
   for (int k = t.z0; k < t.z1; ++k) {
+    // the next plane's cells are requested before this plane is computed
     const R aboveA = ld(k + 1, t.ja, t.i), aboveB = ld(k + 1, t.jb, t.i);
-    const R halo = hly >= 0 ? ld(k, hj, hi) : R(0);
+    const R haloN = hly >= 0 ? ld(k + 1, hj, hi) : R(0);
     __syncthreads();
     tile[ty + 1][tx + 1] = curA;
     tile[ty + 5][tx + 1] = curB;
@@ -531,43 +533,61 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
     belowB = curB;
     curA = aboveA;
     curB = aboveB;
+    halo = haloN;
   }
 }
 
-// Two forward steps in one launch (temporal blocking in 2.5-D). The first
-// step is evaluated on a 64 x 16 region of each plane (four rows per
-// thread), the second on its inner 62 x 14 tile, marching in z: at plane p
-// the workgroup computes the intermediate state y1(p) from x(p-1..p+1) and
-// then the output plane p-1 from y1(p-2..p). x(p) and y1(p-1) are staged in
-// LDS for their xy neighbours, the z neighbours stay in registers. y1 is set
-// to 0 outside the grid, which is the zero ghost value the second step reads.
-constexpr int kAc2RPT = 4, kAc2SX = 64, kAc2SY = 4 * kAc2RPT;
-constexpr int kAc2OX = kAc2SX - 2, kAc2OY = kAc2SY - 2, kAc2ZC = 32;
+// K forward steps in one launch (temporal blocking in 2.5-D).
+// A workgroup of 64 x 4 threads owns a region of 64 columns x SY = 4 RPT
+// rows of each plane (RPT rows per thread, four apart) and marches in z. At
+// iteration p it evaluates step 1 at plane p from x(p-1..p+1), and step l at
+// plane p-l+1 from step l-1's planes p-l..p-l+2. Every step is evaluated on
+// the whole region but is valid only on its inner (64 - 2(l-1)) x (SY -
+// 2(l-1)) cells, because its xy neighbours come from the step before it on
+// the same region; the last step's valid cells are the output tile. x(p)
+// (with a one-cell ring) and each intermediate step's latest plane are
+// staged in LDS for the xy neighbours, the planes below and above stay in
+// registers. Intermediate values are 0 outside the grid, which is the zero
+// ghost value the next step reads; every point evaluates the single-step
+// expression, so any split of the steps into launches gives the same bits.
+// Measured at 1024^3 f64, three steps per launch (64 x 16 regions, 64
+// planes) beat two (the launches of a recomputation run drop by a third);
+// four, with 24-row regions, needed 178 VGPRs and with 16-row regions
+// evaluated 7 points per output point, and both were slower.
+template <int K, int RPT, int NZ>
+struct AcN {
+  static constexpr int SX = kBX, SY = kBY * RPT;
+  static constexpr int OX = SX - 2 * (K - 1), OY = SY - 2 * (K - 1);  // output tile
+  static constexpr int ZC = NZ;                                     // output planes
+};
 
-template <class R>
-__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_x2(const R* __restrict__ x,
-                                                                R* __restrict__ y, int nx, int ny,
-                                                                int nz, int tiles_x, int tiles_y,
-                                                                int ntiles, R D, R C) {
-  constexpr int SX = kAc2SX, SY = kAc2SY, LX = SX + 2, LY = SY + 2, RPT = kAc2RPT;
+template <class R, int K, int RPT, int NZ>
+__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restrict__ x,
+                                                               R* __restrict__ y, int nx, int ny,
+                                                               int nz, int tiles_x, int tiles_y,
+                                                               int ntiles, R D, R C) {
+  using A = AcN<K, RPT, NZ>;
+  constexpr int SX = A::SX, SY = A::SY, LX = SX + 2, LY = SY + 2, H = K - 1;
+  static_assert(K >= 2 && 2 * LX + 2 * SY <= kThreads, "ring cells: one per thread");
   __shared__ R xt[LY][LX];
-  __shared__ R yt[SY][SX];
+  __shared__ R yt[K - 1][SY][SX];  // steps 1 .. K-1
   int b = xcd_tile(ntiles);
   if (b >= ntiles) return;
   const int bx = b % tiles_x;
   b /= tiles_x;
   const int by = b % tiles_y;
   const int bz = b / tiles_y;
-  const int i0 = bx * kAc2OX, j0 = by * kAc2OY;
-  const int z0 = bz * kAc2ZC, z1 = min(z0 + kAc2ZC, nz);
+  const int i0 = bx * A::OX, j0 = by * A::OY;
+  const int z0 = bz * A::ZC, z1 = min(z0 + A::ZC, nz);
   const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
-  const int i1 = i0 - 1 + tx;  // column of this thread in the first-step region
+  const int ic = i0 - H + tx;  // column of this thread
   const int plane = nx * ny;
   auto inxy = [&](int j, int i) { return i >= 0 && i < nx && j >= 0 && j < ny; };
   auto ld = [&](int k, int j, int i) -> R {
     return (k >= 0 && k < nz && inxy(j, i)) ? x[k * plane + j * nx + i] : R(0);
   };
-  // one cell of the LDS ring around the region (2*LX + 2*SY = 164 < 256)
+  auto row = [&](int q) { return ty + kBY * q; };  // region row of the thread's q-th cell
+  // one cell of the LDS ring around the region
   int hly = -1, hlx = 0;
   if (tid < LX) {
     hly = 0;
@@ -582,56 +602,78 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_x2(const R* __restr
     hly = tid - 2 * LX - SY + 1;
     hlx = LX - 1;
   }
-  const int hj = j0 - 2 + hly, hi = i0 - 2 + hlx;
-  R xprev[RPT], xcur[RPT], xnext[RPT], yb[RPT], yc[RPT], yn[RPT];
+  const int hj = j0 - H - 1 + hly, hi = i0 - H - 1 + hlx;
+  // x at planes p-1, p, p+1; step l (index l-1) at planes p-l, p-l+1 and the
+  // one evaluated in this iteration
+  R xp[RPT], xc[RPT], xn[RPT];
+  R sb[K - 1][RPT], sc[K - 1][RPT], sn[K - 1][RPT];
+  const int pfirst = z0 - K + 1, plast = z1 + K - 2;
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
-    const int j1 = j0 - 1 + ty + 4 * q;
-    xprev[q] = ld(z0 - 2, j1, i1);
-    xcur[q] = ld(z0 - 1, j1, i1);
-    yb[q] = R(0);
-    yc[q] = R(0);
-  }
-  for (int p = z0 - 1; p <= z1; ++p) {
-    const R hv = hly >= 0 ? ld(p, hj, hi) : R(0);
+    const int j = j0 - H + row(q);
+    xp[q] = ld(pfirst - 1, j, ic);
+    xc[q] = ld(pfirst, j, ic);
 #pragma unroll
-    for (int q = 0; q < RPT; ++q) xnext[q] = ld(p + 1, j0 - 1 + ty + 4 * q, i1);
+    for (int l = 0; l < K - 1; ++l) sb[l][q] = sc[l][q] = R(0);
+  }
+  R hv = hly >= 0 ? ld(pfirst, hj, hi) : R(0);
+  for (int p = pfirst; p <= plast; ++p) {
+    // the next plane's cells are requested before this plane is computed
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) xn[q] = ld(p + 1, j0 - H + row(q), ic);
+    const R hvn = hly >= 0 ? ld(p + 1, hj, hi) : R(0);
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < RPT; ++q) xt[ty + 4 * q + 1][tx + 1] = xcur[q];
+    for (int q = 0; q < RPT; ++q) xt[row(q) + 1][tx + 1] = xc[q];
     if (hly >= 0) xt[hly][hlx] = hv;
     __syncthreads();
-    const bool pin = p >= 0 && p < nz;
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) {
-      const int r = ty + 4 * q;
-      yn[q] = (pin && inxy(j0 - 1 + r, i1))
-                  ? allencahn_point(xcur[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
-                                    xt[r + 2][tx + 1], xprev[q], xnext[q], D, C)
-                  : R(0);
-    }
-    if (p >= z0 + 1) {
-      const int k = p - 1;
+    {  // step 1 at plane p, on every cell of the region
+      const bool pin = p >= 0 && p < nz;
 #pragma unroll
       for (int q = 0; q < RPT; ++q) {
-        const int r = ty + 4 * q;
-        const int j = j0 - 1 + r;
-        if (tx >= 1 && tx <= kAc2OX && r >= 1 && r <= kAc2OY && inxy(j, i1))
-          y[k * plane + j * nx + i1] =
-              allencahn_point(yc[q], yt[r][tx - 1], yt[r][tx + 1], yt[r - 1][tx], yt[r + 1][tx],
-                              yb[q], yn[q], D, C);
+        const int r = row(q);
+        sn[0][q] = (pin && inxy(j0 - H + r, ic))
+                       ? allencahn_point(xc[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
+                                         xt[r + 2][tx + 1], xp[q], xn[q], D, C)
+                       : R(0);
+      }
+    }
+#pragma unroll
+    for (int l = 2; l <= K; ++l) {  // step l at plane p - l + 1
+      const int pl = p - l + 1;
+      const bool pin = pl >= 0 && pl < nz;
+      const bool xin = tx >= l - 1 && tx <= SX - l;
+#pragma unroll
+      for (int q = 0; q < RPT; ++q) {
+        const int r = row(q);
+        const int j = j0 - H + r;
+        const bool ok = pin && xin && r >= l - 1 && r <= SY - l && inxy(j, ic);
+        const R(*t)[SX] = yt[l - 2];
+        const R v = ok ? allencahn_point(sc[l - 2][q], t[r][tx - 1], t[r][tx + 1], t[r - 1][tx],
+                                         t[r + 1][tx], sb[l - 2][q], sn[l - 2][q], D, C)
+                       : R(0);
+        if (l < K)
+          sn[l - 1][q] = v;
+        else if (ok && pl >= z0 && pl < z1)
+          y[pl * plane + j * nx + ic] = v;
       }
     }
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < RPT; ++q) yt[ty + 4 * q][tx] = yn[q];
+    for (int l = 0; l < K - 1; ++l)
+#pragma unroll
+      for (int q = 0; q < RPT; ++q) yt[l][row(q)][tx] = sn[l][q];
 #pragma unroll
     for (int q = 0; q < RPT; ++q) {
-      xprev[q] = xcur[q];
-      xcur[q] = xnext[q];
-      yb[q] = yc[q];
-      yc[q] = yn[q];
+      xp[q] = xc[q];
+      xc[q] = xn[q];
+#pragma unroll
+      for (int l = 0; l < K - 1; ++l) {
+        sb[l][q] = sc[l][q];
+        sc[l][q] = sn[l][q];
+      }
     }
+    hv = hvn;
   }
 }
 
@@ -663,30 +705,26 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   ac_halo_cell(tid, &hly, &hlx);
   const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
   const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
+  // Every value a plane needs (g and x at the thread's cells, the halo cell)
+  // is requested one plane ahead, before the current plane is computed.
   R belowA = ld(g, t.z0 - 1, t.ja, t.i), belowB = ld(g, t.z0 - 1, t.jb, t.i);
   R curA = ld(g, t.z0, t.ja, t.i), curB = ld(g, t.z0, t.jb, t.i);
-  R xbelowA = R(0), xbelowB = R(0), xcurA = R(0), xcurB = R(0);
+  R halo = hly >= 0 ? ld(g, t.z0, hj, hi) : R(0);
+  R xbelowA = R(0), xbelowB = R(0);
+  R xcurA = ld(x, t.z0, t.ja, t.i), xcurB = ld(x, t.z0, t.jb, t.i);
+  R xhalo = R(0);
   if (DP) {
     xbelowA = ld(x, t.z0 - 1, t.ja, t.i);
     xbelowB = ld(x, t.z0 - 1, t.jb, t.i);
-    xcurA = ld(x, t.z0, t.ja, t.i);
-    xcurB = ld(x, t.z0, t.jb, t.i);
+    xhalo = hly >= 0 ? ld(x, t.z0, hj, hi) : R(0);
   }
   double a0 = 0.0, a1 = 0.0;
   for (int k = t.z0; k < t.z1; ++k) {
     const R aboveA = ld(g, k + 1, t.ja, t.i), aboveB = ld(g, k + 1, t.jb, t.i);
-    const R halo = hly >= 0 ? ld(g, k, hj, hi) : R(0);
-    R xa, xb, xaboveA = R(0), xaboveB = R(0), xhalo = R(0);
-    if (DP) {
-      xa = xcurA;
-      xb = xcurB;
-      xaboveA = ld(x, k + 1, t.ja, t.i);
-      xaboveB = ld(x, k + 1, t.jb, t.i);
-      xhalo = hly >= 0 ? ld(x, k, hj, hi) : R(0);
-    } else {
-      xa = va ? x[k * plane + t.ja * nx + t.i] : R(0);
-      xb = vb ? x[k * plane + t.jb * nx + t.i] : R(0);
-    }
+    const R haloN = hly >= 0 ? ld(g, k + 1, hj, hi) : R(0);
+    const R xaboveA = ld(x, k + 1, t.ja, t.i), xaboveB = ld(x, k + 1, t.jb, t.i);
+    const R xhaloN = DP && hly >= 0 ? ld(x, k + 1, hj, hi) : R(0);
+    const R xa = xcurA, xb = xcurB;
     __syncthreads();
     tile[ty + 1][tx + 1] = curA;
     tile[ty + 5][tx + 1] = curB;
@@ -734,12 +772,12 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
     belowB = curB;
     curA = aboveA;
     curB = aboveB;
-    if (DP) {
-      xbelowA = xcurA;
-      xbelowB = xcurB;
-      xcurA = xaboveA;
-      xcurB = xaboveB;
-    }
+    halo = haloN;
+    xbelowA = xcurA;
+    xbelowB = xcurB;
+    xcurA = xaboveA;
+    xcurB = xaboveB;
+    xhalo = xhaloN;
   }
   if (DP) {
     __syncthreads();
@@ -1058,6 +1096,31 @@ int vec_ok(int nx, const void* a, const void* b = nullptr, const void* c = nullp
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+template <class R, int K, int RPT, int NZ>
+hipError_t ac_forward_n(const StepShape& s, const R* x, R* y, hipStream_t st) {
+  using A = AcN<K, RPT, NZ>;
+  const int tx = cdiv(s.nx, A::OX), ty = cdiv(s.ny, A::OY);
+  const int nt = tx * ty * cdiv(s.nz, A::ZC);
+  fwd_allencahn3d7_n<R, K, RPT, NZ><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
+      x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+  return hipGetLastError();
+}
+
+// Allen-Cahn, n fused forward steps (2 <= n <= kAcMaxFuse).
+template <class R>
+hipError_t ac_forward_steps(const StepShape& s, const void* xv, void* yv, int32_t n,
+                            hipStream_t st) {
+  const R* x = static_cast<const R*>(xv);
+  R* y = static_cast<R*>(yv);
+  switch (n) {
+    case 2:
+      return ac_forward_n<R, 2, 4, 32>(s, x, y, st);
+    case 3:
+      return ac_forward_n<R, 3, 4, 64>(s, x, y, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <class R>
 hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv, bool two,
                      hipStream_t st) {
@@ -1085,10 +1148,7 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
     }
     case ADST_ALLENCAHN3D7: {
       if (two) {
-        const int tx = cdiv(s.nx, kAc2OX), ty = cdiv(s.ny, kAc2OY);
-        const int nt = tx * ty * cdiv(s.nz, kAc2ZC);
-        fwd_allencahn3d7_x2<R><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-            x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+        return ac_forward_n<R, 2, 4, 32>(s, x, y, st);
       } else {
         const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
         const int nt = tx * ty * cdiv(s.nz, kAcZC);
@@ -1233,7 +1293,7 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 }
 
 int32_t max_fused_forward(int32_t kind) {
-  return kind == ADST_JACOBI2D5 ? kJacMaxFuse : kind == ADST_ALLENCAHN3D7 ? 2 : 1;
+  return kind == ADST_JACOBI2D5 ? kJacMaxFuse : kind == ADST_ALLENCAHN3D7 ? kAcMaxFuse : 1;
 }
 // The marching adjoint needs rows wider than one lane's 16 bytes; narrower
 // grids take the fused pair.
@@ -1245,6 +1305,9 @@ int32_t max_fused_adjoint(int32_t kind, int64_t nx) {
 hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, void* y, int32_t n,
                             hipStream_t stream) {
   if (n < 2 || n > max_fused_forward(s.kind)) return hipErrorInvalidValue;
+  if (s.kind == ADST_ALLENCAHN3D7)
+    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, y, n, stream)
+                               : ac_forward_steps<float>(s, x, y, n, stream);
   if (n == 2)
     return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, true, stream)
                                : forward_t<float>(s, x, K, y, true, stream);

@@ -209,7 +209,7 @@ FUSION_CASES = [
 @pytest.mark.parametrize("kind,dtype,shape,T,loss,dK,flags,sched,slots", FUSION_CASES)
 def test_fused_launches_match_single_steps_bitwise(kind, dtype, shape, T, loss, dK, flags, sched,
                                                    slots):
-    """Temporal blocking (two steps per launch) gives the bits of one launch
+    """Temporal blocking (several steps per launch) gives the bits of one launch
     per step, and both match the oracle."""
     say(f"fusion kind={kind} dtype={dtype} shape={shape} T={T} flags={flags} sched={sched}")
     inp = inputs(kind, dtype, shape, 8)
