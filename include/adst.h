@@ -115,9 +115,9 @@ typedef enum {
 #define ADST_TRACE 0x2u      /* time the launches with HIP events, synchronise the stream at
                                 the end of the call and fill the ms_* fields of adst_plan_info */
 #define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking:
-                                otherwise up to 6 Jacobi steps or 3 Allen-Cahn forward
-                                steps share one launch); results are bit-identical either
-                                way */
+                                otherwise up to 6 Jacobi steps, 3 Allen-Cahn forward steps
+                                or 2 variable-coefficient forward steps share one launch);
+                                results are bit-identical either way */
 #define ADST_LIMIT 0x8u      /* a limiter on every step: each new value y (ring included)
                                 becomes lim[0] if y < lim[0], lim[1] if y > lim[1], else stays
                                 y. A data-dependent branch at every point of every step

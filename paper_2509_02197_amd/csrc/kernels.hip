@@ -860,6 +860,107 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
     rows(std::false_type{});
 }
 
+// Two forward steps in one launch. A workgroup owns kX2TW = 252 output
+// columns and TR rows; x and K are staged with a two-cell halo, the first
+// step is evaluated on the tile plus a one-cell ring (254 columns, one per
+// thread, TR + 2 rows) and written back over the staged x, the second on
+// the tile. Both slide the 3 x 3 windows of the single step down a column
+// and evaluate its expression in its order, so the result is bit-identical
+// to two single steps. Values of the first step outside the grid are never
+// read: the second step drops out-of-grid neighbours as the single step
+// does.
+constexpr int kVdX2TR = 8;
+template <class R, int TR>
+__global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restrict__ x,
+                                                                const R* __restrict__ K,
+                                                                R* __restrict__ y, int nx, int ny,
+                                                                int tiles_x, int ntiles, int vec,
+                                                                R dt, R ca, R cd) {
+  using G = Tile2x2<R, TR>;
+  __shared__ R sx[G::LR * G::LW];
+  __shared__ R sk[G::LR * G::LW];
+  const int b = xcd_tile(ntiles);
+  if (b >= ntiles) return;
+  const int i0 = (b % tiles_x) * kX2TW, j0 = (b / tiles_x) * TR;
+  // LDS row r is grid row j0 - 2 + r, LDS column c grid column i0 - PADL + c
+  stage_rows<R, kX2Threads, G::LR, G::LW>(sx, x, i0 - G::PADL, j0 - 2, nx, ny, vec);
+  stage_rows<R, kX2Threads, G::LR, G::LW>(sk, K, i0 - G::PADL, j0 - 2, nx, ny, vec);
+  __syncthreads();
+  const int t = threadIdx.x;
+  R xw[3][3], kw[3][3];
+  // one step on LDS rows r_first .. r_first + n - 1 at LDS column c (grid
+  // column i), from the windows of sx and sk; out[k] = value at row r_first + k
+  auto column = [&](auto all_in_t, int c, int i, int r_first, int n, R* out) {
+    constexpr bool ALL_IN = decltype(all_in_t)::value;
+    auto enter = [&](int slot, int lr) {
+#pragma unroll
+      for (int e = 0; e < 3; ++e) {
+        xw[slot][e] = sx[lr * G::LW + c - 1 + e];
+        kw[slot][e] = sk[lr * G::LW + c - 1 + e];
+      }
+    };
+    enter(0, r_first - 1);
+    enter(1, r_first);
+    const bool xin = i > 0 && i < nx - 1;
+#pragma unroll
+    for (int k = 0; k < TR + 2; ++k) {
+      if (k >= n) break;
+      const int j = j0 - 2 + r_first + k;
+      enter(2, r_first + k + 1);
+      const R xc = xw[1][1], Kc = kw[1][1];
+      R acc = R(0);
+      const bool inner = ALL_IN || (xin && j > 0 && j < ny - 1);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (!ALL_IN && !inner) {
+          const int a = i + kNbrDx[q], bb = j + kNbrDy[q];
+          if (a < 0 || a >= nx || bb < 0 || bb >= ny) continue;
+        }
+        const int wr = 1 + kNbrDy[q], wc = 1 + kNbrDx[q];
+        acc += ((q < 4 ? ca : cd) * (Kc + kw[wr][wc])) * (xw[wr][wc] - xc);
+      }
+      out[k] = xc + dt * acc;
+#pragma unroll
+      for (int e = 0; e < 3; ++e) {
+        xw[0][e] = xw[1][e];
+        kw[0][e] = kw[1][e];
+        xw[1][e] = xw[2][e];
+        kw[1][e] = kw[2][e];
+      }
+    }
+  };
+  // every cell of the first step's region has eight in-grid neighbours
+  // (workgroup-uniform)
+  const bool all_in = i0 - 1 >= 1 && i0 + kX2TW <= nx - 2 && j0 - 1 >= 1 && j0 + TR <= ny - 2;
+  // first step: LDS rows 1 .. TR + 2, LDS column PADL - 1 + t
+  R v[TR + 2];
+  const int c1 = G::PADL - 1 + t, i1 = i0 - 1 + t;
+  const bool act = t < kX2TW + 2;
+  if (act) {
+    if (all_in)
+      column(std::true_type{}, c1, i1, 1, TR + 2, v);
+    else
+      column(std::false_type{}, c1, i1, 1, TR + 2, v);
+  }
+  __syncthreads();
+  if (act) {
+#pragma unroll
+    for (int r = 0; r < TR + 2; ++r) sx[(r + 1) * G::LW + c1] = v[r];
+  }
+  __syncthreads();
+  // second step on the tile: LDS rows 2 .. TR + 1, LDS column PADL + t
+  const int i = i0 + t;
+  if (t >= kX2TW || i >= nx) return;
+  const int rows = min(TR, ny - j0);
+  if (all_in)
+    column(std::true_type{}, G::PADL + t, i, 2, TR, v);
+  else
+    column(std::false_type{}, G::PADL + t, i, 2, rows, v);
+#pragma unroll
+  for (int r = 0; r < TR; ++r)
+    if (r < rows) y[(j0 + r) * nx + i] = v[r];
+}
+
 // Adjoint (the operator is symmetric in x):
 //   g'[m] = g[m] + dt * sum_n (c_n*(K[m]+K[n]))*(g[n]-g[m])
 //   dK[m] += dt * sum_n (c_n*(x[n]-x[m]))*(g[m]-g[n])      (x = x_{t-1})
@@ -1162,7 +1263,13 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       break;
     }
     case ADST_VARDIFF2D9: {
-      if (two) return hipErrorInvalidValue;
+      if (two) {
+        const int tx = cdiv(s.nx, kX2TW), nt = tx * cdiv(s.ny, kVdX2TR);
+        fwd_vardiff2d9_x2<R, kVdX2TR><<<dim3(xcd_grid(nt)), dim3(kX2Threads), 0, st>>>(
+            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
+            R(1) / R(12));
+        break;
+      }
       const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
       if (s.limit)
         fwd_vardiff2d9<R, true><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
@@ -1293,7 +1400,15 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
 }
 
 int32_t max_fused_forward(int32_t kind) {
-  return kind == ADST_JACOBI2D5 ? kJacMaxFuse : kind == ADST_ALLENCAHN3D7 ? kAcMaxFuse : 1;
+  switch (kind) {
+    case ADST_JACOBI2D5:
+      return kJacMaxFuse;
+    case ADST_ALLENCAHN3D7:
+      return kAcMaxFuse;
+    case ADST_VARDIFF2D9:
+      return 2;
+  }
+  return 1;
 }
 // The marching adjoint needs rows wider than one lane's 16 bytes; narrower
 // grids take the fused pair.

@@ -237,7 +237,7 @@ def test_fused_plans_replay_with_the_same_step_counts(kind, flags, sched, slots)
         assert info.fwd_steps_total == infon.fwd_steps_total == nf
         assert info.fwd_launches <= infon.fwd_launches == infon.fwd_steps_total
         assert info.adj_launches <= infon.adj_launches == T
-        depth = 6 if kind == adst.ADST_JACOBI2D5 else 3 if kind == AC else 1
+        depth = {adst.ADST_JACOBI2D5: 6, AC: 3, adst.ADST_VARDIFF2D9: 2}[kind]
         assert all(a[4] <= depth for a in fused if a[0] == adst.ADST_OP_FWD2)
         assert all(a[4] <= depth for a in fused if a[0] == adst.ADST_OP_ADJ2)
 
