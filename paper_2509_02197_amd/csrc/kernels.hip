@@ -43,8 +43,9 @@ inline unsigned xcd_grid(int64_t ntiles) { return (unsigned)(8 * ((ntiles + 7) /
 
 // Streaming stores. When a state is at least kStreamBytes, the states a
 // launch reads and writes exceed the 256 MB Infinity Cache and nothing reads
-// a written value again within the launch, so the Allen-Cahn kernels store
-// (and read their once-read inputs) with non-temporal hints: written lines
+// a written value again within the launch, so the Allen-Cahn and
+// variable-coefficient kernels store (and the Allen-Cahn adjoint reads its
+// once-read x) with non-temporal hints: written lines
 // then stop evicting the halo lines that neighbouring tiles read from L2
 // (measured at 512^3 f64: 4.7 -> 5.25 TB/s adjoint, 2393 -> 2193 ms for the
 // 1024^3 call). Below it, the written state is the next launch's input and
@@ -821,7 +822,7 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
 // ------------------------------------------ variable-coefficient diffusion 2-D
 constexpr int kVdTW = 256, kVdTR = 8, kVdAdjTR = 4;
 
-template <class R, bool LIM>
+template <class R, bool LIM, bool NT>
 __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
                                                         const R* __restrict__ K,
                                                         R* __restrict__ y, int nx, int ny,
@@ -877,7 +878,7 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
         acc += ((n < 4 ? ca : cd) * (Kc + kw[wr][wc])) * (xw[wr][wc] - xc);
       }
       const R v = xc + dt * acc;
-      y[j * nx + i] = LIM ? limited(v, lim) : v;
+      put<NT>(&y[j * nx + i], LIM ? limited(v, lim) : v);
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
         xw[0][c] = xw[1][c];
@@ -903,7 +904,7 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
 // read: the second step drops out-of-grid neighbours as the single step
 // does.
 constexpr int kVdX2TR = 8;
-template <class R, int TR>
+template <class R, int TR, bool NT>
 __global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restrict__ x,
                                                                 const R* __restrict__ K,
                                                                 R* __restrict__ y, int nx, int ny,
@@ -991,7 +992,7 @@ __global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restr
     column(std::false_type{}, G::PADL + t, i, 2, rows, v);
 #pragma unroll
   for (int r = 0; r < TR; ++r)
-    if (r < rows) y[(j0 + r) * nx + i] = v[r];
+    if (r < rows) put<NT>(&y[(j0 + r) * nx + i], v[r]);
 }
 
 // Adjoint (the operator is symmetric in x):
@@ -1001,7 +1002,7 @@ __global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restr
 // DP adds this step's share of dL/ddt (see DpOut), sum_m g[m] * acc[m] with
 // the forward's acc. Threads past the grid's last column take part in the
 // block sum.
-template <class R, bool WANT_DK, int TR, bool DP>
+template <class R, bool WANT_DK, int TR, bool DP, bool NT>
 __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
                                                         const R* __restrict__ K,
                                                         const R* __restrict__ g,
@@ -1068,8 +1069,8 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
         if (DP) acc += (cn * (Kc + kw[wr][wc])) * (xw[XS ? wr : 0][wc] - xc);
       }
       const int o = j * nx + i;
-      gp[o] = gc + dt * ag;
-      if (WANT_DK) dK[o] = (dk_first ? R(0) : dK[o]) + dt * ak;
+      put<NT>(&gp[o], gc + dt * ag);
+      if (WANT_DK) put<NT>(&dK[o], (dk_first ? R(0) : dK[o]) + dt * ak);
       if (DP) a0 += (double)gc * (double)acc;
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
@@ -1314,28 +1315,54 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       break;
     }
     case ADST_VARDIFF2D9: {
+      const bool str = streams(s) != 0;
+      const int vec = vec_ok<R>(s.nx, x, K);
+      const R dt = R(s.p0), ca = R(1) / R(3), cd = R(1) / R(12);
       if (two) {
         const int tx = cdiv(s.nx, kX2TW), nt = tx * cdiv(s.ny, kVdX2TR);
-        fwd_vardiff2d9_x2<R, kVdX2TR><<<dim3(xcd_grid(nt)), dim3(kX2Threads), 0, st>>>(
-            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
-            R(1) / R(12));
+        const dim3 grid(xcd_grid(nt)), block(kX2Threads);
+        if (str)
+          fwd_vardiff2d9_x2<R, kVdX2TR, true><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt,
+                                                                      vec, dt, ca, cd);
+        else
+          fwd_vardiff2d9_x2<R, kVdX2TR, false><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx,
+                                                                       nt, vec, dt, ca, cd);
         break;
       }
       const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
-      if (s.limit)
-        fwd_vardiff2d9<R, true><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
-            R(1) / R(12), lim);
+      const dim3 grid(xcd_grid(nt)), block(kVdTW);
+      if (s.limit && str)
+        fwd_vardiff2d9<R, true, true><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt, vec,
+                                                              dt, ca, cd, lim);
+      else if (s.limit)
+        fwd_vardiff2d9<R, true, false><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt, vec,
+                                                               dt, ca, cd, lim);
+      else if (str)
+        fwd_vardiff2d9<R, false, true><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt, vec,
+                                                               dt, ca, cd, lim);
       else
-        fwd_vardiff2d9<R, false><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-            x, K, y, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, x, K), R(s.p0), R(1) / R(3),
-            R(1) / R(12), lim);
+        fwd_vardiff2d9<R, false, false><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt, vec,
+                                                                dt, ca, cd, lim);
       break;
     }
     default:
       return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// One variable-coefficient adjoint launch over ntiles tiles, streaming or not.
+template <class R, bool WANT_DK, int TR, bool DP>
+void vd_adjoint(bool str, int ntiles, hipStream_t st, const R* x, const R* K, const R* g, R* gp,
+                R* dK, int dk_first, int nx, int ny, int tiles_x, int vec, R dt, R ca, R cd,
+                DpOut dp) {
+  const dim3 grid(xcd_grid(ntiles)), block(kVdTW);
+  if (str)
+    adj_vardiff2d9<R, WANT_DK, TR, DP, true><<<grid, block, 0, st>>>(
+        x, K, g, gp, dK, dk_first, nx, ny, tiles_x, ntiles, vec, dt, ca, cd, dp);
+  else
+    adj_vardiff2d9<R, WANT_DK, TR, DP, false><<<grid, block, 0, st>>>(
+        x, K, g, gp, dK, dk_first, nx, ny, tiles_x, ntiles, vec, dt, ca, cd, dp);
 }
 
 template <class R>
@@ -1385,24 +1412,21 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
       const int tx = cdiv(s.nx, kVdTW);
       const R dt = R(s.p0), ca = R(1) / R(3), cd = R(1) / R(12);
       const int nt4 = tx * cdiv(s.ny, kVdAdjTR);
-      if (dK && dp_part) {
-        adj_vardiff2d9<R, true, kVdAdjTR, true><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
-            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt,
-            ca, cd, dp);
-      } else if (dK) {
-        adj_vardiff2d9<R, true, kVdAdjTR, false><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
-            x, K, g, gp, dK, dk_first ? 1 : 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt,
-            ca, cd, dp);
-      } else if (dp_part) {
-        adj_vardiff2d9<R, false, kVdAdjTR, true><<<dim3(xcd_grid(nt4)), dim3(kVdTW), 0, st>>>(
-            x, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt4, vec_ok<R>(s.nx, g, K, x), dt, ca, cd,
-            dp);
-      } else {
-        const int nt = tx * cdiv(s.ny, kVdTR);
-        adj_vardiff2d9<R, false, kVdTR, false><<<dim3(xcd_grid(nt)), dim3(kVdTW), 0, st>>>(
-            nullptr, K, g, gp, nullptr, 0, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g, K), dt, ca,
-            cd, dp);
-      }
+      const bool str = streams(s) != 0;
+      const int dkf = dk_first ? 1 : 0, vx = vec_ok<R>(s.nx, g, K, x);
+      if (dK && dp_part)
+        vd_adjoint<R, true, kVdAdjTR, true>(str, nt4, st, x, K, g, gp, dK, dkf, s.nx, s.ny, tx,
+                                            vx, dt, ca, cd, dp);
+      else if (dK)
+        vd_adjoint<R, true, kVdAdjTR, false>(str, nt4, st, x, K, g, gp, dK, dkf, s.nx, s.ny, tx,
+                                             vx, dt, ca, cd, dp);
+      else if (dp_part)
+        vd_adjoint<R, false, kVdAdjTR, true>(str, nt4, st, x, K, g, gp, nullptr, 0, s.nx, s.ny,
+                                             tx, vx, dt, ca, cd, dp);
+      else
+        vd_adjoint<R, false, kVdTR, false>(str, tx * cdiv(s.ny, kVdTR), st, nullptr, K, g, gp,
+                                           nullptr, 0, s.nx, s.ny, tx, vec_ok<R>(s.nx, g, K), dt,
+                                           ca, cd, dp);
       break;
     }
     default:
