@@ -255,6 +255,8 @@ def main():
     if args.dparams and (w.kind == adst.ADST_JACOBI2D5 or
                          (w.kind == adst.ADST_VARDIFF2D9 and not w.want_dK)):
         adj_B += isz  # the fused constants' gradients also read x_{t-1}
+    elif args.limit and w.kind == adst.ADST_JACOBI2D5:
+        adj_B += isz  # the adjoint applies the branch mask, reading x_{t-1}
     in_place = w.kind == adst.ADST_GAUSSSEIDEL2D5
     # units of fwd_B * npoints moved per call: one per launch, or one per step
     fwd_units = info.fwd_steps_total if in_place else info.fwd_launches

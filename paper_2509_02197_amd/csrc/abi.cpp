@@ -162,7 +162,14 @@ void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd
   if (c.want_dp && (c.shape.kind == ADST_JACOBI2D5 || (c.shape.kind == ADST_VARDIFF2D9 && !want_dk)))
     *dparam = s;
   // the limiter's branch mask reads x_{t-1} (and K) and updates g_t in place
-  if (c.shape.limit) *dparam += (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
+  // in a pass of its own; where the adjoint applies it, it only adds the
+  // read of x_{t-1} an adjoint without state does not make
+  if (c.shape.limit) {
+    if (!adjoint_applies_limit(c.shape, c.want_dp))
+      *dparam += (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
+    else if (c.shape.kind == ADST_JACOBI2D5)
+      *dparam += s;
+  }
 }
 
 void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,

@@ -61,7 +61,8 @@ hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, cons
                           hipStream_t stream);
 
 // With the limiter on, whether launch_adjoint applies the branch mask itself
-// (reading x = x_{t-1}); otherwise launch_limit_mask must run first.
+// (reading x = x_{t-1}; Jacobi and Allen-Cahn without the constants'
+// gradients); otherwise launch_limit_mask must run first.
 bool adjoint_applies_limit(const StepShape& s, bool dparams);
 
 // Number of per-block loss partials launch_seed writes for n points.

@@ -711,13 +711,19 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
 // DP: also this step's share of dL/dD and dL/dC (see DpOut), from x_{t-1}
 // staged the same way as g (its plane in LDS, the planes below and above in
 // registers).
-template <class R, bool DP, bool NT>
+// LIM (the limiter, without DP): g is masked by the branch outcome of step t
+// as it is read, g'[m] = (k0 - k1*x[m]^2) * gm[m] + D * sum_nbr gm with
+// gm = g where the step's unlimited value (re-evaluated from x = x_{t-1}
+// with the forward's expression, neighbours from global memory) lies in
+// [lo, hi] and 0 elsewhere, so no separate mask pass runs.
+template <class R, bool DP, bool NT, bool LIM>
 __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict__ x,
                                                              const R* __restrict__ g,
                                                              R* __restrict__ gp, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
                                                              int ntiles, R D, R k0, R k1,
-                                                             DpOut dp) {
+                                                             DpOut dp, R C, Limit<R> lim) {
+  static_assert(!(DP && LIM), "the constants' gradients keep the separate mask pass");
   __shared__ R tile[kAcTY + 2][kAcTX + 2];
   __shared__ R tilex[DP ? kAcTY + 2 : 1][DP ? kAcTX + 2 : 1];
   AcTile t;
@@ -727,11 +733,26 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
     return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? a[k * plane + j * nx + i]
                                                                       : R(0);
   };
-  // without the constants' gradients x is read once per point (streamed)
+  // without the constants' gradients or the limiter x is read once per
+  // point (streamed)
   auto ldnt = [&](const R* a, int k, int j, int i) -> R {
     return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx)
-               ? take<NT>(&a[k * plane + j * nx + i])
+               ? take<NT && !LIM>(&a[k * plane + j * nx + i])
                : R(0);
+  };
+  // g at a cell, masked by the limiter's branch outcome there (LIM)
+  auto ldg = [&](int k, int j, int i) -> R {
+    if (!(k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx)) return R(0);
+    const int q = k * plane + j * nx + i;
+    const R v = g[q];
+    if constexpr (LIM) {
+      const R y = allencahn_point(x[q], i > 0 ? x[q - 1] : R(0), i < nx - 1 ? x[q + 1] : R(0),
+                                  j > 0 ? x[q - nx] : R(0), j < ny - 1 ? x[q + nx] : R(0),
+                                  k > 0 ? x[q - plane] : R(0), k < nz - 1 ? x[q + plane] : R(0),
+                                  D, C);
+      return (y < lim.lo || y > lim.hi) ? R(0) : v;
+    }
+    return v;
   };
   const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
   int hly, hlx;
@@ -740,9 +761,9 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
   // Every value a plane needs (g and x at the thread's cells, the halo cell)
   // is requested one plane ahead, before the current plane is computed.
-  R belowA = ld(g, t.z0 - 1, t.ja, t.i), belowB = ld(g, t.z0 - 1, t.jb, t.i);
-  R curA = ld(g, t.z0, t.ja, t.i), curB = ld(g, t.z0, t.jb, t.i);
-  R halo = hly >= 0 ? ld(g, t.z0, hj, hi) : R(0);
+  R belowA = ldg(t.z0 - 1, t.ja, t.i), belowB = ldg(t.z0 - 1, t.jb, t.i);
+  R curA = ldg(t.z0, t.ja, t.i), curB = ldg(t.z0, t.jb, t.i);
+  R halo = hly >= 0 ? ldg(t.z0, hj, hi) : R(0);
   R xbelowA = R(0), xbelowB = R(0);
   R xcurA = ld(x, t.z0, t.ja, t.i), xcurB = ld(x, t.z0, t.jb, t.i);
   R xhalo = R(0);
@@ -753,8 +774,8 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   }
   double a0 = 0.0, a1 = 0.0;
   for (int k = t.z0; k < t.z1; ++k) {
-    const R aboveA = ld(g, k + 1, t.ja, t.i), aboveB = ld(g, k + 1, t.jb, t.i);
-    const R haloN = hly >= 0 ? ld(g, k + 1, hj, hi) : R(0);
+    const R aboveA = ldg(k + 1, t.ja, t.i), aboveB = ldg(k + 1, t.jb, t.i);
+    const R haloN = hly >= 0 ? ldg(k + 1, hj, hi) : R(0);
     const R xaboveA = DP ? ld(x, k + 1, t.ja, t.i) : ldnt(x, k + 1, t.ja, t.i);
     const R xaboveB = DP ? ld(x, k + 1, t.jb, t.i) : ldnt(x, k + 1, t.jb, t.i);
     const R xhaloN = DP && hly >= 0 ? ld(x, k + 1, hj, hi) : R(0);
@@ -1393,19 +1414,24 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
       const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
       const int nt = tx * ty * cdiv(s.nz, kAcZC);
       const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
-      const bool str = streams(s) != 0;
+      const bool str = streams(s) != 0, lm = adjoint_applies_limit(s, dp_part != nullptr);
+      const Limit<R> lim{R(s.lo), R(s.hi)};
+#define ADST_AC_ADJ(DPV, NTV, LIMV)                                                  \
+  adj_allencahn3d7<R, DPV, NTV, LIMV><<<grid, block, 0, st>>>(                       \
+      x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1, dp, C, lim)
       if (dp_part && str)
-        adj_allencahn3d7<R, true, true><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx,
-                                                                ty, nt, D, k0, k1, dp);
+        ADST_AC_ADJ(true, true, false);
       else if (dp_part)
-        adj_allencahn3d7<R, true, false><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx,
-                                                                 ty, nt, D, k0, k1, dp);
+        ADST_AC_ADJ(true, false, false);
+      else if (lm && str)
+        ADST_AC_ADJ(false, true, true);
+      else if (lm)
+        ADST_AC_ADJ(false, false, true);
       else if (str)
-        adj_allencahn3d7<R, false, true><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx,
-                                                                 ty, nt, D, k0, k1, dp);
+        ADST_AC_ADJ(false, true, false);
       else
-        adj_allencahn3d7<R, false, false><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx,
-                                                                  ty, nt, D, k0, k1, dp);
+        ADST_AC_ADJ(false, false, false);
+#undef ADST_AC_ADJ
       break;
     }
     case ADST_VARDIFF2D9: {
@@ -1522,7 +1548,7 @@ hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev
 }
 
 bool adjoint_applies_limit(const StepShape& s, bool dparams) {
-  return s.limit && s.kind == ADST_JACOBI2D5 && !dparams;
+  return s.limit && !dparams && (s.kind == ADST_JACOBI2D5 || s.kind == ADST_ALLENCAHN3D7);
 }
 
 hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, const void* g_next,
@@ -1530,7 +1556,7 @@ hipError_t launch_adjoint(const StepShape& s, const void* x, const void* K, cons
                           hipStream_t stream) {
   if (dp_part && (s.kind < ADST_JACOBI2D5 || s.kind > ADST_VARDIFF2D9 || !x))
     return hipErrorInvalidValue;
-  if (adjoint_applies_limit(s, dp_part != nullptr))
+  if (s.kind == ADST_JACOBI2D5 && adjoint_applies_limit(s, dp_part != nullptr))
     return launch_jacobi_lim_adjoint(s, x, g_next, g_prev, stream);
   return s.dtype == ADST_F64
              ? adjoint_t<double>(s, x, K, g_next, g_prev, dK, dk_first, dp_part, dp_first, stream)

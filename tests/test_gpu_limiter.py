@@ -151,3 +151,40 @@ def test_fused_limiter_adjoint_full_grid():
     b = gpu_vjp(J, inp, 8, HALF_SQ, 2 * S, adst.ADST_SCHED_BINOMIAL, lim=(0.3, 0.7),
                 want_xT=False, want_dparams=True)
     assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
+
+
+# The Allen-Cahn adjoint applies the branch mask as it reads g (the step's
+# value re-evaluated at every cell it reads: its own, the six neighbours'
+# and the LDS ring's); with the constants' gradients it keeps the separate
+# mask pass. Shapes put the 64 x 8 x 32 tiles' edges, ragged tails in every
+# axis and one-plane and one-row grids against the ring.
+FUSED_LIM_AC_SHAPES = [
+    (F64, (39, 45, 67)), (F64, (33, 9, 65)), (F64, (1, 20, 70)), (F64, (40, 1, 3)),
+    (F64, (3, 4, 5)), (F32, (17, 33, 65)), (F32, (64, 16, 128)),
+]
+
+
+@pytest.mark.parametrize("dtype,shape", FUSED_LIM_AC_SHAPES)
+def test_fused_limiter_allencahn_matches_two_pass(dtype, shape):
+    say(f"fused limiter allen-cahn dtype={dtype} shape={shape}")
+    inp = inputs(AC, dtype, shape, 7)
+    T, loss = 7, DOT_W
+    a = gpu_vjp(AC, inp, T, loss, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL, lim=LIM[AC])
+    b = gpu_vjp(AC, inp, T, loss, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL, lim=LIM[AC],
+                want_dparams=True)
+    assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
+    ref = oracle.vjp(AC, inp["x0"], steps=T, loss=loss, aux=inp["aux"], lim=LIM[AC])
+    assert rel(a["dx0"], ref[0]) <= TOL[dtype]
+
+
+def test_fused_limiter_allencahn_full_grid():
+    """512^3 f64, the benchmark's Allen-Cahn limiter leg: the masked adjoint
+    (streaming stores at this size) and the two-pass one give the same bits."""
+    say("fused limiter allen-cahn 512^3 T=4")
+    inp = inputs(AC, F64, (512, 512, 512), 8)
+    S = inp["x0"].nbytes
+    a = gpu_vjp(AC, inp, 4, DOT_W, 2 * S, adst.ADST_SCHED_BINOMIAL, lim=(-0.9, 0.9),
+                want_xT=False)
+    b = gpu_vjp(AC, inp, 4, DOT_W, 2 * S, adst.ADST_SCHED_BINOMIAL, lim=(-0.9, 0.9),
+                want_xT=False, want_dparams=True)
+    assert np.array_equal(a["dx0"], b["dx0"]) and a["loss"] == b["loss"]
