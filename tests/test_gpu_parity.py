@@ -203,6 +203,9 @@ FUSION_CASES = [
     (AC, F64, (1, 1, 1), 6, SEED, False, 0, adst.ADST_SCHED_BINOMIAL, 0),
     (AC, F64, (3, 1, 200), 7, HALF_SQ, False, 0, adst.ADST_SCHED_BINOMIAL, 1),
     (AC, F64, (33, 14, 62), 5, DOT_W, False, 0, adst.ADST_SCHED_BINOMIAL, 0),
+    (AC, F64, (33, 17, 129), 6, DOT_W, False, 0, adst.ADST_SCHED_BINOMIAL, 2),
+    (AC, F64, (20, 32, 256), 5, HALF_SQ, False, 0, adst.ADST_SCHED_UNIFORM, 2),
+    (AC, F32, (9, 16, 128), 4, DIFF, False, 0, adst.ADST_SCHED_BINOMIAL, 1),
 ]
 
 
