@@ -711,19 +711,13 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
 // DP: also this step's share of dL/dD and dL/dC (see DpOut), from x_{t-1}
 // staged the same way as g (its plane in LDS, the planes below and above in
 // registers).
-// LIM (the limiter, without DP): g is masked by the branch outcome of step t
-// as it is read, g'[m] = (k0 - k1*x[m]^2) * gm[m] + D * sum_nbr gm with
-// gm = g where the step's unlimited value (re-evaluated from x = x_{t-1}
-// with the forward's expression, neighbours from global memory) lies in
-// [lo, hi] and 0 elsewhere, so no separate mask pass runs.
-template <class R, bool DP, bool NT, bool LIM>
+template <class R, bool DP, bool NT>
 __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict__ x,
                                                              const R* __restrict__ g,
                                                              R* __restrict__ gp, int nx, int ny,
                                                              int nz, int tiles_x, int tiles_y,
                                                              int ntiles, R D, R k0, R k1,
-                                                             DpOut dp, R C, Limit<R> lim) {
-  static_assert(!(DP && LIM), "the constants' gradients keep the separate mask pass");
+                                                             DpOut dp) {
   __shared__ R tile[kAcTY + 2][kAcTX + 2];
   __shared__ R tilex[DP ? kAcTY + 2 : 1][DP ? kAcTX + 2 : 1];
   AcTile t;
@@ -733,27 +727,13 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
     return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? a[k * plane + j * nx + i]
                                                                       : R(0);
   };
-  // without the constants' gradients or the limiter x is read once per
-  // point (streamed)
+  // without the constants' gradients x is read once per point (streamed)
   auto ldnt = [&](const R* a, int k, int j, int i) -> R {
     return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx)
-               ? take<NT && !LIM>(&a[k * plane + j * nx + i])
+               ? take<NT>(&a[k * plane + j * nx + i])
                : R(0);
   };
-  // g at a cell, masked by the limiter's branch outcome there (LIM)
-  auto ldg = [&](int k, int j, int i) -> R {
-    if (!(k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx)) return R(0);
-    const int q = k * plane + j * nx + i;
-    const R v = g[q];
-    if constexpr (LIM) {
-      const R y = allencahn_point(x[q], i > 0 ? x[q - 1] : R(0), i < nx - 1 ? x[q + 1] : R(0),
-                                  j > 0 ? x[q - nx] : R(0), j < ny - 1 ? x[q + nx] : R(0),
-                                  k > 0 ? x[q - plane] : R(0), k < nz - 1 ? x[q + plane] : R(0),
-                                  D, C);
-      return (y < lim.lo || y > lim.hi) ? R(0) : v;
-    }
-    return v;
-  };
+  auto ldg = [&](int k, int j, int i) -> R { return ld(g, k, j, i); };
   const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
   int hly, hlx;
   ac_halo_cell(tid, &hly, &hlx);
@@ -837,6 +817,142 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   if (DP) {
     __syncthreads();
     dp_commit(dp, t.b, a0, a1);
+  }
+}
+
+// The limiter's adjoint, g'[m] = (k0 - k1*x[m]^2) * gm[m] + D * sum_nbr gm,
+// with gm = g where the step's unlimited value (re-evaluated from x =
+// x_{t-1} with the forward's expression) lies in [lo, hi] and 0 elsewhere.
+// The masked plane k+1 is formed in iteration k: x(k+1) is staged in LDS
+// with a two-cell ring (the masks of g's one-cell ring need their own xy
+// neighbours), x(k) and x(k+2) at the thread's cells and ring cell stay in
+// registers, so every mask is evaluated from on-chip values and x is read
+// from HBM about once per point.
+template <class R, bool NT>
+__global__ __launch_bounds__(kThreads) void adj_allencahn3d7_lim(const R* __restrict__ x,
+                                                                 const R* __restrict__ g,
+                                                                 R* __restrict__ gp, int nx,
+                                                                 int ny, int nz, int tiles_x,
+                                                                 int tiles_y, int ntiles, R D,
+                                                                 R k0, R k1, R C, Limit<R> lim) {
+  constexpr int LY = kAcTY + 2, LX = kAcTX + 2;          // g: one-cell ring
+  constexpr int XY = kAcTY + 4, XX = kAcTX + 4;          // x: two-cell ring
+  __shared__ R tile[LY][LX];
+  __shared__ R xt[XY][XX];
+  AcTile t;
+  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;  // the whole block
+  const int plane = nx * ny;
+  auto in = [&](int k, int j, int i) {
+    return k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx;
+  };
+  auto ld = [&](const R* a, int k, int j, int i) -> R {
+    return in(k, j, i) ? a[k * plane + j * nx + i] : R(0);
+  };
+  auto keep = [&](R y) { return !(y < lim.lo || y > lim.hi); };
+  // g at a cell masked from global memory (the first planes only)
+  auto ldg = [&](int k, int j, int i) -> R {
+    if (!in(k, j, i)) return R(0);
+    const int q = k * plane + j * nx + i;
+    const R y = allencahn_point(x[q], i > 0 ? x[q - 1] : R(0), i < nx - 1 ? x[q + 1] : R(0),
+                                j > 0 ? x[q - nx] : R(0), j < ny - 1 ? x[q + nx] : R(0),
+                                k > 0 ? x[q - plane] : R(0), k < nz - 1 ? x[q + plane] : R(0),
+                                D, C);
+    return keep(y) ? g[q] : R(0);
+  };
+  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
+  const int i0 = t.bx * kAcTX, j0 = t.by * kAcTY;
+  // this thread's cell of g's ring (tile coordinates hly-1, hlx-1), if any
+  int hly, hlx;
+  ac_halo_cell(tid, &hly, &hlx);
+  const bool hr = hly >= 0;
+  const int hj = j0 + hly - 1, hi = i0 + hlx - 1;
+  // this thread's cell of x's outer ring, or one of the four corners of
+  // g's ring (which g's ring cells need as x neighbours), in x-tile
+  // coordinates, if any: 2*68 + 2*10 + 4 = 160 cells
+  int oy = -1, ox = 0;
+  if (tid < XX) {
+    oy = 0;
+    ox = tid;
+  } else if (tid < 2 * XX) {
+    oy = XY - 1;
+    ox = tid - XX;
+  } else if (tid < 2 * XX + LY) {
+    oy = tid - 2 * XX + 1;
+    ox = 0;
+  } else if (tid < 2 * XX + 2 * LY) {
+    oy = tid - 2 * XX - LY + 1;
+    ox = XX - 1;
+  } else if (tid < 2 * XX + 2 * LY + 4) {
+    const int c = tid - 2 * XX - 2 * LY;
+    oy = (c & 2) ? XY - 2 : 1;
+    ox = (c & 1) ? XX - 2 : 1;
+  }
+  const bool orr = oy >= 0;
+  const int oj = j0 + oy - 2, oi = i0 + ox - 2;
+  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
+  // masked g: planes k-1, k at the thread's cells, plane k at its ring cell
+  R belowA = ldg(t.z0 - 1, t.ja, t.i), belowB = ldg(t.z0 - 1, t.jb, t.i);
+  R curA = ldg(t.z0, t.ja, t.i), curB = ldg(t.z0, t.jb, t.i);
+  R halo = hr ? ldg(t.z0, hj, hi) : R(0);
+  // x at planes k, k+1 (the thread's cells and ring cell), outer ring at k+1
+  R xA0 = ld(x, t.z0, t.ja, t.i), xB0 = ld(x, t.z0, t.jb, t.i);
+  R xA1 = ld(x, t.z0 + 1, t.ja, t.i), xB1 = ld(x, t.z0 + 1, t.jb, t.i);
+  R xr0 = hr ? ld(x, t.z0, hj, hi) : R(0), xr1 = hr ? ld(x, t.z0 + 1, hj, hi) : R(0);
+  R xo1 = orr ? ld(x, t.z0 + 1, oj, oi) : R(0);
+  for (int k = t.z0; k < t.z1; ++k) {
+    // plane k+1's g, plane k+2's x and the outer ring of plane k+2 (for the
+    // next iteration) are requested before this plane is computed
+    const R gA = ld(g, k + 1, t.ja, t.i), gB = ld(g, k + 1, t.jb, t.i);
+    const R gr = hr ? ld(g, k + 1, hj, hi) : R(0);
+    const R xA2 = ld(x, k + 2, t.ja, t.i), xB2 = ld(x, k + 2, t.jb, t.i);
+    const R xr2 = hr ? ld(x, k + 2, hj, hi) : R(0);
+    const R xo2 = orr ? ld(x, k + 2, oj, oi) : R(0);
+    __syncthreads();
+    tile[ty + 1][tx + 1] = curA;
+    tile[ty + 5][tx + 1] = curB;
+    if (hr) tile[hly][hlx] = halo;
+    xt[ty + 2][tx + 2] = xA1;
+    xt[ty + 6][tx + 2] = xB1;
+    if (hr) xt[hly + 1][hlx + 1] = xr1;
+    if (orr) xt[oy][ox] = xo1;
+    __syncthreads();
+    // the masks of plane k+1 (x-tile position r, c; x(k) and x(k+2) there)
+    auto masked = [&](int r, int c, R xb, R xa, R gv) {
+      const R y = allencahn_point(xt[r][c], xt[r][c - 1], xt[r][c + 1], xt[r - 1][c],
+                                  xt[r + 1][c], xb, xa, D, C);
+      return keep(y) ? gv : R(0);
+    };
+    const R aboveA = masked(ty + 2, tx + 2, xA0, xA2, gA);
+    const R aboveB = masked(ty + 6, tx + 2, xB0, xB2, gB);
+    const R halon = hr ? masked(hly + 1, hlx + 1, xr0, xr2, gr) : R(0);
+    if (va) {
+      R s = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
+      s += tile[ty][tx + 1];
+      s += tile[ty + 2][tx + 1];
+      s += belowA;
+      s += aboveA;
+      put<NT>(&gp[k * plane + t.ja * nx + t.i], (k0 - k1 * (xA0 * xA0)) * curA + D * s);
+    }
+    if (vb) {
+      R s = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
+      s += tile[ty + 4][tx + 1];
+      s += tile[ty + 6][tx + 1];
+      s += belowB;
+      s += aboveB;
+      put<NT>(&gp[k * plane + t.jb * nx + t.i], (k0 - k1 * (xB0 * xB0)) * curB + D * s);
+    }
+    belowA = curA;
+    belowB = curB;
+    curA = aboveA;
+    curB = aboveB;
+    halo = halon;
+    xA0 = xA1;
+    xB0 = xB1;
+    xA1 = xA2;
+    xB1 = xB2;
+    xr0 = xr1;
+    xr1 = xr2;
+    xo1 = xo2;
   }
 }
 
@@ -1416,22 +1532,26 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
       const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
       const bool str = streams(s) != 0, lm = adjoint_applies_limit(s, dp_part != nullptr);
       const Limit<R> lim{R(s.lo), R(s.hi)};
-#define ADST_AC_ADJ(DPV, NTV, LIMV)                                                  \
-  adj_allencahn3d7<R, DPV, NTV, LIMV><<<grid, block, 0, st>>>(                       \
-      x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, D, k0, k1, dp, C, lim)
+#define ADST_AC_ADJ(DPV, NTV)                                                        \
+  adj_allencahn3d7<R, DPV, NTV><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, \
+                                                         D, k0, k1, dp)
+#define ADST_AC_LIM(NTV)                                                             \
+  adj_allencahn3d7_lim<R, NTV><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, \
+                                                        D, k0, k1, C, lim)
       if (dp_part && str)
-        ADST_AC_ADJ(true, true, false);
+        ADST_AC_ADJ(true, true);
       else if (dp_part)
-        ADST_AC_ADJ(true, false, false);
+        ADST_AC_ADJ(true, false);
       else if (lm && str)
-        ADST_AC_ADJ(false, true, true);
+        ADST_AC_LIM(true);
       else if (lm)
-        ADST_AC_ADJ(false, false, true);
+        ADST_AC_LIM(false);
       else if (str)
-        ADST_AC_ADJ(false, true, false);
+        ADST_AC_ADJ(false, true);
       else
-        ADST_AC_ADJ(false, false, false);
+        ADST_AC_ADJ(false, false);
 #undef ADST_AC_ADJ
+#undef ADST_AC_LIM
       break;
     }
     case ADST_VARDIFF2D9: {
