@@ -34,9 +34,13 @@ KERNELS = {  # (forward, adjoint) kernel names as rocprofv3 reports them
 }
 
 
-def kernel_name(kind, adj, n):
-    """Short name of the kernel an action of n steps launches."""
+def kernel_name(kind, adj, n, xpass=False):
+    """Short name of the kernel an action of n steps launches (xpass: the
+    Jacobi adjoint that also reads x_{t-1}, for the limiter or the
+    constants' gradients)."""
     base = KERNELS[kind][1 if adj else 0]
+    if adj and xpass and kind == 0 and n == 1:
+        return "jacobi_lim_adjoint"
     if kind == 3 or n == 1:
         return base
     if kind == 1:
@@ -46,14 +50,14 @@ def kernel_name(kind, adj, n):
     return f"jacobi_march<{'adj' if adj else 'fwd'},{n}>"
 
 
-def kernel_mix(kind, acts, adj):
+def kernel_mix(kind, acts, adj, xpass=False):
     """Action count per kernel name over a plan's forward or adjoint actions
     (a pipelined run of the in-place kind counts once)."""
     ops = (2, 4, 6) if adj else (0, 3, 5)  # ADJ, ADJ2, ADJW / FWD, FWD2, FWDW
     mix = {}
     for op, _t, _s, _d, n in acts:
         if op in ops:
-            k = kernel_name(kind, adj, n)
+            k = kernel_name(kind, adj, n, xpass)
             mix[k] = mix.get(k, 0) + 1
     return mix
 def kernel_source(kernel):
@@ -269,7 +273,7 @@ def main():
         mix = kernel_mix(w.kind, acts, False)
         ms_k, per_pt, units, nl, ns = ms_fwd, fwd_B, fwd_units, n_fwd, info.fwd_steps_total
     else:
-        mix = kernel_mix(w.kind, acts, True)
+        mix = kernel_mix(w.kind, acts, True, bool(args.dparams or args.limit))
         ms_k, per_pt, units, nl, ns = acc["ms_adj"], adj_B, adj_units, n_adj, info.adj_steps
     kernel = max(mix, key=lambda k: mix[k]) if mix else "none"
     alg_total = per_pt * w.npoints * units

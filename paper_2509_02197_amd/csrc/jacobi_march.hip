@@ -104,8 +104,10 @@ struct MarchGrid {
 
 // This workgroup's strip and chunk of rows [r0, r1); false when the
 // workgroup has no work (the grid is rounded up to whole XCD shares).
+// item (optional): the work item's index, edge items first, unique in
+// [0, nedge*ce + (ns-nedge)*ci).
 __device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* chunk, int* r0,
-                                  int* r1) {
+                                  int* r1, int* item = nullptr) {
   const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
   int nch, mid;
   if (slot < g.pe) {
@@ -115,6 +117,7 @@ __device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* c
     *chunk = t % g.ce;
     nch = g.ce;
     mid = kEdgeRows;
+    if (item) *item = t;
   } else {
     const int t = xcd * g.pi + (slot - g.pe);
     if (t >= (g.ns - g.nedge) * g.ci) return false;
@@ -122,6 +125,7 @@ __device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* c
     *chunk = t % g.ci;
     nch = g.ci;
     mid = kRows;
+    if (item) *item = g.nedge * g.ce + t;
   }
   // kEndRows at each end of the strip, mid rows between
   const int c = *chunk;
@@ -456,23 +460,30 @@ hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
 // masked g rows: when input row p arrives, row p-1 is masked (its x
 // neighbourhood is complete) and row p-2 transposed. The mask reads x one
 // column beyond the masked g, so strips overlap by V >= 2 columns.
-template <class R, bool VEC>
+// DP (instead of the mask): g passes unmasked and the pass adds this step's
+// share of dL/dw, sum over interior points of g[c] * ((((x[c]+x[W])+x[E])
+// +x[S])+x[N]) (the forward's sum, in double), over the work item's output
+// points; a wave butterfly then adds it into the item's slot
+// (dp_part[item], or overwrites it on the step t = T).
+template <class R, bool VEC, bool DP>
 __global__ __launch_bounds__(kLanes) void jacobi_lim_adjoint(const R* __restrict__ x,
                                                              const R* __restrict__ g,
                                                              R* __restrict__ gp, int nx, int ny,
-                                                             MarchGrid grid, R w, R lo, R hi) {
+                                                             MarchGrid grid, R w, R lo, R hi,
+                                                             double* dp_part, int dp_first) {
   // six rows of each array in flight: the pass is lighter than the n-step
   // march and registers allow it
   constexpr int V = 16 / sizeof(R), H = V, OW = kLanes * V - 2 * H, P = 6, U = kUnroll;
   static_assert(H >= 2, "the mask reaches two columns beyond an output");
   static_assert(U % P == 0, "register slots must stay static");
   typedef R vec_t __attribute__((ext_vector_type(V)));
-  int strip, chunk, r0, r1;
-  if (!march_item(grid, ny, &strip, &chunk, &r0, &r1)) return;
+  int strip, chunk, r0, r1, item;
+  if (!march_item(grid, ny, &strip, &chunk, &r0, &r1, &item)) return;
   const int lane = threadIdx.x;
   const int s0 = strip * OW;
   const int c0 = s0 - H + lane * V;
   const int nit = (r1 - r0) + 4;  // input rows r0-2 .. r1+1
+  double a0 = 0.0;
   const int lo_need = max(r0 - 2, 0), hi_need = min(r1 + 1, ny - 1);
   auto cin = [&](int c) { return c >= 1 && c <= nx - 2; };
   bool cok[V], cI[V], cW[V], cE[V];
@@ -541,13 +552,20 @@ __global__ __launch_bounds__(kLanes) void jacobi_lim_adjoint(const R* __restrict
           const R* N = xw[DIR > 0 ? sNew : sOld];
           const R wl = from_prev(a[V - 1]), er = from_next(a[0]);
           const bool rm = m >= 1 && m <= ny - 2;
+          const bool own = m >= r0 && m < r1 && st_lane;  // this item's output row
 #pragma unroll
           for (int e = 0; e < V; ++e) {
             const R Wn = e > 0 ? a[e > 0 ? e - 1 : 0] : wl;
             const R En = e < V - 1 ? a[e < V - 1 ? e + 1 : 0] : er;
-            const R f = w * ((((a[e] + Wn) + En) + S[e]) + N[e]);
-            const R yv = (MODE == kFast || (cI[e] && rm)) ? f : a[e];
-            mg[sc][e] = (yv < lo || yv > hi) ? R(0) : gr[sc][e];
+            const R sum = (((a[e] + Wn) + En) + S[e]) + N[e];
+            if constexpr (DP) {
+              mg[sc][e] = gr[sc][e];
+              if ((MODE == kFast || (cI[e] && rm)) && own)
+                a0 += (double)gr[sc][e] * (double)sum;
+            } else {
+              const R yv = (MODE == kFast || (cI[e] && rm)) ? w * sum : a[e];
+              mg[sc][e] = (yv < lo || yv > hi) ? R(0) : gr[sc][e];
+            }
           }
         }
         {  // transpose row index rr-2 from masked rows rr-3 .. rr-1
@@ -626,11 +644,18 @@ __global__ __launch_bounds__(kLanes) void jacobi_lim_adjoint(const R* __restrict
     else
       march(Up{}, General{});
   }
+  if constexpr (DP) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) a0 += __shfl_xor(a0, off, kLanes);
+    if (lane == 0) dp_part[item] = dp_first ? a0 : dp_part[item] + a0;
+  }
 }
 
+// One pass reading x and g: the limiter's masked adjoint (dp_part null) or
+// the adjoint with dL/dw's share (dp_part: jacobi_x_adjoint_slots doubles).
 template <class R>
 hipError_t lim_adjoint_launch(const StepShape& s, const R* x, const R* g, R* gp,
-                              hipStream_t st) {
+                              double* dp_part, bool dp_first, hipStream_t st) {
   constexpr int V = 16 / sizeof(R), OW = kLanes * V - 2 * V;
   MarchGrid grid;
   int64_t blocks;
@@ -638,12 +663,21 @@ hipError_t lim_adjoint_launch(const StepShape& s, const R* x, const R* g, R* gp,
   const bool vec = s.nx % V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(g) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(gp) & 15u) == 0;
-  if (vec)
-    jacobi_lim_adjoint<R, true><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
-        x, g, gp, s.nx, s.ny, grid, R(s.p0), R(s.lo), R(s.hi));
+  const dim3 gr((unsigned)blocks), bl(kLanes);
+  const R w = R(s.p0), lo = R(s.lo), hi = R(s.hi);
+  const int first = dp_first ? 1 : 0;
+  if (dp_part && vec)
+    jacobi_lim_adjoint<R, true, true><<<gr, bl, 0, st>>>(x, g, gp, s.nx, s.ny, grid, w, lo, hi,
+                                                         dp_part, first);
+  else if (dp_part)
+    jacobi_lim_adjoint<R, false, true><<<gr, bl, 0, st>>>(x, g, gp, s.nx, s.ny, grid, w, lo, hi,
+                                                          dp_part, first);
+  else if (vec)
+    jacobi_lim_adjoint<R, true, false><<<gr, bl, 0, st>>>(x, g, gp, s.nx, s.ny, grid, w, lo, hi,
+                                                          nullptr, 0);
   else
-    jacobi_lim_adjoint<R, false><<<dim3((unsigned)blocks), dim3(kLanes), 0, st>>>(
-        x, g, gp, s.nx, s.ny, grid, R(s.p0), R(s.lo), R(s.hi));
+    jacobi_lim_adjoint<R, false, false><<<gr, bl, 0, st>>>(x, g, gp, s.nx, s.ny, grid, w, lo,
+                                                           hi, nullptr, 0);
   return hipGetLastError();
 }
 
@@ -668,9 +702,28 @@ hipError_t launch_jacobi_lim_adjoint(const StepShape& s, const void* x, const vo
   if (s.dtype == ADST_F64)
     return lim_adjoint_launch<double>(s, static_cast<const double*>(x),
                                       static_cast<const double*>(g), static_cast<double*>(gp),
-                                      stream);
+                                      nullptr, false, stream);
   return lim_adjoint_launch<float>(s, static_cast<const float*>(x), static_cast<const float*>(g),
-                                   static_cast<float*>(gp), stream);
+                                   static_cast<float*>(gp), nullptr, false, stream);
+}
+
+hipError_t launch_jacobi_dp_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
+                                    double* dp_part, bool dp_first, hipStream_t stream) {
+  if (s.kind != ADST_JACOBI2D5 || !x || !dp_part) return hipErrorInvalidValue;
+  if (s.dtype == ADST_F64)
+    return lim_adjoint_launch<double>(s, static_cast<const double*>(x),
+                                      static_cast<const double*>(g), static_cast<double*>(gp),
+                                      dp_part, dp_first, stream);
+  return lim_adjoint_launch<float>(s, static_cast<const float*>(x), static_cast<const float*>(g),
+                                   static_cast<float*>(gp), dp_part, dp_first, stream);
+}
+
+int64_t jacobi_x_adjoint_slots(const StepShape& s) {
+  const int V = s.dtype == ADST_F64 ? 2 : 4, OW = kLanes * V - 2 * V;  // as lim_adjoint_launch
+  MarchGrid g;
+  int64_t blocks;
+  if (!make_grid(s.nx, s.ny, OW, &g, &blocks)) return 0;
+  return int64_t(g.nedge) * g.ce + int64_t(g.ns - g.nedge) * g.ci;
 }
 
 hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32_t n, bool adjoint,

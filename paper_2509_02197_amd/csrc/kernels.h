@@ -49,6 +49,14 @@ hipError_t launch_jacobi_march(const StepShape& s, const void* x, void* y, int32
 hipError_t launch_jacobi_lim_adjoint(const StepShape& s, const void* x, const void* g_next,
                                      void* g_prev, hipStream_t stream);
 
+// Jacobi: one adjoint step and its share of dL/dw in the same one-pass
+// layout, into jacobi_x_adjoint_slots(s) per-work-item slots of dp_part
+// (overwritten when dp_first, else added to).
+hipError_t launch_jacobi_dp_adjoint(const StepShape& s, const void* x, const void* g_next,
+                                    void* g_prev, double* dp_part, bool dp_first,
+                                    hipStream_t stream);
+int64_t jacobi_x_adjoint_slots(const StepShape& s);
+
 // g_prev = J_t^T g_next with x = x_{t-1} (may be null when the kind's adjoint
 // reads no state and neither dK nor the constants' gradients are asked for).
 // dK (nullable) is accumulated: dK = (dk_first ? 0 : dK) + contribution of

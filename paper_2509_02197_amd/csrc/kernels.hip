@@ -392,50 +392,6 @@ __global__ __launch_bounds__(kJacTW) void adj_jacobi2d5(const R* __restrict__ g,
                                                         int tiles_x, int ntiles, int vec, R w) {
   jacobi_tile<R, true>(g, gp, nx, ny, tiles_x, ntiles, vec, w);
 }
-// Adjoint step with its share of dL/dw: the tile of x_{t-1} is staged beside
-// g's (tiles of kJacDpTR rows, so two staged arrays leave room for as many
-// workgroups per CU as one array of kJacTR rows). Threads past the grid's
-// last column take part in the block sum.
-constexpr int kJacDpTR = 4;
-template <class R>
-__global__ __launch_bounds__(kJacTW) void adj_jacobi2d5_dp(const R* __restrict__ x,
-                                                           const R* __restrict__ g,
-                                                           R* __restrict__ gp, int nx, int ny,
-                                                           int tiles_x, int ntiles, int vec, R w,
-                                                           DpOut dp) {
-  using G = Tile2<R, kJacTW, kJacDpTR>;
-  __shared__ R sg[G::LR * G::LW];
-  __shared__ R sx[G::LR * G::LW];
-  const int b = xcd_tile(ntiles);
-  if (b >= ntiles) return;  // the whole block
-  const int i0 = (b % tiles_x) * kJacTW, j0 = (b / tiles_x) * kJacDpTR;
-  stage_rows<R, kJacTW, G::LR, G::LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
-  stage_rows<R, kJacTW, G::LR, G::LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
-  __syncthreads();
-  const int i = i0 + (int)threadIdx.x;
-  const int cx = G::V + (int)threadIdx.x;
-  const bool avg = jacobi_all_avg<true>(i0, i0 + kJacTW - 1, j0, j0 + kJacDpTR - 1, nx, ny);
-  double a0 = 0.0;
-  if (i < nx) {
-#pragma unroll
-    for (int r = 0; r < kJacDpTR; ++r) {
-      const int j = j0 + r;
-      if (j >= ny) break;
-      const int q = (r + 1) * G::LW + cx;
-      gp[j * nx + i] = avg ? jacobi_adj_inner_at<R, G::LW>(sg, q, w)
-                           : jacobi_adj_at<R, G::LW>(sg, q, i, j, nx, ny, w);
-      if (i > 0 && i < nx - 1 && j > 0 && j < ny - 1) {
-        R sum = sx[q];
-        sum += sx[q - 1];
-        sum += sx[q + 1];
-        sum += sx[q - G::LW];
-        sum += sx[q + G::LW];
-        a0 += (double)sg[q] * (double)sum;
-      }
-    }
-  }
-  dp_commit(dp, b, a0, 0.0);
-}
 template <class R>
 __global__ __launch_bounds__(kX2Threads) void fwd_jacobi2d5_x2(const R* __restrict__ x,
                                                                R* __restrict__ y, int nx, int ny,
@@ -1515,13 +1471,17 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
   switch (s.kind) {
     case ADST_JACOBI2D5: {
       const int tx = cdiv(s.nx, kJacTW), nt = tx * cdiv(s.ny, kJacTR);
-      if (dp_part)
-        adj_jacobi2d5_dp<R><<<dim3(xcd_grid(tx * cdiv(s.ny, kJacDpTR))), dim3(kJacTW), 0, st>>>(
-            x, g, gp, s.nx, s.ny, tx, tx * cdiv(s.ny, kJacDpTR), vec_ok<R>(s.nx, g, x), R(s.p0),
-            dp);
-      else
-        adj_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
-            g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
+      if (dp_part) {
+        // slot layout: nslots for w, then nslots for the unused second constant
+        const int64_t n = dparam_slots(s);
+        if (dp_first) {
+          const hipError_t e = launch_fill_zero(dp_part + n, n * (int64_t)sizeof(double), st);
+          if (e != hipSuccess) return e;
+        }
+        return launch_jacobi_dp_adjoint(s, xv, gv, gpv, dp_part, dp_first, st);
+      }
+      adj_jacobi2d5<R><<<dim3(xcd_grid(nt)), dim3(kJacTW), 0, st>>>(
+          g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
       break;
     }
     case ADST_ALLENCAHN3D7: {
@@ -1733,7 +1693,7 @@ hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, v
 
 int64_t dparam_slots(const StepShape& s) {
   switch (s.kind) {
-    case ADST_JACOBI2D5: return int64_t(cdiv(s.nx, kJacTW)) * cdiv(s.ny, kJacDpTR);
+    case ADST_JACOBI2D5: return jacobi_x_adjoint_slots(s);
     case ADST_ALLENCAHN3D7:
       return int64_t(cdiv(s.nx, kAcTX)) * cdiv(s.ny, kAcTY) * cdiv(s.nz, kAcZC);
     case ADST_VARDIFF2D9: return int64_t(cdiv(s.nx, kVdTW)) * cdiv(s.ny, kVdAdjTR);

@@ -162,17 +162,25 @@ def test_gradient_mask():
     plain = adst.adst_plan(pj, 5, BIG, 0)
     withp = adst.adst_plan(pj, 5, BIG, 0, adst.ADST_GRAD_PARAMS)
     assert plain.needs_state == 0 and withp.needs_state == 1 and withp.slots == 3
-    # their slots (one per adjoint workgroup and constant: an 8 x 8 grid is two
-    # 256 x 4 tiles, so 4 doubles) sit after the checkpoint slots, 4 KiB aligned
+    # their slots (one per adjoint workgroup and constant: an 8 x 8 grid is one
+    # work item, so 2 doubles) sit after the checkpoint slots, 4 KiB aligned
     S = 8 * 8 * 8
     stride = -(-S // 4096) * 4096
     assert withp.workspace_bytes == 16384 + (3 + 3) * stride + 4096
     # bytes: every adjoint step also reads x_{t-1} for the partials
     assert withp.alg_bytes - (16 * 5 + 16 * 5 + 16) * 64 == 8 * 5 * 64
-    # slot counts follow the adjoint tiles: Jacobi 256 x 4, Allen-Cahn 64 x 8 x 32,
-    # variable coefficients 256 x 4 (2 doubles per tile, 4 KiB aligned)
-    for kind, dims, tiles in [(adst.ADST_JACOBI2D5, (600, 100, 1), 3 * 25),
-                              (adst.ADST_JACOBI2D5, (4096, 4096, 1), 16 * 1024),
+    # slot counts follow the adjoint's work items: Jacobi one per column strip
+    # (124 columns in f64) and row chunk (12 rows in the two edge strips, 48
+    # in the others, 6 at each end), Allen-Cahn 64 x 8 x 32 tiles, variable
+    # coefficients 256 x 4 tiles (2 doubles per item, 4 KiB aligned)
+    def march_items(nx, ny):
+        ns = -(-nx // 124)
+        chunks = lambda mid: 2 + -(-(ny - 12) // mid) if ny > 12 else 1
+        nedge = 2 if ns >= 2 else 1
+        return nedge * chunks(12) + (ns - nedge) * chunks(48)
+    assert march_items(600, 100) == 2 * 10 + 3 * 4
+    for kind, dims, tiles in [(adst.ADST_JACOBI2D5, (600, 100, 1), march_items(600, 100)),
+                              (adst.ADST_JACOBI2D5, (4096, 4096, 1), march_items(4096, 4096)),
                               (adst.ADST_ALLENCAHN3D7, (65, 9, 33), 2 * 2 * 2),
                               (adst.ADST_VARDIFF2D9, (257, 9, 1), 2 * 3)]:
         dt = adst.ADST_F32 if kind == adst.ADST_VARDIFF2D9 else adst.ADST_F64
