@@ -1115,8 +1115,19 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   stage_rows<R, kVdTW, G::LR, LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
   stage_rows<R, kVdTW, G::LR, LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
   if (XS) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
-  __syncthreads();
   const int i = i0 + (int)threadIdx.x;
+  // the accumulated dK of the thread's cells, requested with the staged
+  // rows (where the row loop is unrolled, so the registers stay static)
+  constexpr bool PRE = WANT_DK && !DP;
+  R dk0[PRE ? TR : 1];
+  if (PRE) {
+#pragma unroll
+    for (int r = 0; r < TR; ++r) {
+      const int j = j0 + r;
+      dk0[PRE ? r : 0] = (!dk_first && i < nx && j < ny) ? dK[j * nx + i] : R(0);
+    }
+  }
+  __syncthreads();
   const int cx = G::V + (int)threadIdx.x;
   const bool xin = i > 0 && i < nx - 1;
   double a0 = 0.0;
@@ -1163,7 +1174,8 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
       }
       const int o = j * nx + i;
       put<NT>(&gp[o], gc + dt * ag);
-      if (WANT_DK) put<NT>(&dK[o], (dk_first ? R(0) : dK[o]) + dt * ak);
+      if (WANT_DK)
+        put<NT>(&dK[o], (PRE ? dk0[PRE ? r : 0] : (dk_first ? R(0) : dK[o])) + dt * ak);
       if (DP) a0 += (double)gc * (double)acc;
 #pragma unroll
       for (int c = 0; c < 3; ++c) {
