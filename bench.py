@@ -50,15 +50,43 @@ def kernel_name(kind, adj, n, xpass=False):
     return f"jacobi_march<{'adj' if adj else 'fwd'},{n}>"
 
 
-def kernel_mix(kind, acts, adj, xpass=False):
-    """Action count per kernel name over a plan's forward or adjoint actions
-    (a pipelined run of the in-place kind counts once)."""
+STORE_DEPTH = {1: 3, 2: 2}  # single steps per store-through launch (Allen-Cahn, VarDiff)
+
+
+def stored_run(acts, i, depth):
+    """Length of the run of chained single forward steps from acts[i] that
+    adst_vjp takes in one launch writing every state (1: none)."""
+    if depth < 2 or acts[i][0] != 0:
+        return 1
+    n = 1
+    while n < depth and i + n < len(acts):
+        a, p = acts[i + n], acts[i + n - 1]
+        if a[0] != 0 or a[2] != p[3] or a[1] != p[1] + 1:
+            break
+        if a[3] == acts[i][2] or any(acts[i + k][3] == a[3] for k in range(n)):
+            break
+        n += 1
+    return n
+
+
+def kernel_mix(kind, acts, adj, xpass=False, store_depth=1):
+    """Launch count per kernel name over a plan's forward or adjoint actions
+    (a pipelined run of the in-place kind counts once, and so does a run of
+    single forward steps that one store-through launch takes)."""
     ops = (2, 4, 6) if adj else (0, 3, 5)  # ADJ, ADJ2, ADJW / FWD, FWD2, FWDW
     mix = {}
-    for op, _t, _s, _d, n in acts:
+    i = 0
+    while i < len(acts):
+        op, n = acts[i][0], acts[i][4]
+        r = 1 if adj else stored_run(acts, i, store_depth)
         if op in ops:
-            k = kernel_name(kind, adj, n, xpass)
+            if r >= 2:
+                k = (f"{KERNELS[kind][0]}_n<{r},store>" if kind == 1
+                     else f"{KERNELS[kind][0]}_x2<store>")
+            else:
+                k = kernel_name(kind, adj, n, xpass)
             mix[k] = mix.get(k, 0) + 1
+        i += r
     return mix
 
 
@@ -262,7 +290,6 @@ def main():
     # time. avg_launch_ms is the phase's time over its kernel dispatches; the
     # kernel named is the phase's most frequent one, kernel_mix the rest.
     isz = 8 if w.dtype == adst.ADST_F64 else 4
-    fwd_B = {0: 2, 1: 2, 2: 3, 3: 2}[w.kind] * isz
     adj_B = {0: 2, 1: 3, 2: 6 if w.want_dK else 3, 3: 2}[w.kind] * isz
     if args.dparams and (w.kind == adst.ADST_JACOBI2D5 or
                          (w.kind == adst.ADST_VARDIFF2D9 and not w.want_dK)):
@@ -270,21 +297,24 @@ def main():
     elif args.limit and w.kind == adst.ADST_JACOBI2D5:
         adj_B += isz  # the adjoint applies the branch mask, reading x_{t-1}
     in_place = w.kind == adst.ADST_GAUSSSEIDEL2D5
-    # units of fwd_B * npoints moved per call: one per launch, or one per step
-    fwd_units = info.fwd_steps_total if in_place else info.fwd_launches
+    # units of adj_B * npoints moved per call: one per launch, or one per step;
+    # the forward launches' bytes come from the plan (a store-through launch
+    # of n steps moves its input once and each of its n states once)
     adj_units = info.adj_steps if in_place else info.adj_launches
+    fwd_total = info.fwd_alg_bytes
+    store_depth = 1 if (args.no_fuse or args.limit) else STORE_DEPTH.get(w.kind, 1)
     n_fwd, n_adj = info.fwd_kernels, info.adj_kernels
     ms_fwd = acc["ms_fwd_sweep"] + acc["ms_fwd_recompute"]
     fwd_avg = ms_fwd / max(n_fwd, 1)
     adj_avg = acc["ms_adj"] / max(n_adj, 1)
     if ms_fwd >= acc["ms_adj"]:
-        mix = kernel_mix(w.kind, acts, False)
-        ms_k, per_pt, units, nl, ns = ms_fwd, fwd_B, fwd_units, n_fwd, info.fwd_steps_total
+        mix = kernel_mix(w.kind, acts, False, store_depth=store_depth)
+        ms_k, alg_total, nl, ns = ms_fwd, fwd_total, n_fwd, info.fwd_steps_total
     else:
         mix = kernel_mix(w.kind, acts, True, bool(args.dparams or args.limit))
-        ms_k, per_pt, units, nl, ns = acc["ms_adj"], adj_B, adj_units, n_adj, info.adj_steps
+        ms_k, nl, ns = acc["ms_adj"], n_adj, info.adj_steps
+        alg_total = adj_B * w.npoints * adj_units
     kernel = max(mix, key=lambda k: mix[k]) if mix else "none"
-    alg_total = per_pt * w.npoints * units
     avg_ms = ms_k / max(nl, 1)
     alg_bytes = alg_total / max(nl, 1)
     achieved = alg_total / (ms_k * 1e-3) / 1e9
@@ -296,7 +326,7 @@ def main():
         "avg_launch_ms": round(avg_ms, 5), "launches_per_step": nl,
         "steps_per_launch": round(ns / max(nl, 1), 3),
         "fwd_avg_ms": round(fwd_avg, 5),
-        "fwd_gbps": round(fwd_B * w.npoints * fwd_units / max(ms_fwd, 1e-9) / 1e6, 1),
+        "fwd_gbps": round(fwd_total / max(ms_fwd, 1e-9) / 1e6, 1),
         "adj_avg_ms": round(adj_avg, 5),
         "adj_gbps": round(adj_B * w.npoints * adj_units / max(acc["ms_adj"], 1e-9) / 1e6, 1),
     }

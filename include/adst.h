@@ -171,7 +171,13 @@ typedef struct {
  *                 pipelined the same way (its adjoint reads no state)
  * Fused and pipelined actions evaluate every point with the same expression
  * as the single steps, so results are bit-identical. `n` is the number of
- * steps an action covers (1 for FWD/ADJ, 0 for SEED). */
+ * steps an action covers (1 for FWD/ADJ, 0 for SEED).
+ * Consecutive FWD actions that form a chain (each reads the state the one
+ * before it wrote, into buffers all different from each other and from the
+ * chain's input) are run by adst_vjp as one launch per up to 3 (Allen-Cahn)
+ * or 2 (variable coefficients) of them, which writes every state of the run
+ * (a store-all run of the binomial schedule); fwd_kernels counts those
+ * launches. Not with ADST_NO_FUSE or ADST_LIMIT. */
 typedef enum {
   ADST_OP_FWD = 0,
   ADST_OP_SEED = 1,
@@ -223,6 +229,8 @@ typedef struct {
   float ms_total;           /*   first launch start to last launch end */
   float ms_dparams;         /*   ... of the constants' gradient sum (the final reduction; the
                                per-step shares run inside the adjoint launches) */
+  uint64_t fwd_alg_bytes;   /* algorithmic HBM bytes of the forward launches (sweep and
+                               recomputation; part of alg_bytes) */
 } adst_plan_info;
 
 /* Plan a forward+VJP call without touching the GPU (host only).

@@ -55,7 +55,7 @@ class adst_plan_info(ctypes.Structure):
                 ("alg_bytes", ctypes.c_uint64), ("ms_fwd_sweep", ctypes.c_float),
                 ("ms_fwd_recompute", ctypes.c_float), ("ms_adj", ctypes.c_float),
                 ("ms_seed", ctypes.c_float), ("ms_total", ctypes.c_float),
-                ("ms_dparams", ctypes.c_float)]
+                ("ms_dparams", ctypes.c_float), ("fwd_alg_bytes", ctypes.c_uint64)]
 
     def as_dict(self):
         return {f[0]: getattr(self, f[0]) for f in self._fields_}

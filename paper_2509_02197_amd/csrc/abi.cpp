@@ -46,6 +46,7 @@ struct Checked {
   bool needs_state = false;
   bool trace = false;
   int32_t fuse_fwd = 1, fuse_adj = 1;  // most steps per launch
+  int32_t store_fwd = 1;  // most single steps per launch that stores every state
   bool in_place = false;  // the Gauss-Seidel kind: pipelined sweeps, adjoint in place
   bool want_dk = false, want_dp = false;
 };
@@ -103,7 +104,27 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   out->fuse_fwd = (fuse && !limit) ? max_fused_forward(p->kind) : 1;
   out->fuse_adj = fuse ? max_fused_adjoint(p->kind, p->n[0]) : 1;
   out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
+  out->store_fwd = (fuse && !limit) ? max_stored_forward(p->kind) : 1;
   return ADST_OK;
+}
+
+// Length of the run of single forward steps starting at acts[i] that one
+// store-through launch takes (1: none): each action reads the state the one
+// before it wrote, and the states go to buffers that differ from each other
+// and from the run's input (which the launch reads while it writes them).
+int32_t stored_run(const std::vector<adst_action>& acts, size_t i, int32_t depth) {
+  if (depth < 2 || acts[i].op != ADST_OP_FWD) return 1;
+  int32_t n = 1;
+  while (n < depth && i + n < acts.size()) {
+    const adst_action& a = acts[i + n];
+    const adst_action& p = acts[i + n - 1];
+    if (a.op != ADST_OP_FWD || a.src != p.dst || a.t != p.t + 1) break;
+    bool clash = a.dst == acts[i].src;
+    for (int32_t k = 0; k < n; ++k) clash = clash || acts[i + k].dst == a.dst;
+    if (clash) break;
+    ++n;
+  }
+  return n;
 }
 
 struct Layout {
@@ -188,31 +209,40 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
   info->n_actions = (int64_t)plan.acts.size();
   info->fwd_launches = plan.fwd_launches;
   info->adj_launches = plan.adj_launches;
-  for (const adst_action& a : plan.acts) {
+  for (size_t i = 0; i < plan.acts.size(); ++i) {
+    const adst_action& a = plan.acts[i];
     const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
     const bool adj_op = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJ2 || a.op == ADST_OP_ADJW;
     if (!fwd_op && !adj_op) continue;
     const int64_t k = c.in_place ? gs_kernel_launches(c.shape, adj_op, a.n) : 1;
     (fwd_op ? info->fwd_kernels : info->adj_kernels) += k;
+    i += stored_run(plan.acts, i, c.store_fwd) - 1;
   }
   info->state_bytes = c.state_bytes;
   info->budget_bytes = budget;
   info->slot_bytes_peak = uint64_t(plan.slots) * c.state_bytes;
   info->workspace_bytes = L.total;
   info->fwd_workspace_bytes = (plan.steps >= 2 && !c.in_place) ? c.state_bytes : 0;
-  // A fused launch moves its inputs and outputs once for its n steps; a
-  // pipelined run of the in-place kind is counted as its n steps.
+  // A fused launch moves its inputs and outputs once for its n steps (a
+  // store-through run writes each of its n states); a pipelined run of the
+  // in-place kind is counted as its n steps.
   const uint64_t n = uint64_t(c.npoints);
-  uint64_t per_point = sb;
+  uint64_t per_point = sb, fwd_per_point = 0;
   bool first_adj = true;
-  for (const adst_action& a : plan.acts) {
+  for (size_t i = 0; i < plan.acts.size(); ++i) {
+    const adst_action& a = plan.acts[i];
     switch (a.op) {
-      case ADST_OP_FWD:
+      case ADST_OP_FWD: {
+        const int32_t r = stored_run(plan.acts, i, c.store_fwd);
+        fwd_per_point += fb + uint64_t(r - 1) * itemsize(c.shape.dtype);
+        i += r - 1;
+        break;
+      }
       case ADST_OP_FWD2:
-        per_point += fb;
+        fwd_per_point += fb;
         break;
       case ADST_OP_FWDW:
-        per_point += uint64_t(a.n) * fb;
+        fwd_per_point += uint64_t(a.n) * fb;
         break;
       case ADST_OP_ADJ:
       case ADST_OP_ADJ2:
@@ -227,7 +257,8 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
         break;
     }
   }
-  info->alg_bytes = n * per_point;
+  info->alg_bytes = n * (per_point + fwd_per_point);
+  info->fwd_alg_bytes = n * fwd_per_point;
 }
 
 adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
@@ -492,7 +523,8 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
   Tracer tr(c.trace);
   bool seeded = false;
   hipError_t e = hipSuccess;
-  for (const adst_action& a : plan.acts) {
+  for (size_t ai = 0; ai < plan.acts.size(); ++ai) {
+    const adst_action& a = plan.acts[ai];
     const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
     const Tracer::Cat cat = fwd_op               ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
                             : a.op == ADST_OP_SEED ? Tracer::SEED
@@ -509,9 +541,18 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
       continue;
     }
     switch (a.op) {
-      case ADST_OP_FWD:
-        e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+      case ADST_OP_FWD: {
+        const int32_t r = stored_run(plan.acts, ai, c.store_fwd);
+        if (r >= 2) {  // one launch writes the run's r states
+          void* ys[kMaxStoredRun];
+          for (int32_t k = 0; k < r; ++k) ys[k] = buffer(plan.acts[ai + k].dst);
+          e = launch_forward_store(c.shape, buffer(a.src), coeff, ys, r, stream);
+          ai += r - 1;
+        } else {
+          e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+        }
         break;
+      }
       case ADST_OP_FWD2:
         e = launch_forward_n(c.shape, buffer(a.src), coeff, buffer(a.dst), a.n, stream);
         break;

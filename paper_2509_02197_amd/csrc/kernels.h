@@ -34,6 +34,16 @@ int32_t max_fused_adjoint(int32_t kind, int64_t nx);
 hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, void* y, int32_t n,
                             hipStream_t stream);
 
+// A run of n single steps whose every state is kept (2 <= n <=
+// max_stored_forward): x_{t-n+1+k} = F^{k+1}(x_{t-n}) into ys[k] for
+// k = 0 .. n-1, in one launch that reads x once and writes each state once.
+// The ys are distinct and none overlaps x. Allen-Cahn and the
+// variable-coefficient kind only, without the limiter.
+constexpr int32_t kMaxStoredRun = kAcMaxFuse;
+int32_t max_stored_forward(int32_t kind);
+hipError_t launch_forward_store(const StepShape& s, const void* x, const void* K, void* const* ys,
+                                int32_t n, hipStream_t stream);
+
 // g_{t-n} = J_{t-n+1}^T ... J_t^T g_t in one launch, state-free adjoints.
 hipError_t launch_adjoint_n(const StepShape& s, const void* g_next, void* g_prev, int32_t n,
                             hipStream_t stream);

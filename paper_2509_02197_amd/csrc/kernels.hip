@@ -544,14 +544,22 @@ struct AcN {
   static constexpr int ZC = NZ;                                     // output planes
 };
 
-template <class R, int K, int RPT, int NZ, bool NT>
+// ST: the intermediate states are stored too, step l's into mid[l-1], each
+// point by the workgroup whose output tile holds it (a run of steps whose
+// every state is kept moves 8 + 8n bytes per point for n steps instead of
+// 16n).
+template <class R, int K, int RPT, int NZ, bool NT, bool ST>
 __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restrict__ x,
-                                                               R* __restrict__ y, int nx, int ny,
-                                                               int nz, int tiles_x, int tiles_y,
-                                                               int ntiles, R D, R C) {
+                                                               R* __restrict__ y,
+                                                               R* __restrict__ mid0,
+                                                               R* __restrict__ mid1, int nx,
+                                                               int ny, int nz, int tiles_x,
+                                                               int tiles_y, int ntiles, R D,
+                                                               R C) {
   using A = AcN<K, RPT, NZ>;
   constexpr int SX = A::SX, SY = A::SY, LX = SX + 2, LY = SY + 2, H = K - 1;
   static_assert(K >= 2 && 2 * LX + 2 * SY <= kThreads, "ring cells: one per thread");
+  static_assert(!ST || K <= 3, "intermediate states go to mid0 (step 1) and mid1 (step 2)");
   __shared__ R xt[LY][LX];
   __shared__ R yt[K - 1][SY][SX];  // steps 1 .. K-1
   int b = xcd_tile(ntiles);
@@ -591,6 +599,8 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
   R xp[RPT], xc[RPT], xn[RPT];
   R sb[K - 1][RPT], sc[K - 1][RPT], sn[K - 1][RPT];
   const int pfirst = z0 - K + 1, plast = z1 + K - 2;
+  // this thread's column lies in the output tile (rows are checked per cell)
+  const bool tile_col = tx >= H && tx < SX - H;
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
     const int j = j0 - H + row(q);
@@ -615,10 +625,14 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
 #pragma unroll
       for (int q = 0; q < RPT; ++q) {
         const int r = row(q);
-        sn[0][q] = (pin && inxy(j0 - H + r, ic))
-                       ? allencahn_point(xc[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
+        const bool cin = pin && inxy(j0 - H + r, ic);
+        sn[0][q] = cin ? allencahn_point(xc[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
                                          xt[r + 2][tx + 1], xp[q], xn[q], D, C)
                        : R(0);
+        if constexpr (ST) {
+          if (cin && tile_col && r >= H && r < SY - H && p >= z0 && p < z1)
+            put<NT>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
+        }
       }
     }
 #pragma unroll
@@ -635,10 +649,15 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
         const R v = ok ? allencahn_point(sc[l - 2][q], t[r][tx - 1], t[r][tx + 1], t[r - 1][tx],
                                          t[r + 1][tx], sb[l - 2][q], sn[l - 2][q], D, C)
                        : R(0);
-        if (l < K)
+        if (l < K) {
           sn[l - 1][q] = v;
-        else if (ok && pl >= z0 && pl < z1)
+          if constexpr (ST) {
+            if (ok && tile_col && r >= H && r < SY - H && pl >= z0 && pl < z1)
+              put<NT>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
+          }
+        } else if (ok && pl >= z0 && pl < z1) {
           put<NT>(&y[pl * plane + j * nx + ic], v);
+        }
       }
     }
     __syncthreads();
@@ -997,12 +1016,14 @@ __global__ __launch_bounds__(kVdTW) void fwd_vardiff2d9(const R* __restrict__ x,
 // read: the second step drops out-of-grid neighbours as the single step
 // does.
 constexpr int kVdX2TR = 8;
-template <class R, int TR, bool NT>
+// ST: the first step's state is stored too, into mid, on the tile's cells.
+template <class R, int TR, bool NT, bool ST>
 __global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restrict__ x,
                                                                 const R* __restrict__ K,
-                                                                R* __restrict__ y, int nx, int ny,
-                                                                int tiles_x, int ntiles, int vec,
-                                                                R dt, R ca, R cd) {
+                                                                R* __restrict__ y,
+                                                                R* __restrict__ mid, int nx,
+                                                                int ny, int tiles_x, int ntiles,
+                                                                int vec, R dt, R ca, R cd) {
   using G = Tile2x2<R, TR>;
   __shared__ R sx[G::LR * G::LW];
   __shared__ R sk[G::LR * G::LW];
@@ -1068,6 +1089,13 @@ __global__ __launch_bounds__(kX2Threads) void fwd_vardiff2d9_x2(const R* __restr
       column(std::true_type{}, c1, i1, 1, TR + 2, v);
     else
       column(std::false_type{}, c1, i1, 1, TR + 2, v);
+    if constexpr (ST) {  // v[r] is grid row j0 - 1 + r; the tile's rows are r = 1 .. TR
+      if (t >= 1 && t <= kX2TW && i1 < nx) {
+#pragma unroll
+        for (int r = 1; r <= TR; ++r)
+          if (j0 - 1 + r < ny) put<NT>(&mid[(j0 - 1 + r) * nx + i1], v[r]);
+      }
+    }
   }
   __syncthreads();
   if (act) {
@@ -1342,38 +1370,51 @@ inline int streams(const StepShape& s) {
   return bytes >= kStreamBytes ? 1 : 0;
 }
 
+// mids (nullable): the intermediate states' buffers, step l's at mids[l-1].
 template <class R, int K, int RPT, int NZ>
-hipError_t ac_forward_n(const StepShape& s, const R* x, R* y, hipStream_t st) {
+hipError_t ac_forward_n(const StepShape& s, const R* x, R* y, R* const* mids, hipStream_t st) {
   using A = AcN<K, RPT, NZ>;
   const int tx = cdiv(s.nx, A::OX), ty = cdiv(s.ny, A::OY);
   const int nt = tx * ty * cdiv(s.nz, A::ZC);
-  if (streams(s))
-    fwd_allencahn3d7_n<R, K, RPT, NZ, true><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-        x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+  const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
+  R* m0 = mids ? mids[0] : nullptr;
+  R* m1 = (mids && K >= 3) ? mids[1] : nullptr;
+  const bool str = streams(s) != 0;
+  if (mids && str)
+    fwd_allencahn3d7_n<R, K, RPT, NZ, true, true><<<grid, block, 0, st>>>(
+        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+  else if (mids)
+    fwd_allencahn3d7_n<R, K, RPT, NZ, false, true><<<grid, block, 0, st>>>(
+        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+  else if (str)
+    fwd_allencahn3d7_n<R, K, RPT, NZ, true, false><<<grid, block, 0, st>>>(
+        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   else
-    fwd_allencahn3d7_n<R, K, RPT, NZ, false><<<dim3(xcd_grid(nt)), dim3(kBX, kBY), 0, st>>>(
-        x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
+    fwd_allencahn3d7_n<R, K, RPT, NZ, false, false><<<grid, block, 0, st>>>(
+        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   return hipGetLastError();
 }
 
-// Allen-Cahn, n fused forward steps (2 <= n <= kAcMaxFuse).
+// Allen-Cahn, n fused forward steps (2 <= n <= kAcMaxFuse); mids as above.
 template <class R>
-hipError_t ac_forward_steps(const StepShape& s, const void* xv, void* yv, int32_t n,
-                            hipStream_t st) {
+hipError_t ac_forward_steps(const StepShape& s, const void* xv, void* yv, void* const* mids,
+                            int32_t n, hipStream_t st) {
   const R* x = static_cast<const R*>(xv);
   R* y = static_cast<R*>(yv);
+  R* const* m = reinterpret_cast<R* const*>(mids);
   switch (n) {
     case 2:
-      return ac_forward_n<R, 2, 4, 32>(s, x, y, st);
+      return ac_forward_n<R, 2, 4, 32>(s, x, y, m, st);
     case 3:
-      return ac_forward_n<R, 3, 4, 64>(s, x, y, st);
+      return ac_forward_n<R, 3, 4, 64>(s, x, y, m, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <class R>
 hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv, bool two,
-                     hipStream_t st) {
+                     hipStream_t st, void* midv = nullptr) {
+  R* mid = static_cast<R*>(midv);
   const R* x = static_cast<const R*>(xv);
   const R* K = static_cast<const R*>(Kv);
   R* y = static_cast<R*>(yv);
@@ -1398,7 +1439,7 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
     }
     case ADST_ALLENCAHN3D7: {
       if (two) {
-        return ac_forward_n<R, 2, 4, 32>(s, x, y, st);
+        return ac_forward_n<R, 2, 4, 32>(s, x, y, nullptr, st);
       } else {
         const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
         const int nt = tx * ty * cdiv(s.nz, kAcZC);
@@ -1426,12 +1467,18 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       if (two) {
         const int tx = cdiv(s.nx, kX2TW), nt = tx * cdiv(s.ny, kVdX2TR);
         const dim3 grid(xcd_grid(nt)), block(kX2Threads);
-        if (str)
-          fwd_vardiff2d9_x2<R, kVdX2TR, true><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx, nt,
-                                                                      vec, dt, ca, cd);
+        if (mid && str)
+          fwd_vardiff2d9_x2<R, kVdX2TR, true, true><<<grid, block, 0, st>>>(
+              x, K, y, mid, s.nx, s.ny, tx, nt, vec, dt, ca, cd);
+        else if (mid)
+          fwd_vardiff2d9_x2<R, kVdX2TR, false, true><<<grid, block, 0, st>>>(
+              x, K, y, mid, s.nx, s.ny, tx, nt, vec, dt, ca, cd);
+        else if (str)
+          fwd_vardiff2d9_x2<R, kVdX2TR, true, false><<<grid, block, 0, st>>>(
+              x, K, y, mid, s.nx, s.ny, tx, nt, vec, dt, ca, cd);
         else
-          fwd_vardiff2d9_x2<R, kVdX2TR, false><<<grid, block, 0, st>>>(x, K, y, s.nx, s.ny, tx,
-                                                                       nt, vec, dt, ca, cd);
+          fwd_vardiff2d9_x2<R, kVdX2TR, false, false><<<grid, block, 0, st>>>(
+              x, K, y, mid, s.nx, s.ny, tx, nt, vec, dt, ca, cd);
         break;
       }
       const int tx = cdiv(s.nx, kVdTW), nt = tx * cdiv(s.ny, kVdTR);
@@ -1600,6 +1647,26 @@ hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void
                              : forward_t<float>(s, x, K, y, false, stream);
 }
 
+int32_t max_stored_forward(int32_t kind) {
+  switch (kind) {
+    case ADST_ALLENCAHN3D7:
+      return kAcMaxFuse;
+    case ADST_VARDIFF2D9:
+      return 2;
+  }
+  return 1;
+}
+
+hipError_t launch_forward_store(const StepShape& s, const void* x, const void* K, void* const* ys,
+                                int32_t n, hipStream_t stream) {
+  if (n < 2 || n > max_stored_forward(s.kind) || s.limit) return hipErrorInvalidValue;
+  if (s.kind == ADST_ALLENCAHN3D7)
+    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, ys[n - 1], ys, n, stream)
+                               : ac_forward_steps<float>(s, x, ys[n - 1], ys, n, stream);
+  return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, ys[1], true, stream, ys[0])
+                             : forward_t<float>(s, x, K, ys[1], true, stream, ys[0]);
+}
+
 int32_t max_fused_forward(int32_t kind) {
   switch (kind) {
     case ADST_JACOBI2D5:
@@ -1622,8 +1689,8 @@ hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, vo
                             hipStream_t stream) {
   if (n < 2 || n > max_fused_forward(s.kind)) return hipErrorInvalidValue;
   if (s.kind == ADST_ALLENCAHN3D7)
-    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, y, n, stream)
-                               : ac_forward_steps<float>(s, x, y, n, stream);
+    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, y, nullptr, n, stream)
+                               : ac_forward_steps<float>(s, x, y, nullptr, n, stream);
   if (n == 2)
     return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, true, stream)
                                : forward_t<float>(s, x, K, y, true, stream);

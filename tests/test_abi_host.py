@@ -53,8 +53,9 @@ def test_struct_layouts_match_header():
     # int32 x2, int64 x3, double x4, uint32 (+pad) = 72 bytes
     assert ctypes.sizeof(adst.adst_problem) == 72
     assert ctypes.sizeof(adst.adst_action) == 20
-    # int32 x4, int64 x8, uint64 x6, float x6
-    assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 8 * 8 + 6 * 8 + 6 * 4
+    # int32 x4, int64 x8, uint64 x6, float x6, uint64
+    assert ctypes.sizeof(adst.adst_plan_info) == 4 * 4 + 8 * 8 + 6 * 8 + 6 * 4 + 8
+    assert adst.adst_plan_info.fwd_alg_bytes.offset == 4 * 4 + 8 * 8 + 6 * 8 + 6 * 4
 
 
 def _p(kind=adst.ADST_ALLENCAHN3D7, dims=(8, 8, 8), dtype=adst.ADST_F64, flags=0):

@@ -196,11 +196,62 @@ def test_workspace_and_bytes():
     assert info.state_bytes == S
     assert info.workspace_bytes == 16384 + (3 + info.slots) * stride
     assert info.fwd_workspace_bytes == S
-    # Allen-Cahn: 16 B per point per forward launch (one or two steps), 24 per
-    # adjoint, 16 for the seed
+    # Allen-Cahn: 8 B per point per forward launch read and 8 per state it
+    # writes (a fused run writes one, a store-through run each of its
+    # states), 24 per adjoint, 16 for the seed
     n = 100 * 30 * 7
-    assert info.alg_bytes == n * (16 * info.fwd_launches + 24 * 12 + 16)
+    assert info.fwd_kernels < info.fwd_launches
+    assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels + 8 * info.fwd_launches)
+    assert info.alg_bytes == info.fwd_alg_bytes + n * (24 * 12 + 16)
     assert adst.adst_plan(p, 0, 0, 0).workspace_bytes == 16384
+
+
+@pytest.mark.parametrize("kind,dtype,dims,grads,depth,bytes_in", [
+    (adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8), 0, 3, 8),
+    (adst.ADST_VARDIFF2D9, adst.ADST_F32, (10, 9, 1), adst.ADST_GRAD_COEFF, 2, 8),
+])
+def test_store_through_runs(kind, dtype, dims, grads, depth, bytes_in):
+    # store-all: one chain x0 -> slot -> ... -> work -> x_T through all T
+    # single steps, taken up to `depth` steps per launch
+    isz = 8 if dtype == adst.ADST_F64 else 4
+    n = dims[0] * dims[1] * dims[2]
+    T = 8
+    p = adst.make_problem(kind, dtype, dims)
+    info = adst.adst_plan(p, T, 20 * n * isz, adst.ADST_SCHED_STORE_ALL, grads)
+    assert info.fwd_launches == T and info.fwd_kernels == -(-T // depth)
+    assert info.fwd_alg_bytes == n * (bytes_in * info.fwd_kernels + isz * T)
+    # one launch per step without fusion or with the limiter
+    for q in (adst.make_problem(kind, dtype, dims, flags=adst.ADST_NO_FUSE),
+              adst.make_problem(kind, dtype, dims, lim=(0.0, 1.0))):
+        i = adst.adst_plan(q, T, 20 * n * isz, adst.ADST_SCHED_STORE_ALL, grads)
+        assert i.fwd_kernels == T and i.fwd_alg_bytes == n * (bytes_in + isz) * T
+
+
+def test_store_through_runs_counted_like_the_executor():
+    # binomial plans: the launches fwd_kernels counts are the runs of chained
+    # single steps (up to three, into buffers other than the run's input)
+    # and the fused actions
+    p = adst.make_problem(adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8))
+    S = 10 * 9 * 8 * 8
+    for T, slots in ((8, 3), (13, 4), (23, 5), (40, 6)):
+        acts = adst.adst_plan_actions(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
+        info = adst.adst_plan(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
+        kernels, i = 0, 0
+        while i < len(acts):
+            a = acts[i]
+            if a[0] in (adst.ADST_OP_FWD, adst.ADST_OP_FWD2):
+                kernels += 1
+            r = 1
+            if a[0] == adst.ADST_OP_FWD:
+                while r < 3 and i + r < len(acts):
+                    b, prev = acts[i + r], acts[i + r - 1]
+                    if b[0] != adst.ADST_OP_FWD or b[2] != prev[3] or b[1] != prev[1] + 1:
+                        break
+                    if b[3] == a[2] or any(acts[i + k][3] == b[3] for k in range(r)):
+                        break
+                    r += 1
+            i += r
+        assert info.fwd_kernels == kernels
 
 
 def test_zero_steps_plan():
