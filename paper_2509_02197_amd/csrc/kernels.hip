@@ -547,7 +547,8 @@ struct AcN {
 // ST: the intermediate states are stored too, step l's into mid[l-1], each
 // point by the workgroup whose output tile holds it (a run of steps whose
 // every state is kept moves 8 + 8n bytes per point for n steps instead of
-// 16n).
+// 16n). They are stored without the non-temporal hint: the reverse sweep
+// reads them back soon after (measured at 512^3: 58.9 -> 58.5 ms per call).
 template <class R, int K, int RPT, int NZ, bool NT, bool ST>
 __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restrict__ x,
                                                                R* __restrict__ y,
@@ -631,7 +632,7 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
                        : R(0);
         if constexpr (ST) {
           if (cin && tile_col && r >= H && r < SY - H && p >= z0 && p < z1)
-            put<NT>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
+            put<false>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
         }
       }
     }
@@ -653,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
           sn[l - 1][q] = v;
           if constexpr (ST) {
             if (ok && tile_col && r >= H && r < SY - H && pl >= z0 && pl < z1)
-              put<NT>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
+              put<false>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
           }
         } else if (ok && pl >= z0 && pl < z1) {
           put<NT>(&y[pl * plane + j * nx + ic], v);
