@@ -86,3 +86,36 @@ def test_store_runs_bitwise_and_oracle(kind, dtype, shape):
         else:
             for k in ("dx0", "xT") + (("dK",) if want_dK else ()):
                 assert np.array_equal(a[k], ref[k]), (sched, k)
+
+
+@pytest.mark.parametrize("kind,dtype,shape,T,flags,dparams", [
+    (AC, F64, (5, 15, 63), 1, 0, False), (AC, F64, (5, 15, 63), 2, 0, False),
+    (AC, F64, (5, 15, 63), 3, 0, False), (AC, F64, (5, 15, 63), 4, 0, False),
+    (AC, F64, (33, 14, 62), 7, 0, True),
+    (VD, F32, (9, 253), 3, 0, False), (VD, F32, (9, 253), 6, 0, True),
+    (VD, F32, (17, 504), 5, adst.ADST_FORCE_TAPE, False),
+])
+def test_store_runs_short_forced_and_dparams(kind, dtype, shape, T, flags, dparams):
+    # runs of every length up to the depth, the constants' gradients (whose
+    # adjoint reads the stored states) and a forced tape for the linear
+    # variable-coefficient step without dK: all bit-identical to one launch
+    # per step
+    inp = _inputs(kind, dtype, shape, 62)
+    loss = adst.ADST_LOSS_DOT_W if kind == AC else adst.ADST_LOSS_HALF_SQ_DIFF
+    want_dK = kind == VD and not flags
+    S = inp["x0"].nbytes
+    say(f"store runs short kind={kind} dtype={dtype} shape={shape} T={T} flags={flags} dp={dparams}")
+    kw = dict(want_dK=want_dK, want_dparams=dparams)
+    a = gpu_vjp(kind, inp, T, loss, T * S, adst.ADST_SCHED_STORE_ALL, flags=flags, **kw)
+    b = gpu_vjp(kind, inp, T, loss, T * S, adst.ADST_SCHED_STORE_ALL,
+                flags=flags | adst.ADST_NO_FUSE, **kw)
+    if T >= 2:
+        assert a["info"]["fwd_kernels"] < b["info"]["fwd_kernels"]
+    keys = ("dx0", "xT") + (("dK",) if want_dK else ()) + (("dparams",) if dparams else ())
+    for k in keys:
+        assert np.array_equal(a[k], b[k]), k
+    assert a["loss"] == b["loss"]
+    dx0, _, xT, _ = oracle.vjp(kind, inp["x0"], K=inp.get("K"), steps=T, loss=loss,
+                               aux=inp["aux"], want_dK=want_dK)
+    assert np.array_equal(a["xT"], xT)
+    assert rel(a["dx0"], dx0) <= TOL[dtype]
