@@ -57,6 +57,10 @@ namespace {
 
 constexpr int kLanes = 64;
 constexpr int kRows = 48;      // rows per chunk of an interior strip
+constexpr int kAdjRows = 42;   // the same for the marching adjoint: 4086 waves
+                               // at 4096^2, about one per wave slot of the chip
+                               // (54.0 against 55.1 us per 6-step launch; the
+                               // forward is faster with 48)
 constexpr int kEdgeRows = 12;  // rows per chunk of the first and last strip
 constexpr int kEndRows = 6;    // rows of a strip's first and last chunk, whose
                                // blocks near the grid's top and bottom edge
@@ -66,6 +70,8 @@ constexpr int kUnroll = 6;     // input rows per straight-line block
 constexpr int kXcds = 8;       // workgroup i runs on XCD i mod 8
 static_assert(kUnroll % kAhead == 0 && kUnroll % 3 == 0, "register slots must stay static");
 static_assert(2 * kEndRows <= kRows && kEdgeRows <= kRows && kRows <= 64, "chunk sizes");
+static_assert(2 * kEndRows <= kAdjRows && kEdgeRows <= kAdjRows && kAdjRows <= kRows,
+              "chunk sizes");
 
 // Whole-wave lane shifts: lane i receives lane i-1's value (lane 0: 0) or
 // lane i+1's (lane 63: 0).
@@ -100,6 +106,7 @@ struct Geom {
 // chunks [x*pi, (x+1)*pi), edge chunks first.
 struct MarchGrid {
   int ns, nedge, ce, ci, pe, pi;
+  int rows;  // rows per chunk of an interior strip (at most kRows)
 };
 
 // This workgroup's strip and chunk of rows [r0, r1); false when the
@@ -124,7 +131,7 @@ __device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* c
     *strip = 1 + t / g.ci;
     *chunk = t % g.ci;
     nch = g.ci;
-    mid = kRows;
+    mid = g.rows;
     if (item) *item = g.nedge * g.ce + t;
   }
   // kEndRows at each end of the strip, mid rows between
@@ -146,14 +153,15 @@ __device__ inline bool march_item(const MarchGrid& g, int ny, int* strip, int* c
 }
 
 // The work list for strips of ow output columns; false if it is too long.
-inline bool make_grid(int nx, int ny, int ow, MarchGrid* g, int64_t* blocks) {
+inline bool make_grid(int nx, int ny, int ow, MarchGrid* g, int64_t* blocks, int rows = kRows) {
+  g->rows = rows;
   g->ns = (nx + ow - 1) / ow;
   g->nedge = g->ns >= 2 ? 2 : 1;
   auto chunks = [&](int mid) {
     return ny > 2 * kEndRows ? 2 + (ny - 2 * kEndRows + mid - 1) / mid : 1;
   };
   g->ce = chunks(kEdgeRows);
-  g->ci = chunks(kRows);
+  g->ci = chunks(rows);
   const int64_t E = int64_t(g->nedge) * g->ce, I = int64_t(g->ns - g->nedge) * g->ci;
   g->pe = (int)((E + kXcds - 1) / kXcds);
   g->pi = (int)((I + kXcds - 1) / kXcds);
@@ -438,7 +446,8 @@ hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
   if (ADJ && s.nx <= G::V) return hipErrorInvalidValue;  // a lane would hold both ring columns
   MarchGrid g;
   int64_t blocks;
-  if (!make_grid(s.nx, s.ny, G::OW, &g, &blocks)) return hipErrorInvalidValue;
+  if (!make_grid(s.nx, s.ny, G::OW, &g, &blocks, ADJ ? kAdjRows : kRows))
+    return hipErrorInvalidValue;
   const bool vec = s.nx % G::V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(y) & 15u) == 0;
   if (vec)
