@@ -53,6 +53,9 @@
  *     before anything is enqueued.
  *   - On failure the call returns a non-zero adst_status and
  *     adst_last_error() holds a thread-local description.
+ *   - ADST_LOG=1 in the environment prints each adst_vjp plan to stderr
+ *     (ADST_LOG=2 also its actions); the phases of a call are marked as
+ *     roctx ranges for rocprofv3's marker trace.
  */
 #ifndef ADST_H
 #define ADST_H
@@ -112,8 +115,10 @@ typedef enum {
 /* Problem flags. */
 #define ADST_FORCE_TAPE 0x1u /* treat every step as reading x_{t-1} in its adjoint, even when
                                 the kind is linear, so store/recompute runs at any shape */
-#define ADST_TRACE 0x2u      /* time the launches with HIP events, synchronise the stream at
-                                the end of the call and fill the ms_* fields of adst_plan_info */
+#define ADST_TRACE 0x2u      /* time every launch with a HIP event pair, synchronise the
+                                stream at the end of the call, fill the ms_* fields of
+                                adst_plan_info and the per-kernel statistics that
+                                adst_trace_kernels returns */
 #define ADST_NO_FUSE 0x4u    /* run every step as its own launch (no temporal blocking:
                                 otherwise up to 6 Jacobi steps, 3 Allen-Cahn forward steps
                                 or 2 variable-coefficient forward steps share one launch);
@@ -234,6 +239,11 @@ typedef struct {
 } adst_plan_info;
 
 /* Plan a forward+VJP call without touching the GPU (host only).
+ * Defined by Sec. IV (the store/recompute trade-off for the forwarded
+ * values the backward pass reads, made within a user memory limit, with
+ * store-all as the default and a manual choice available) and Sec. III-B
+ * (the loop is reversed as one compact loop of the same range, so the
+ * reverse sweep needs x_{t-1} in the order t = T..1).
  * The budget counts checkpoint-slot storage only: slots = floor(budget /
  * state_bytes); x0 is the caller's and is the free base checkpoint, so the
  * schedule has c = slots + 1 checkpoints. grads is a mask of ADST_GRAD_COEFF
@@ -250,13 +260,18 @@ adst_status adst_plan(const adst_problem* prob, int32_t steps, uint64_t mem_budg
                       int32_t sched, int32_t grads, adst_plan_info* out);
 
 /* The same plan as its action list (host only; for tests and inspection).
+ * Sec. IV: which forward values are stored and which are recomputed from
+ * the nearest checkpoint, written out step by step.
  * Writes min(cap, n) actions to out (out may be NULL when cap == 0) and the
  * full length to *n_out. Same errors as adst_plan. */
 adst_status adst_plan_actions(const adst_problem* prob, int32_t steps, uint64_t mem_budget_bytes,
                               int32_t sched, int32_t grads, adst_action* out, int64_t cap,
                               int64_t* n_out);
 
-/* x_T after `steps` forward steps (the unmodified program). coeff is K for
+/* x_T after `steps` forward steps: the unmodified program whose gradient
+ * adst_vjp computes (Sec. I: the user's program is differentiated without
+ * modification; the step kinds are defined at the top of this file).
+ * x0 and xT are [nz][ny][nx] arrays of the working precision; coeff is K for
  * VARDIFF2D9 and must be NULL-or-ignored otherwise. ws must hold
  * adst_plan_info.fwd_workspace_bytes (one state when steps >= 2, else 0;
  * always 0 for the in-place kind, which runs in xT).
@@ -266,7 +281,14 @@ adst_status adst_forward(const adst_problem* prob, const void* x0, const void* c
                          hipStream_t stream);
 
 /* Forward sweep, loss, and reverse sweep under the budget, enqueued on
- * `stream`. Outputs: dx0 (required), dcoeff (dK, VARDIFF2D9 only, NULL = not
+ * `stream`: the vector-Jacobian product of one scalar output with respect to
+ * the inputs (Sec. II: gradients of one dependent variable, accumulated over
+ * every read of an input and cleared where a value is overwritten; Sec.
+ * III-B: the time loop reversed as one compact loop; Sec. III-C: each
+ * parallel map of a step reversed into a map of the same range, here in
+ * gather form; Sec. IV: forwarded values stored or recomputed within
+ * mem_budget_bytes). Arrays are [nz][ny][nx] of the working precision,
+ * device memory owned by the caller. Outputs: dx0 (required), dcoeff (dK, VARDIFF2D9 only, NULL = not
  * requested), xT (optional), loss_dev (optional device double), dparams
  * (optional device double[2]: the constants' gradients, see
  * ADST_GRAD_PARAMS; NULL = not requested). The plan is the one adst_plan
@@ -341,6 +363,39 @@ typedef struct {
 adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,
                            const adst_ilp_event* events, int64_t n_events, double limit,
                            int32_t* store_out, adst_ilp_info* info);
+
+/* ---- Measurement and observability ------------------------------------
+ * Per-kernel launch statistics of the last adst_vjp call on this thread
+ * that ran with ADST_TRACE (host only, no GPU call). With ADST_TRACE every
+ * launch (every pipelined sequence of launches for the in-place kind) is
+ * bracketed by a HIP event pair on the call's stream, so ms_sum / launches
+ * is the kernel's average duration; alg_bytes_sum is the algorithmic HBM
+ * bytes of those launches (each input read once and each output written
+ * once per launch: a launch of n fused steps moves one step's bytes). name
+ * is the kernel's base name as a profiler reports it, with the variant in
+ * angle brackets (e.g. "fwd_allencahn3d7_n<3,store>", "jacobi_march<adj,6>").
+ * Writes min(cap, n) entries to out (out may be NULL when cap == 0) and the
+ * count to *n_out. Errors: ADST_ERR_ARG (NULL n_out, bad cap). */
+typedef struct {
+  char name[56];
+  int32_t phase;          /* 0 forward sweep, 1 recomputation, 2 adjoint, 3 loss and seed,
+                             4 the constants' final sum (the phase of its first launch) */
+  int32_t reserved;
+  int64_t launches;       /* kernel dispatches */
+  double ms_sum;          /* summed duration (ms) */
+  double ms_min, ms_max;  /* per dispatch (a pipelined sequence: its average dispatch) */
+  double alg_bytes_sum;   /* algorithmic bytes of all those dispatches */
+} adst_kernel_stat;
+
+adst_status adst_trace_kernels(adst_kernel_stat* out, int32_t cap, int32_t* n_out);
+
+/* Device-to-device copy of `bytes` (a multiple of 4) from src to dst on
+ * `stream`, one 16-byte vector per work-item when both pointers are 16-byte
+ * aligned. adst_forward uses it for steps = 0; the benchmark times it as the
+ * plain-copy bandwidth ceiling the stencil kernels are compared with.
+ * Errors: ADST_ERR_ARG (NULL pointer with bytes > 0, misaligned pointer or
+ * size, overlapping ranges), ADST_ERR_HIP. */
+adst_status adst_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* adst_status_str(adst_status status);

@@ -27,7 +27,8 @@ ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2, ADST_OP_FWDW
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
 EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
-            "adst_status_str", "adst_last_error")
+            "adst_trace_kernels", "adst_copy", "adst_status_str", "adst_last_error")
+PHASE_NAMES = ("forward sweep", "recomputation", "adjoint", "loss and seed", "constants")
 ILP_EVENTS = {"alloc": 0, "free": 1, "produce": 2, "drop": 3, "recompute": 4,
               "recompute_done": 5, "release": 6, "path": 7}
 
@@ -76,6 +77,13 @@ class adst_ilp_info(ctypes.Structure):
                 ("paths", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class adst_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 56), ("phase", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("launches", ctypes.c_int64),
+                ("ms_sum", ctypes.c_double), ("ms_min", ctypes.c_double),
+                ("ms_max", ctypes.c_double), ("alg_bytes_sum", ctypes.c_double)]
+
+
 class AdstError(RuntimeError):
     def __init__(self, status, detail):
         self.status = status
@@ -104,7 +112,10 @@ def lib():
                            u64, vp, P(adst_plan_info)]
     L.adst_ilp_solve.argtypes = [P(adst_ilp_array), i32, P(adst_ilp_event), i64, ctypes.c_double,
                                  P(i32), P(adst_ilp_info)]
-    for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve"):
+    L.adst_trace_kernels.argtypes = [P(adst_kernel_stat), i32, P(i32)]
+    L.adst_copy.argtypes = [vp, vp, u64, vp]
+    for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
+              "adst_trace_kernels", "adst_copy"):
         getattr(L, f).restype = ctypes.c_int
     L.adst_status_str.argtypes = [ctypes.c_int]
     L.adst_status_str.restype = ctypes.c_char_p
@@ -195,6 +206,24 @@ def adst_vjp(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx
     return info
 
 
+def adst_trace_kernels():
+    """Per-kernel statistics of this thread's last adst_vjp call made with
+    ADST_TRACE: a list of dicts (name, phase, launches, ms_sum, ms_min,
+    ms_max, alg_bytes_sum)."""
+    n = ctypes.c_int32(0)
+    L = lib()
+    _check(L.adst_trace_kernels(None, 0, ctypes.byref(n)))
+    buf = (adst_kernel_stat * max(n.value, 1))()
+    _check(L.adst_trace_kernels(buf, n.value, ctypes.byref(n)))
+    return [{"name": s.name.decode(), "phase": PHASE_NAMES[s.phase], "launches": s.launches,
+             "ms_sum": s.ms_sum, "ms_min": s.ms_min, "ms_max": s.ms_max,
+             "alg_bytes_sum": s.alg_bytes_sum} for s in buf[:n.value]]
+
+
+def adst_copy(dst, src, nbytes, stream=None):
+    _check(lib().adst_copy(_ptr(dst), _ptr(src), int(nbytes), _stream(stream)))
+
+
 def adst_ilp_solve(arrays, events, limit):
     """arrays: sequence of (size, overhead, cost); events: sequence of
     ("alloc"|"free", amount), (kind, array_index) or ("path",).
@@ -234,9 +263,37 @@ def _dims(shape):
     raise ValueError(f"expected a 2-D or 3-D array, got {tuple(shape)}")
 
 
+def _check_tensors(x0, **others):
+    """The kernels read and write row-major, unpadded arrays of one dtype on
+    one device: reject anything else before any plan or launch."""
+    import torch
+    if not torch.is_tensor(x0):
+        raise ValueError("x0 must be a torch tensor")
+    _dtype_code(x0)
+    _dims(x0.shape)
+    if not x0.is_contiguous():
+        raise ValueError("x0 must be contiguous (row-major, unpadded)")
+    for name, t in others.items():
+        if t is None:
+            continue
+        if not torch.is_tensor(t):
+            raise ValueError(f"{name} must be a torch tensor")
+        if t.dtype != x0.dtype:
+            raise ValueError(f"{name} has dtype {t.dtype}, x0 has {x0.dtype}")
+        if tuple(t.shape) != tuple(x0.shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, x0 has {tuple(x0.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous (row-major, unpadded)")
+        if t.device != x0.device:
+            raise ValueError(f"{name} is on {t.device}, x0 on {x0.device}")
+    if x0.device.type != "cuda":
+        raise ValueError(f"x0 must be on a GPU, not {x0.device}")
+
+
 def forward(kind, x0, coeff=None, steps=1, params=None, stream=None, lim=None, flags=0):
     """x_T on the device of x0 (torch tensors, row-major)."""
     import torch
+    _check_tensors(x0, coeff=coeff)
     prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags, lim)
     xT = torch.empty_like(x0)
     info = adst_plan(prob, steps, 1 << 62, ADST_SCHED_STORE_ALL)
@@ -255,6 +312,7 @@ def vjp(kind, x0, coeff=None, steps=1, loss=ADST_LOSS_HALF_SQ, aux=None, budget_
     dparams (device double[2], or None unless want_dparams), info and the
     workspace."""
     import torch
+    _check_tensors(x0, coeff=coeff, aux=aux)
     prob = make_problem(kind, _dtype_code(x0), _dims(x0.shape), params, flags, lim)
     if budget_bytes is None:
         budget_bytes = (1 << 63)

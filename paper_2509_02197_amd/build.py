@@ -57,7 +57,9 @@ def build(verbose: bool = False) -> str:
     with ThreadPoolExecutor(max_workers=len(jobs)) as ex:
         list(ex.map(lambda c: _run(c, verbose), jobs))
     objs = [os.path.join(BUILD, s + ".o") for s in HOST_SOURCES + HIP_SOURCES]
-    _run([hipcc, "-shared", "--offload-arch=" + ARCH, "-o", LIB + ".tmp"] + objs, verbose)
+    _run([hipcc, "-shared", "--offload-arch=" + ARCH, "-o", LIB + ".tmp"] + objs +
+         ["-L" + os.path.join(ROCM, "lib"), "-lrocprofiler-sdk-roctx",
+          "-Wl,-rpath," + os.path.join(ROCM, "lib")], verbose)
     os.replace(LIB + ".tmp", LIB)
     return LIB
 

@@ -14,6 +14,8 @@
 #include <utility>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "adst.h"
 #include "kernels.h"
 #include "ilp.h"
@@ -157,47 +159,85 @@ Layout layout_for(const Checked& c, const Plan& plan) {
 
 // Algorithmic HBM bytes per point of one forward / adjoint step and of the
 // seed: what the step must read and write at least once.
-void per_point_bytes(const Checked& c, bool want_dk, int32_t loss, uint64_t* fwd, uint64_t* adj,
-                     uint64_t* adj_first, uint64_t* seed, uint64_t* dparam) {
+struct PerPoint {
+  uint64_t fwd = 0, adj = 0, adj_first = 0, seed = 0;
+  uint64_t adj_extra = 0;  // reads the adjoint launch adds for the constants or the limiter
+  uint64_t mask = 0;       // the limiter's separate mask pass, where the adjoint does not apply it
+};
+
+PerPoint per_point_bytes(const Checked& c, bool want_dk, int32_t loss) {
+  PerPoint b;
   const uint64_t s = itemsize(c.shape.dtype);
   switch (c.shape.kind) {
     case ADST_JACOBI2D5:
     case ADST_GAUSSSEIDEL2D5:  // in place: read and write each point once per step
-      *fwd = 2 * s;
-      *adj = *adj_first = 2 * s;
+      b.fwd = 2 * s;
+      b.adj = b.adj_first = 2 * s;
       break;
     case ADST_ALLENCAHN3D7:
-      *fwd = 2 * s;
-      *adj = *adj_first = 3 * s;  // g, x, g'
+      b.fwd = 2 * s;
+      b.adj = b.adj_first = 3 * s;  // g, x, g'
       break;
-    default:                      // VARDIFF2D9
-      *fwd = 3 * s;               // x, K, x'
-      *adj = want_dk ? 6 * s : 3 * s;  // g, x, K, dK read+write, g'  |  g, K, g'
-      *adj_first = want_dk ? 5 * s : 3 * s;
+    default:                        // VARDIFF2D9
+      b.fwd = 3 * s;                // x, K, x'
+      b.adj = want_dk ? 6 * s : 3 * s;  // g, x, K, dK read+write, g'  |  g, K, g'
+      b.adj_first = want_dk ? 5 * s : 3 * s;
       break;
   }
-  *seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
+  b.seed = (loss == ADST_LOSS_HALF_SQ ? 2 : 3) * s;
   // the constants' gradients, fused into the adjoint, add the reads of
   // x_{t-1} the adjoint does not already make
-  *dparam = 0;
   if (c.want_dp && (c.shape.kind == ADST_JACOBI2D5 || (c.shape.kind == ADST_VARDIFF2D9 && !want_dk)))
-    *dparam = s;
+    b.adj_extra = s;
   // the limiter's branch mask reads x_{t-1} (and K) and updates g_t in place
   // in a pass of its own; where the adjoint applies it, it only adds the
   // read of x_{t-1} an adjoint without state does not make
   if (c.shape.limit) {
     if (!adjoint_applies_limit(c.shape, c.want_dp))
-      *dparam += (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
+      b.mask = (c.shape.kind == ADST_VARDIFF2D9 ? 4 : 3) * s;
     else if (c.shape.kind == ADST_JACOBI2D5)
-      *dparam += s;
+      b.adj_extra += s;
   }
+  return b;
+}
+
+// Short name of the kernel an action launches, as a profiler reports its
+// base name (template arguments that select the kernel's variant are
+// written out where the variants differ in the bytes they move).
+std::string kernel_label(const Checked& c, const adst_action& a, int32_t stored, bool dparams) {
+  const int32_t k = c.shape.kind;
+  const bool adj = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJ2 || a.op == ADST_OP_ADJW;
+  if (k == ADST_GAUSSSEIDEL2D5) return adj ? "gs_wave<adj>" : "gs_wave<fwd>";
+  static const char* const kFwd[3] = {"fwd_jacobi2d5", "fwd_allencahn3d7", "fwd_vardiff2d9"};
+  static const char* const kAdj[3] = {"adj_jacobi2d5", "adj_allencahn3d7", "adj_vardiff2d9"};
+  if (!adj) {
+    if (stored >= 2)
+      return k == ADST_ALLENCAHN3D7
+                 ? "fwd_allencahn3d7_n<" + std::to_string(stored) + ",store>"
+                 : std::string(kFwd[k]) + "_x2<store>";
+    if (a.n <= 1) return kFwd[k];
+    if (k == ADST_ALLENCAHN3D7) return "fwd_allencahn3d7_n<" + std::to_string(a.n) + ">";
+    if (a.n == 2) return std::string(kFwd[k]) + "_x2";
+    return "jacobi_march<fwd," + std::to_string(a.n) + ">";
+  }
+  if (a.n >= 3) return "jacobi_march<adj," + std::to_string(a.n) + ">";
+  if (a.n == 2) return std::string(kAdj[k]) + "_x2";
+  if (k == ADST_JACOBI2D5 && dparams) return "jacobi_lim_adjoint<dp>";
+  if (k == ADST_JACOBI2D5 && adjoint_applies_limit(c.shape, dparams)) return "jacobi_lim_adjoint";
+  if (k == ADST_ALLENCAHN3D7 && adjoint_applies_limit(c.shape, dparams))
+    return "adj_allencahn3d7_lim";
+  std::string n = kAdj[k];
+  if (k == ADST_VARDIFF2D9 && c.want_dk) n += dparams ? "<dK,dp>" : "<dK>";
+  else if (dparams) n += "<dp>";
+  return n;
 }
 
 void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,
                adst_plan_info* info) {
   const Layout L = layout_for(c, plan);
-  uint64_t fb, ab, ab1, sb, db;
-  per_point_bytes(c, want_dk, loss, &fb, &ab, &ab1, &sb, &db);
+  const PerPoint pp = per_point_bytes(c, want_dk, loss);
+  const uint64_t fb = pp.fwd, ab = pp.adj, ab1 = pp.adj_first, sb = pp.seed,
+                 db = pp.adj_extra + pp.mask;
   *info = adst_plan_info{};
   info->steps = plan.steps;
   info->sched = plan.sched;
@@ -261,6 +301,43 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
   info->fwd_alg_bytes = n * fwd_per_point;
 }
 
+// ADST_LOG=1 in the environment prints each adst_vjp call's plan to
+// stderr before anything is enqueued; ADST_LOG=2 also its action list.
+int log_level() {
+  static const int level = [] {
+    const char* v = std::getenv("ADST_LOG");
+    return v ? std::atoi(v) : 0;
+  }();
+  return level;
+}
+
+void log_plan(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss) {
+  static const char* const kSched[4] = {"auto", "store_all", "uniform", "binomial"};
+  static const char* const kKind[4] = {"jacobi2d5", "allencahn3d7", "vardiff2d9",
+                                       "gaussseidel2d5"};
+  adst_plan_info info;
+  fill_info(c, plan, budget, want_dk, loss, &info);
+  std::fprintf(stderr,
+               "adst plan: %s %s %dx%dx%d T=%d budget=%llu B sched=%s slots=%d (c=%d) "
+               "needs_state=%d fwd_steps=%lld (recompute %lld) adj_steps=%lld "
+               "actions=%lld kernels fwd=%lld adj=%lld workspace=%llu B alg_bytes=%llu\n",
+               kKind[c.shape.kind], c.shape.dtype == ADST_F64 ? "f64" : "f32", c.shape.nx,
+               c.shape.ny, c.shape.nz, plan.steps, (unsigned long long)budget,
+               kSched[plan.sched & 3], plan.slots, plan.slots + 1, plan.needs_state ? 1 : 0,
+               (long long)info.fwd_steps_total, (long long)info.recompute_steps,
+               (long long)info.adj_steps, (long long)info.n_actions, (long long)info.fwd_kernels,
+               (long long)info.adj_kernels, (unsigned long long)info.workspace_bytes,
+               (unsigned long long)info.alg_bytes);
+  if (log_level() >= 2) {
+    static const char* const kOp[7] = {"FWD", "SEED", "ADJ", "FWD2", "ADJ2", "FWDW", "ADJW"};
+    for (size_t i = 0; i < plan.acts.size(); ++i) {
+      const adst_action& a = plan.acts[i];
+      std::fprintf(stderr, "  %5zu %-4s t=%-6d src=%-3d dst=%-3d n=%d\n", i,
+                   (a.op >= 0 && a.op < 7) ? kOp[a.op] : "?", a.t, a.src, a.dst, a.n);
+    }
+  }
+}
+
 adst_status make_plan(const adst_problem* prob, int32_t steps, uint64_t budget, int32_t sched,
                       int32_t grads, Checked* c, Plan* plan) {
   adst_status st = check_problem(prob, grads, c);
@@ -302,49 +379,92 @@ adst_status check_disjoint(const std::vector<Range>& outs, const std::vector<Ran
   return ADST_OK;
 }
 
-// HIP event timing for ADST_TRACE. Events bracket maximal runs of launches
-// of one category (forward sweep, recomputation, seed, adjoint), so the
-// markers themselves add no gap between back-to-back kernels of a run.
+// Per-launch statistics of the last traced call on this thread.
+struct KernelStat {
+  std::string name;
+  int32_t phase = 0;
+  int64_t launches = 0;
+  double ms_sum = 0, ms_min = 0, ms_max = 0, alg_bytes = 0;
+};
+thread_local std::vector<KernelStat> g_kernel_stats;
+
+// HIP event timing for ADST_TRACE: an event pair brackets every launch (or
+// every pipelined sequence of launches), so the per-kernel averages are
+// kernel durations, comparable with a profiler's. Phases (forward sweep,
+// recomputation, adjoint, seed, the constants' final sum) are also marked
+// as roctx ranges whether or not the call is traced, for rocprofv3's marker
+// trace.
 class Tracer {
  public:
   enum Cat { SWEEP = 0, RECOMPUTE, ADJ, SEED, DPARAM, NCAT };
   explicit Tracer(bool on) : on_(on) {}
   ~Tracer() {
+    if (phase_open_) roctxRangePop();
     for (auto& g : segs_) {
-      if (g.start) hipEventDestroy(g.start);
-      if (g.stop) hipEventDestroy(g.stop);
+      if (g.start) (void)hipEventDestroy(g.start);
+      if (g.stop) (void)hipEventDestroy(g.stop);
     }
   }
-  // Call before enqueueing a launch of category cat.
-  hipError_t before(hipStream_t s, Cat cat) {
-    if (!on_ || (open_ && cat == cur_)) return hipSuccess;
-    hipError_t r = close(s);
+  // Call before enqueueing a launch (or a pipelined sequence of `launches`
+  // kernels) of category cat; alg_bytes are the algorithmic bytes it moves.
+  hipError_t begin(hipStream_t s, Cat cat, std::string label, double alg_bytes,
+                   int64_t launches = 1) {
+    if (!phase_open_ || cat != phase_) {
+      static const char* const kPhase[NCAT] = {"adst forward sweep", "adst recomputation",
+                                               "adst adjoint", "adst loss and seed",
+                                               "adst constants' gradients"};
+      if (phase_open_) roctxRangePop();
+      roctxRangePushA(kPhase[cat]);
+      phase_open_ = true;
+      phase_ = cat;
+    }
+    if (!on_) return hipSuccess;
+    Seg g{nullptr, nullptr, cat, std::move(label), alg_bytes, launches};
+    hipError_t r = hipEventCreate(&g.start);
     if (r != hipSuccess) return r;
-    Seg g{nullptr, nullptr, cat};
-    if ((r = hipEventCreate(&g.start)) != hipSuccess) return r;
     segs_.push_back(g);
-    open_ = true;
-    cur_ = cat;
+    if ((r = hipEventCreate(&segs_.back().stop)) != hipSuccess) return r;
     return hipEventRecord(segs_.back().start, s);
   }
-  hipError_t close(hipStream_t s) {
-    if (!on_ || !open_) return hipSuccess;
-    open_ = false;
-    hipError_t r = hipEventCreate(&segs_.back().stop);
-    if (r != hipSuccess) return r;
+  // Call after enqueueing what begin() announced.
+  hipError_t end(hipStream_t s) {
+    if (!on_ || segs_.empty()) return hipSuccess;
     return hipEventRecord(segs_.back().stop, s);
   }
-  // Waits for the last marker and fills the ms_* fields.
+  // Waits for the last marker, fills the ms_* fields and the per-kernel
+  // statistics adst_trace_kernels returns.
   hipError_t finish(hipStream_t s, adst_plan_info* info) {
+    (void)s;
+    if (phase_open_) {
+      roctxRangePop();
+      phase_open_ = false;
+    }
     if (!on_) return hipSuccess;
-    hipError_t r = close(s);
-    if (r != hipSuccess || segs_.empty()) return r;
-    if ((r = hipEventSynchronize(segs_.back().stop)) != hipSuccess) return r;
+    g_kernel_stats.clear();
+    if (segs_.empty()) return hipSuccess;
+    hipError_t r = hipEventSynchronize(segs_.back().stop);
+    if (r != hipSuccess) return r;
     float ms[NCAT] = {0, 0, 0, 0, 0};
     for (const Seg& g : segs_) {
       float dt = 0.f;
       if ((r = hipEventElapsedTime(&dt, g.start, g.stop)) != hipSuccess) return r;
       ms[g.cat] += dt;
+      KernelStat* k = nullptr;
+      for (KernelStat& e : g_kernel_stats)
+        if (e.name == g.label) k = &e;
+      if (!k) {
+        g_kernel_stats.push_back(KernelStat{});
+        k = &g_kernel_stats.back();
+        k->name = g.label;
+        k->phase = g.cat;
+        k->ms_min = 1e30;
+      }
+      const double per = double(dt) / double(g.launches);
+      k->launches += g.launches;
+      k->ms_sum += dt;
+      k->ms_min = std::min(k->ms_min, per);
+      k->ms_max = std::max(k->ms_max, per);
+      k->alg_bytes += g.alg_bytes;
     }
     float total = 0.f;
     if ((r = hipEventElapsedTime(&total, segs_.front().start, segs_.back().stop)) != hipSuccess)
@@ -364,15 +484,203 @@ class Tracer {
   struct Seg {
     hipEvent_t start, stop;
     Cat cat;
+    std::string label;
+    double alg_bytes;
+    int64_t launches;
   };
   bool on_;
-  bool open_ = false;
-  Cat cur_ = SWEEP;
+  bool phase_open_ = false;
+  Cat phase_ = SWEEP;
   std::vector<Seg> segs_;
 };
 
 adst_status hip_fail(hipError_t e, const char* what) {
   return fail(ADST_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+}  // namespace adst
+
+namespace adst {
+namespace {
+
+// adst_vjp: validation, then the plan's actions enqueued on the stream.
+adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
+                     int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
+                     void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
+                     void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
+  const int32_t grads = (dcoeff ? ADST_GRAD_COEFF : 0) | (dparams ? ADST_GRAD_PARAMS : 0);
+  const bool want_dk = dcoeff != nullptr;
+  Checked c;
+  Plan plan;
+  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, grads, &c, &plan);
+  if (st != ADST_OK) return st;
+  if (!x0 || !dx0) return fail(ADST_ERR_ARG, "x0 and dx0 are required");
+  if (prob->kind == ADST_VARDIFF2D9 && !coeff)
+    return fail(ADST_ERR_ARG, "the variable-coefficient kind needs coeff (K)");
+  if (loss < ADST_LOSS_HALF_SQ || loss > ADST_LOSS_SEED)
+    return fail(ADST_ERR_ARG, "unknown loss " + std::to_string(loss));
+  if (loss != ADST_LOSS_HALF_SQ && !loss_aux)
+    return fail(ADST_ERR_ARG, "this loss needs loss_aux");
+  const Layout L = layout_for(c, plan);
+  if (ws_bytes < L.total || !ws)
+    return fail(ADST_ERR_WORKSPACE, "adst_vjp needs " + std::to_string(L.total) +
+                                        " workspace bytes, got " + std::to_string(ws_bytes));
+  const uint64_t S = c.state_bytes;
+  std::vector<Range> outs = {range_of("dx0", dx0, S), range_of("ws", ws, L.total)};
+  if (dcoeff) outs.push_back(range_of("dcoeff", dcoeff, S));
+  if (xT) outs.push_back(range_of("xT", xT, S));
+  if (loss_dev) outs.push_back(range_of("loss_dev", loss_dev, sizeof(double)));
+  if (dparams) outs.push_back(range_of("dparams", dparams, 2 * sizeof(double)));
+  std::vector<Range> ins = {range_of("x0", x0, S)};
+  if (prob->kind == ADST_VARDIFF2D9) ins.push_back(range_of("coeff", coeff, S));
+  if (loss != ADST_LOSS_HALF_SQ) ins.push_back(range_of("loss_aux", loss_aux, S));
+  st = check_disjoint(outs, ins);
+  if (st != ADST_OK) return st;
+  if (info) fill_info(c, plan, mem_budget_bytes, want_dk, loss, info);
+  if (log_level() > 0) log_plan(c, plan, mem_budget_bytes, want_dk, loss);
+
+  // ---- interpret the plan
+  // The adjoint ping-pongs between dx0 and the workspace buffer G, one swap
+  // per adjoint launch; g_T starts where the last launch leaves g_0 in dx0.
+  // The in-place kind reverses its sweeps in dx0 itself.
+  char* wsb = static_cast<char*>(ws);
+  double* partials = reinterpret_cast<double*>(wsb);
+  double* loss_out = loss_dev ? loss_dev : reinterpret_cast<double*>(wsb + kLossOffset);
+  void* gws = wsb + L.g;
+  void* gcur = (c.in_place || plan.adj_launches % 2 == 0) ? dx0 : gws;
+  void* gnext = (gcur == dx0) ? gws : dx0;
+  void* const g_T = gcur;
+  double* dp_part = reinterpret_cast<double*>(wsb + L.dp);
+  auto buffer = [&](int32_t id) -> void* {
+    switch (id) {
+      case ADST_BUF_X0: return const_cast<void*>(x0);
+      case ADST_BUF_W0: return wsb + L.w0;
+      case ADST_BUF_W1: return wsb + L.w1;
+      case ADST_BUF_XT: return xT ? xT : g_T;
+      default: return wsb + L.slot0 + uint64_t(id - ADST_BUF_SLOT0) * L.state_stride;
+    }
+  };
+
+  Tracer tr(c.trace);
+  const PerPoint pp = per_point_bytes(c, want_dk, loss);
+  const double npts = double(c.npoints);
+  bool seeded = false, first_adj = true;
+  hipError_t e = hipSuccess;
+  auto traced = [&](Tracer::Cat cat, std::string label, double bytes, auto&& launch,
+                    int64_t launches = 1) -> hipError_t {
+    hipError_t r = tr.begin(stream, cat, std::move(label), bytes, launches);
+    if (r == hipSuccess) r = launch();
+    if (r == hipSuccess) r = tr.end(stream);
+    return r;
+  };
+  for (size_t ai = 0; ai < plan.acts.size(); ++ai) {
+    const adst_action& a = plan.acts[ai];
+    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
+    const Tracer::Cat cat = fwd_op               ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
+                            : a.op == ADST_OP_SEED ? Tracer::SEED
+                                                   : Tracer::ADJ;
+    if (c.in_place && a.op != ADST_OP_SEED) {
+      const bool adj = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJW;
+      if (!adj && a.op != ADST_OP_FWD && a.op != ADST_OP_FWDW) return hip_fail(hipErrorInvalidValue, "plan");
+      e = traced(cat, kernel_label(c, a, 1, false),
+                 npts * double(a.n) * double(adj ? pp.adj : pp.fwd),
+                 [&] {
+                   return adj ? launch_gs_adjoint(c.shape, dx0, a.n, stream)
+                              : launch_gs_forward(c.shape, buffer(a.src), buffer(a.dst), a.n,
+                                                  stream);
+                 },
+                 gs_kernel_launches(c.shape, adj, a.n));
+      if (e != hipSuccess) return hip_fail(e, "kernel launch");
+      continue;
+    }
+    switch (a.op) {
+      case ADST_OP_FWD: {
+        const int32_t r = stored_run(plan.acts, ai, c.store_fwd);
+        const double bytes = npts * double(pp.fwd + uint64_t(r - 1) * itemsize(c.shape.dtype));
+        if (r >= 2) {  // one launch writes the run's r states
+          void* ys[kMaxStoredRun];
+          for (int32_t k = 0; k < r; ++k) ys[k] = buffer(plan.acts[ai + k].dst);
+          e = traced(cat, kernel_label(c, a, r, false), bytes, [&] {
+            return launch_forward_store(c.shape, buffer(a.src), coeff, ys, r, stream);
+          });
+          ai += r - 1;
+        } else {
+          e = traced(cat, kernel_label(c, a, 1, false), bytes, [&] {
+            return launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
+          });
+        }
+        break;
+      }
+      case ADST_OP_FWD2:
+        e = traced(cat, kernel_label(c, a, 1, false), npts * double(pp.fwd), [&] {
+          return launch_forward_n(c.shape, buffer(a.src), coeff, buffer(a.dst), a.n, stream);
+        });
+        break;
+      case ADST_OP_SEED: {
+        const void* xsrc = buffer(a.src);
+        void* xcopy = (steps == 0 && xT) ? xT : nullptr;
+        e = traced(cat, "seed_loss", npts * double(pp.seed), [&] {
+          return launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, g_T, xcopy, partials,
+                             stream);
+        });
+        if (e == hipSuccess)
+          e = traced(cat, "finalize_loss", 8.0 * seed_partials(c.npoints), [&] {
+            return launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
+          });
+        if (e == hipSuccess && steps == 0 && dcoeff)
+          e = traced(cat, "fill_zero", double(S), [&] {
+            return launch_fill_zero(dcoeff, (int64_t)S, stream);
+          });
+        if (e == hipSuccess && steps == 0 && dparams)
+          e = traced(cat, "fill_zero", 16.0, [&] {
+            return launch_fill_zero(dparams, 2 * sizeof(double), stream);
+          });
+        seeded = true;
+        break;
+      }
+      case ADST_OP_ADJ: {
+        const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
+        if (c.shape.limit && !adjoint_applies_limit(c.shape, dparams != nullptr)) {
+          // the branch each point took at step t (otherwise applied by the
+          // adjoint launch itself)
+          e = traced(cat, "limit_mask", npts * double(pp.mask), [&] {
+            return launch_limit_mask(c.shape, xs, coeff, gcur, stream);
+          });
+          if (e != hipSuccess) return hip_fail(e, "kernel launch");
+        }
+        // with dparams, the launch also adds this step's share of the
+        // constants' gradients, from g_t and x_{t-1}
+        const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
+        e = traced(cat, kernel_label(c, a, 1, dparams != nullptr), bytes, [&] {
+          return launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps,
+                                dparams ? dp_part : nullptr, a.t == steps, stream);
+        });
+        std::swap(gcur, gnext);
+        first_adj = false;
+        break;
+      }
+      case ADST_OP_ADJ2:
+        e = traced(cat, kernel_label(c, a, 1, false), npts * double(pp.adj), [&] {
+          return launch_adjoint_n(c.shape, gcur, gnext, a.n, stream);
+        });
+        std::swap(gcur, gnext);
+        first_adj = false;
+        break;
+      default:
+        e = hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  }
+  if (dparams && steps > 0) {
+    e = traced(Tracer::DPARAM, "dparam_finalize", 16.0 * dparam_slots(c.shape), [&] {
+      return launch_dparam_finalize(c.shape, dp_part, dparams, stream);
+    });
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  }
+  if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");
+  g_last_error.clear();
+  return ADST_OK;
 }
 
 }  // namespace
@@ -468,140 +776,8 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
                      int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
                      void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
                      void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
-  const int32_t grads = (dcoeff ? ADST_GRAD_COEFF : 0) | (dparams ? ADST_GRAD_PARAMS : 0);
-  const bool want_dk = dcoeff != nullptr;
-  Checked c;
-  Plan plan;
-  adst_status st = make_plan(prob, steps, mem_budget_bytes, sched, grads, &c, &plan);
-  if (st != ADST_OK) return st;
-  if (!x0 || !dx0) return fail(ADST_ERR_ARG, "x0 and dx0 are required");
-  if (prob->kind == ADST_VARDIFF2D9 && !coeff)
-    return fail(ADST_ERR_ARG, "the variable-coefficient kind needs coeff (K)");
-  if (loss < ADST_LOSS_HALF_SQ || loss > ADST_LOSS_SEED)
-    return fail(ADST_ERR_ARG, "unknown loss " + std::to_string(loss));
-  if (loss != ADST_LOSS_HALF_SQ && !loss_aux)
-    return fail(ADST_ERR_ARG, "this loss needs loss_aux");
-  const Layout L = layout_for(c, plan);
-  if (ws_bytes < L.total || !ws)
-    return fail(ADST_ERR_WORKSPACE, "adst_vjp needs " + std::to_string(L.total) +
-                                        " workspace bytes, got " + std::to_string(ws_bytes));
-  const uint64_t S = c.state_bytes;
-  std::vector<Range> outs = {range_of("dx0", dx0, S), range_of("ws", ws, L.total)};
-  if (dcoeff) outs.push_back(range_of("dcoeff", dcoeff, S));
-  if (xT) outs.push_back(range_of("xT", xT, S));
-  if (loss_dev) outs.push_back(range_of("loss_dev", loss_dev, sizeof(double)));
-  if (dparams) outs.push_back(range_of("dparams", dparams, 2 * sizeof(double)));
-  std::vector<Range> ins = {range_of("x0", x0, S)};
-  if (prob->kind == ADST_VARDIFF2D9) ins.push_back(range_of("coeff", coeff, S));
-  if (loss != ADST_LOSS_HALF_SQ) ins.push_back(range_of("loss_aux", loss_aux, S));
-  st = check_disjoint(outs, ins);
-  if (st != ADST_OK) return st;
-  if (info) fill_info(c, plan, mem_budget_bytes, want_dk, loss, info);
-
-  // ---- interpret the plan
-  // The adjoint ping-pongs between dx0 and the workspace buffer G, one swap
-  // per adjoint launch; g_T starts where the last launch leaves g_0 in dx0.
-  // The in-place kind reverses its sweeps in dx0 itself.
-  char* wsb = static_cast<char*>(ws);
-  double* partials = reinterpret_cast<double*>(wsb);
-  double* loss_out = loss_dev ? loss_dev : reinterpret_cast<double*>(wsb + kLossOffset);
-  void* gws = wsb + L.g;
-  void* gcur = (c.in_place || plan.adj_launches % 2 == 0) ? dx0 : gws;
-  void* gnext = (gcur == dx0) ? gws : dx0;
-  void* const g_T = gcur;
-  double* dp_part = reinterpret_cast<double*>(wsb + L.dp);
-  auto buffer = [&](int32_t id) -> void* {
-    switch (id) {
-      case ADST_BUF_X0: return const_cast<void*>(x0);
-      case ADST_BUF_W0: return wsb + L.w0;
-      case ADST_BUF_W1: return wsb + L.w1;
-      case ADST_BUF_XT: return xT ? xT : g_T;
-      default: return wsb + L.slot0 + uint64_t(id - ADST_BUF_SLOT0) * L.state_stride;
-    }
-  };
-
-  Tracer tr(c.trace);
-  bool seeded = false;
-  hipError_t e = hipSuccess;
-  for (size_t ai = 0; ai < plan.acts.size(); ++ai) {
-    const adst_action& a = plan.acts[ai];
-    const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
-    const Tracer::Cat cat = fwd_op               ? (seeded ? Tracer::RECOMPUTE : Tracer::SWEEP)
-                            : a.op == ADST_OP_SEED ? Tracer::SEED
-                                                   : Tracer::ADJ;
-    if ((e = tr.before(stream, cat)) != hipSuccess) return hip_fail(e, "trace event");
-    if (c.in_place && a.op != ADST_OP_SEED) {
-      if (a.op == ADST_OP_FWD || a.op == ADST_OP_FWDW)
-        e = launch_gs_forward(c.shape, buffer(a.src), buffer(a.dst), a.n, stream);
-      else if (a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJW)
-        e = launch_gs_adjoint(c.shape, dx0, a.n, stream);
-      else
-        e = hipErrorInvalidValue;
-      if (e != hipSuccess) return hip_fail(e, "kernel launch");
-      continue;
-    }
-    switch (a.op) {
-      case ADST_OP_FWD: {
-        const int32_t r = stored_run(plan.acts, ai, c.store_fwd);
-        if (r >= 2) {  // one launch writes the run's r states
-          void* ys[kMaxStoredRun];
-          for (int32_t k = 0; k < r; ++k) ys[k] = buffer(plan.acts[ai + k].dst);
-          e = launch_forward_store(c.shape, buffer(a.src), coeff, ys, r, stream);
-          ai += r - 1;
-        } else {
-          e = launch_forward(c.shape, buffer(a.src), coeff, buffer(a.dst), stream);
-        }
-        break;
-      }
-      case ADST_OP_FWD2:
-        e = launch_forward_n(c.shape, buffer(a.src), coeff, buffer(a.dst), a.n, stream);
-        break;
-      case ADST_OP_SEED: {
-        const void* xsrc = buffer(a.src);
-        void* xcopy = (steps == 0 && xT) ? xT : nullptr;
-        e = launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, g_T, xcopy, partials,
-                        stream);
-        if (e == hipSuccess)
-          e = launch_finalize(partials, seed_partials(c.npoints), loss_out, stream);
-        if (e == hipSuccess && steps == 0 && dcoeff)
-          e = launch_fill_zero(dcoeff, (int64_t)S, stream);
-        if (e == hipSuccess && steps == 0 && dparams)
-          e = launch_fill_zero(dparams, 2 * sizeof(double), stream);
-        seeded = true;
-        break;
-      }
-      case ADST_OP_ADJ: {
-        const void* xs = a.src == ADST_BUF_NONE ? nullptr : buffer(a.src);
-        if (c.shape.limit && !adjoint_applies_limit(c.shape, dparams != nullptr)) {
-          // the branch each point took at step t (otherwise applied by the
-          // adjoint launch itself)
-          e = launch_limit_mask(c.shape, xs, coeff, gcur, stream);
-          if (e != hipSuccess) return hip_fail(e, "kernel launch");
-        }
-        // with dparams, the launch also adds this step's share of the
-        // constants' gradients, from g_t and x_{t-1}
-        e = launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps,
-                           dparams ? dp_part : nullptr, a.t == steps, stream);
-        std::swap(gcur, gnext);
-        break;
-      }
-      case ADST_OP_ADJ2:
-        e = launch_adjoint_n(c.shape, gcur, gnext, a.n, stream);
-        std::swap(gcur, gnext);
-        break;
-      default:
-        e = hipErrorInvalidValue;
-    }
-    if (e != hipSuccess) return hip_fail(e, "kernel launch");
-  }
-  if (dparams && steps > 0) {
-    if ((e = tr.before(stream, Tracer::DPARAM)) != hipSuccess) return hip_fail(e, "trace event");
-    if ((e = launch_dparam_finalize(c.shape, dp_part, dparams, stream)) != hipSuccess)
-      return hip_fail(e, "kernel launch");
-  }
-  if ((e = tr.finish(stream, info)) != hipSuccess) return hip_fail(e, "trace");
-  g_last_error.clear();
-  return ADST_OK;
+  return vjp_impl(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0, dcoeff,
+                  xT, loss_dev, dparams, ws, ws_bytes, stream, info);
 }
 
 adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,
@@ -633,6 +809,44 @@ adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,
     info->objective = r.objective;
     info->peak = r.peak;
   }
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream) {
+  if (bytes == 0) {
+    g_last_error.clear();
+    return ADST_OK;
+  }
+  if (!dst || !src) return fail(ADST_ERR_ARG, "dst and src are required");
+  if ((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src) | bytes) & 3u)
+    return fail(ADST_ERR_ARG, "dst, src and bytes must be multiples of 4");
+  if (bytes > (uint64_t(1) << 62)) return fail(ADST_ERR_ARG, "bytes too large");
+  const adst_status st = check_disjoint({range_of("dst", dst, bytes)}, {range_of("src", src, bytes)});
+  if (st != ADST_OK) return st;
+  const hipError_t e = launch_copy(dst, src, (int64_t)bytes, stream);
+  if (e != hipSuccess) return hip_fail(e, "copy");
+  g_last_error.clear();
+  return ADST_OK;
+}
+
+adst_status adst_trace_kernels(adst_kernel_stat* out, int32_t cap, int32_t* n_out) {
+  if (!n_out) return fail(ADST_ERR_ARG, "n_out is NULL");
+  if (cap < 0 || (cap > 0 && !out)) return fail(ADST_ERR_ARG, "bad output capacity");
+  const int32_t n = (int32_t)g_kernel_stats.size();
+  for (int32_t i = 0; i < std::min(n, cap); ++i) {
+    const KernelStat& k = g_kernel_stats[i];
+    adst_kernel_stat& o = out[i];
+    o = adst_kernel_stat{};
+    std::snprintf(o.name, sizeof(o.name), "%s", k.name.c_str());
+    o.phase = k.phase;
+    o.launches = k.launches;
+    o.ms_sum = k.ms_sum;
+    o.ms_min = k.ms_min;
+    o.ms_max = k.ms_max;
+    o.alg_bytes_sum = k.alg_bytes;
+  }
+  *n_out = n;
   g_last_error.clear();
   return ADST_OK;
 }

@@ -215,3 +215,29 @@ def test_forward_argument_errors():
     assert fwd(xT=X0) == adst.ADST_ERR_ARG
     assert fwd(ws_bytes=10) == adst.ADST_ERR_WORKSPACE
     assert fwd(ws=XT + 16) == adst.ADST_ERR_ARG
+
+
+# ---- the binding's tensor checks (before any plan or launch)
+def _t(*shape, dtype=None):
+    import torch
+    return torch.zeros(*shape, dtype=dtype or torch.float64)
+
+
+@pytest.mark.parametrize("make,msg", [
+    (lambda: dict(x0=_t(8, 9).t()), "contiguous"),
+    (lambda: dict(x0=_t(8, 9), coeff=_t(8, 9, dtype=__import__("torch").float32)), "dtype"),
+    (lambda: dict(x0=_t(8, 9), coeff=_t(9, 8)), "shape"),
+    (lambda: dict(x0=_t(8, 9), aux=_t(8, 18)[:, ::2]), "contiguous"),
+    (lambda: dict(x0=_t(8, 9), aux=_t(1, 9).expand(8, 9)), "contiguous"),
+    (lambda: dict(x0=_t(8, 9)), "GPU"),
+    (lambda: dict(x0=_t(8, 9, dtype=__import__("torch").int32)), "dtype"),
+])
+def test_binding_rejects_bad_tensors(make, msg):
+    kw = make()
+    with pytest.raises((ValueError, TypeError), match=msg):
+        adst.vjp(adst.ADST_VARDIFF2D9, kw.pop("x0"), kw.get("coeff"), 3,
+                 adst.ADST_LOSS_HALF_SQ_DIFF, kw.get("aux"))
+    if "aux" not in kw:
+        kw2 = make()
+        with pytest.raises((ValueError, TypeError), match=msg):
+            adst.forward(adst.ADST_VARDIFF2D9, kw2.pop("x0"), kw2.get("coeff"), 3)

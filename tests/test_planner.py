@@ -313,27 +313,3 @@ def test_elided_jacobi_fuses_everything():
     pn = prob(flags=adst.ADST_NO_FUSE)
     info = adst.adst_plan(pn, 30, budget_for(4), adst.ADST_SCHED_BINOMIAL)
     assert info.fwd_launches == info.fwd_steps_total
-
-
-@pytest.mark.parametrize("kind,dtype,dims,grads,budget_states,sched,T", [
-    (adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8), 0, 8, adst.ADST_SCHED_BINOMIAL, 50),
-    (adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8), 0, 7, adst.ADST_SCHED_BINOMIAL, 200),
-    (adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8), 0, 60, adst.ADST_SCHED_STORE_ALL, 31),
-    (adst.ADST_VARDIFF2D9, adst.ADST_F32, (10, 9, 1), adst.ADST_GRAD_COEFF, 16,
-     adst.ADST_SCHED_BINOMIAL, 200),
-    (adst.ADST_VARDIFF2D9, adst.ADST_F32, (10, 9, 1), adst.ADST_GRAD_COEFF, 5,
-     adst.ADST_SCHED_UNIFORM, 40),
-])
-def test_bench_kernel_mix_counts_the_library_launches(kind, dtype, dims, grads, budget_states,
-                                                     sched, T):
-    # bench.py names the launches of a plan from its actions; its grouping of
-    # store-through runs must give the library's own forward launch count
-    import bench
-    isz = 8 if dtype == adst.ADST_F64 else 4
-    S = dims[0] * dims[1] * dims[2] * isz
-    p = adst.make_problem(kind, dtype, dims)
-    acts = adst.adst_plan_actions(p, T, budget_states * S, sched, grads)
-    info = adst.adst_plan(p, T, budget_states * S, sched, grads)
-    mix = bench.kernel_mix(kind, acts, False, store_depth=bench.STORE_DEPTH[kind])
-    assert sum(mix.values()) == info.fwd_kernels
-    assert sum(bench.kernel_mix(kind, acts, True).values()) == info.adj_kernels
