@@ -306,6 +306,31 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
                      void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
                      void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info);
 
+/* ---- Without allocation -------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): adst_vjp
+ * with its workspace in a static device array of ADST_STATIC_WS_BYTES
+ * (64 MiB) per GPU instead of a caller buffer. The array is part of the
+ * library's code object: each GPU the library runs on holds its own copy
+ * until the process ends; its address is looked up on the call's first use
+ * of a device, with no allocation. Arguments, outputs, plan and results are
+ * those of adst_vjp with the same arguments (bit for bit: the same kernels
+ * run). No part of the workspace needs to start at zero: every value the
+ * call reads from it was written earlier in the same call. Every call on a
+ * GPU shares that GPU's array, so calls that overlap on one GPU (on
+ * different streams, or from several host threads) race and must be
+ * serialised by the caller. Calls no hipMalloc, hipFree or allocating
+ * library routine.
+ * Errors: as adst_vjp; ADST_ERR_WORKSPACE when the plan's workspace_bytes
+ * (adst_plan) exceed ADST_STATIC_WS_BYTES; ADST_ERR_ARG with ADST_TRACE
+ * (tracing creates HIP events). */
+#define ADST_STATIC_WS_BYTES (64ull << 20)
+adst_status adst_vjp_static_ws(const adst_problem* prob, const void* x0, const void* coeff,
+                               int32_t steps, int32_t loss, const void* loss_aux,
+                               uint64_t mem_budget_bytes, int32_t sched, void* dx0, void* dcoeff,
+                               void* xT, double* loss_dev, double* dparams, hipStream_t stream,
+                               adst_plan_info* info);
+
 /* ---- Store/recompute selection for a general program (Sec. IV) --------
  * The integer program of Sec. IV-A: one binary per forwarded array (store or
  * recompute), objective sum_i cost_i * (1 - store_i), and every memory

@@ -27,7 +27,9 @@ ADST_OP_FWD, ADST_OP_SEED, ADST_OP_ADJ, ADST_OP_FWD2, ADST_OP_ADJ2, ADST_OP_FWDW
 ADST_BUF_NONE, ADST_BUF_X0, ADST_BUF_W0, ADST_BUF_W1, ADST_BUF_XT, ADST_BUF_SLOT0 = -1, 0, 1, 2, 3, 4
 
 EXPORTED = ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
-            "adst_trace_kernels", "adst_copy", "adst_status_str", "adst_last_error")
+            "adst_trace_kernels", "adst_copy", "adst_vjp_static_ws", "adst_status_str",
+            "adst_last_error")
+ADST_STATIC_WS_BYTES = 64 << 20
 PHASE_NAMES = ("forward sweep", "recomputation", "adjoint", "loss and seed", "constants")
 ILP_EVENTS = {"alloc": 0, "free": 1, "produce": 2, "drop": 3, "recompute": 4,
               "recompute_done": 5, "release": 6, "path": 7}
@@ -112,10 +114,12 @@ def lib():
                            u64, vp, P(adst_plan_info)]
     L.adst_ilp_solve.argtypes = [P(adst_ilp_array), i32, P(adst_ilp_event), i64, ctypes.c_double,
                                  P(i32), P(adst_ilp_info)]
+    L.adst_vjp_static_ws.argtypes = [P(adst_problem), vp, vp, i32, i32, vp, u64, i32, vp, vp, vp,
+                                     vp, vp, vp, P(adst_plan_info)]
     L.adst_trace_kernels.argtypes = [P(adst_kernel_stat), i32, P(i32)]
     L.adst_copy.argtypes = [vp, vp, u64, vp]
     for f in ("adst_plan", "adst_plan_actions", "adst_forward", "adst_vjp", "adst_ilp_solve",
-              "adst_trace_kernels", "adst_copy"):
+              "adst_trace_kernels", "adst_copy", "adst_vjp_static_ws"):
         getattr(L, f).restype = ctypes.c_int
     L.adst_status_str.argtypes = [ctypes.c_int]
     L.adst_status_str.restype = ctypes.c_char_p
@@ -203,6 +207,19 @@ def adst_vjp(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx
                           mem_budget_bytes, sched, _ptr(dx0), _ptr(dcoeff), _ptr(xT),
                           _ptr(loss_dev), _ptr(dparams), _ptr(ws), ws_bytes, _stream(stream),
                           ctypes.byref(info) if info is not None else None))
+    return info
+
+
+def adst_vjp_static_ws(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0,
+                       dcoeff, xT, loss_dev, dparams, stream=None, want_info=True):
+    """adst_vjp with the library's static per-GPU workspace (no allocation;
+    plans whose workspace exceeds ADST_STATIC_WS_BYTES are rejected)."""
+    info = adst_plan_info() if want_info else None
+    _check(lib().adst_vjp_static_ws(ctypes.byref(prob), _ptr(x0), _ptr(coeff), steps, loss,
+                                    _ptr(loss_aux), mem_budget_bytes, sched, _ptr(dx0),
+                                    _ptr(dcoeff), _ptr(xT), _ptr(loss_dev), _ptr(dparams),
+                                    _stream(stream),
+                                    ctypes.byref(info) if info is not None else None))
     return info
 
 

@@ -504,11 +504,13 @@ adst_status hip_fail(hipError_t e, const char* what) {
 namespace adst {
 namespace {
 
-// adst_vjp: validation, then the plan's actions enqueued on the stream.
+// adst_vjp, with the workspace either the caller's (ws, ws_bytes) or, with
+// static_ws, this device's static workspace.
 adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff, int32_t steps,
                      int32_t loss, const void* loss_aux, uint64_t mem_budget_bytes, int32_t sched,
                      void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
-                     void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
+                     void* ws, uint64_t ws_bytes, bool static_ws, hipStream_t stream,
+                     adst_plan_info* info) {
   const int32_t grads = (dcoeff ? ADST_GRAD_COEFF : 0) | (dparams ? ADST_GRAD_PARAMS : 0);
   const bool want_dk = dcoeff != nullptr;
   Checked c;
@@ -523,6 +525,18 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
   if (loss != ADST_LOSS_HALF_SQ && !loss_aux)
     return fail(ADST_ERR_ARG, "this loss needs loss_aux");
   const Layout L = layout_for(c, plan);
+  if (static_ws) {
+    if (c.trace)
+      return fail(ADST_ERR_ARG, "ADST_TRACE creates HIP events: use adst_vjp to trace");
+    if (L.total > kStaticWsBytes)
+      return fail(ADST_ERR_WORKSPACE,
+                  "adst_vjp_static_ws: this plan needs " + std::to_string(L.total) +
+                      " workspace bytes; the static workspace holds " +
+                      std::to_string(kStaticWsBytes) + " (use adst_vjp with a caller buffer)");
+    const hipError_t e = static_workspace(&ws);
+    if (e != hipSuccess) return hip_fail(e, "static workspace");
+    ws_bytes = kStaticWsBytes;
+  }
   if (ws_bytes < L.total || !ws)
     return fail(ADST_ERR_WORKSPACE, "adst_vjp needs " + std::to_string(L.total) +
                                         " workspace bytes, got " + std::to_string(ws_bytes));
@@ -777,7 +791,16 @@ adst_status adst_vjp(const adst_problem* prob, const void* x0, const void* coeff
                      void* dx0, void* dcoeff, void* xT, double* loss_dev, double* dparams,
                      void* ws, uint64_t ws_bytes, hipStream_t stream, adst_plan_info* info) {
   return vjp_impl(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0, dcoeff,
-                  xT, loss_dev, dparams, ws, ws_bytes, stream, info);
+                  xT, loss_dev, dparams, ws, ws_bytes, false, stream, info);
+}
+
+adst_status adst_vjp_static_ws(const adst_problem* prob, const void* x0, const void* coeff,
+                               int32_t steps, int32_t loss, const void* loss_aux,
+                               uint64_t mem_budget_bytes, int32_t sched, void* dx0, void* dcoeff,
+                               void* xT, double* loss_dev, double* dparams, hipStream_t stream,
+                               adst_plan_info* info) {
+  return vjp_impl(prob, x0, coeff, steps, loss, loss_aux, mem_budget_bytes, sched, dx0, dcoeff,
+                  xT, loss_dev, dparams, nullptr, 0, true, stream, info);
 }
 
 adst_status adst_ilp_solve(const adst_ilp_array* arrays, int32_t n_arrays,

@@ -123,4 +123,11 @@ hipError_t launch_dparam_finalize(const StepShape& s, const double* partials, do
 hipError_t launch_fill_zero(void* p, int64_t bytes, hipStream_t stream);
 hipError_t launch_copy(void* dst, const void* src, int64_t bytes, hipStream_t stream);
 
+// The static workspace of adst_vjp_static_ws: kStaticWsBytes of device memory
+// per GPU, held from the library's first use on that GPU to the end of the
+// process. static_workspace() returns the current device's address of it
+// (looked up once per device; no allocation).
+constexpr uint64_t kStaticWsBytes = uint64_t(64) << 20;
+hipError_t static_workspace(void** ptr);
+
 }  // namespace adst
