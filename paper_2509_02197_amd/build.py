@@ -19,7 +19,8 @@ ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 HOST_SOURCES = ["planner.cpp", "ilp.cpp", "abi.cpp"]
-HIP_SOURCES = ["kernels.hip", "jacobi_march.hip", "gauss_seidel.hip", "static_ws.hip"]
+HIP_SOURCES = ["kernels.hip", "allencahn.hip", "jacobi_march.hip", "gauss_seidel.hip",
+               "static_ws.hip"]
 
 COMMON = ["-std=c++17", "-O3", "-fPIC", "-ffp-contract=off", "-Wall",
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

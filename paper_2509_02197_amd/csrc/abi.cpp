@@ -49,6 +49,7 @@ struct Checked {
   bool trace = false;
   int32_t fuse_fwd = 1, fuse_adj = 1;  // most steps per launch
   int32_t store_fwd = 1;  // most single steps per launch that stores every state
+  bool fuse_adj_fwd = false;  // a recomputed step may share the adjoint's launch
   bool in_place = false;  // the Gauss-Seidel kind: pipelined sweeps, adjoint in place
   bool want_dk = false, want_dp = false;
 };
@@ -107,20 +108,51 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   out->fuse_adj = fuse ? max_fused_adjoint(p->kind, p->n[0]) : 1;
   out->in_place = p->kind == ADST_GAUSSSEIDEL2D5;
   out->store_fwd = (fuse && !limit) ? max_stored_forward(p->kind) : 1;
+  out->fuse_adj_fwd = fuse && p->kind == ADST_ALLENCAHN3D7 && ac_fuses_forward_adjoint(out->shape);
   return ADST_OK;
+}
+
+// A forward step whose result only the next action, the adjoint step that
+// reads it as x_{t-1}, uses: the two run as one launch (ac_launch_forward_
+// adjoint), x_{t-1} formed on chip and never written. True when acts[i] is
+// that forward step: the kind's adjoint reads x_{t-1} only pointwise
+// (Allen-Cahn without the limiter or the constants' gradients), and no later
+// action reads the buffer before it is written again.
+bool fused_fwd_adj(const Checked& c, const std::vector<adst_action>& acts, size_t i) {
+  if (c.shape.kind != ADST_ALLENCAHN3D7 || c.want_dp || c.shape.limit || !c.fuse_adj_fwd)
+    return false;
+  if (i + 1 >= acts.size()) return false;
+  const adst_action& f = acts[i];
+  const adst_action& g = acts[i + 1];
+  if (f.op != ADST_OP_FWD || f.n != 1 || g.op != ADST_OP_ADJ || g.src != f.dst ||
+      g.t != f.t + 1 || f.dst == f.src)
+    return false;
+  for (size_t k = i + 2; k < acts.size(); ++k) {
+    const adst_action& a = acts[k];
+    const bool reads = (a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW ||
+                        a.op == ADST_OP_ADJ || a.op == ADST_OP_SEED) && a.src == f.dst;
+    if (reads) return false;
+    const bool writes = (a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW) &&
+                        a.dst == f.dst;
+    if (writes) break;
+  }
+  return true;
 }
 
 // Length of the run of single forward steps starting at acts[i] that one
 // store-through launch takes (1: none): each action reads the state the one
 // before it wrote, and the states go to buffers that differ from each other
 // and from the run's input (which the launch reads while it writes them).
-int32_t stored_run(const std::vector<adst_action>& acts, size_t i, int32_t depth) {
-  if (depth < 2 || acts[i].op != ADST_OP_FWD) return 1;
+// A step fused with the adjoint after it ends the run before it.
+int32_t stored_run(const Checked& c, const std::vector<adst_action>& acts, size_t i) {
+  const int32_t depth = c.store_fwd;
+  if (depth < 2 || acts[i].op != ADST_OP_FWD || fused_fwd_adj(c, acts, i)) return 1;
   int32_t n = 1;
   while (n < depth && i + n < acts.size()) {
     const adst_action& a = acts[i + n];
     const adst_action& p = acts[i + n - 1];
     if (a.op != ADST_OP_FWD || a.src != p.dst || a.t != p.t + 1) break;
+    if (fused_fwd_adj(c, acts, i + n)) break;
     bool clash = a.dst == acts[i].src;
     for (int32_t k = 0; k < n; ++k) clash = clash || acts[i + k].dst == a.dst;
     if (clash) break;
@@ -210,6 +242,8 @@ std::string kernel_label(const Checked& c, const adst_action& a, int32_t stored,
   if (k == ADST_GAUSSSEIDEL2D5) return adj ? "gs_wave<adj>" : "gs_wave<fwd>";
   static const char* const kFwd[3] = {"fwd_jacobi2d5", "fwd_allencahn3d7", "fwd_vardiff2d9"};
   static const char* const kAdj[3] = {"adj_jacobi2d5", "adj_allencahn3d7", "adj_vardiff2d9"};
+  const bool march = k == ADST_ALLENCAHN3D7 && !c.shape.limit && ac_fuses_forward_adjoint(c.shape);
+  if (march && adj && a.n == 1 && !dparams) return "ac_march<adj>";
   if (!adj) {
     if (stored >= 2)
       return k == ADST_ALLENCAHN3D7
@@ -254,9 +288,10 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
     const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
     const bool adj_op = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJ2 || a.op == ADST_OP_ADJW;
     if (!fwd_op && !adj_op) continue;
+    if (fused_fwd_adj(c, plan.acts, i)) continue;  // counted with its adjoint
     const int64_t k = c.in_place ? gs_kernel_launches(c.shape, adj_op, a.n) : 1;
     (fwd_op ? info->fwd_kernels : info->adj_kernels) += k;
-    i += stored_run(plan.acts, i, c.store_fwd) - 1;
+    i += stored_run(c, plan.acts, i) - 1;
   }
   info->state_bytes = c.state_bytes;
   info->budget_bytes = budget;
@@ -273,7 +308,8 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
     const adst_action& a = plan.acts[i];
     switch (a.op) {
       case ADST_OP_FWD: {
-        const int32_t r = stored_run(plan.acts, i, c.store_fwd);
+        if (fused_fwd_adj(c, plan.acts, i)) break;  // moves the adjoint's bytes only
+        const int32_t r = stored_run(c, plan.acts, i);
         fwd_per_point += fb + uint64_t(r - 1) * itemsize(c.shape.dtype);
         i += r - 1;
         break;
@@ -610,7 +646,18 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
     }
     switch (a.op) {
       case ADST_OP_FWD: {
-        const int32_t r = stored_run(plan.acts, ai, c.store_fwd);
+        if (fused_fwd_adj(c, plan.acts, ai)) {
+          // this recomputed step and the adjoint step after it in one launch
+          const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
+          e = traced(Tracer::ADJ, "ac_march<fwd1+adj>", bytes, [&] {
+            return ac_launch_forward_adjoint(c.shape, buffer(a.src), gcur, gnext, stream);
+          });
+          std::swap(gcur, gnext);
+          first_adj = false;
+          ++ai;
+          break;
+        }
+        const int32_t r = stored_run(c, plan.acts, ai);
         const double bytes = npts * double(pp.fwd + uint64_t(r - 1) * itemsize(c.shape.dtype));
         if (r >= 2) {  // one launch writes the run's r states
           void* ys[kMaxStoredRun];

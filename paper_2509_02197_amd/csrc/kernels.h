@@ -22,6 +22,24 @@ struct StepShape {
 hipError_t launch_forward(const StepShape& s, const void* x, const void* K, void* y,
                           hipStream_t stream);
 
+// Allen-Cahn launchers (allencahn.hip): one forward step; n = 2..kAcMaxFuse
+// fused forward steps (mids: the intermediate states' buffers for a
+// store-through run, else null); one adjoint step with the constants'
+// gradients (dp_part, per-workgroup slots) or the limiter's mask.
+hipError_t ac_launch_forward(const StepShape& s, const void* x, void* y, hipStream_t st);
+hipError_t ac_launch_forward_steps(const StepShape& s, const void* x, void* y, void* const* mids,
+                                   int32_t n, hipStream_t st);
+hipError_t ac_launch_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
+                             double* dp_part, bool dp_first, hipStream_t st);
+int64_t ac_dparam_slots(const StepShape& s);
+// One recomputed forward step and the adjoint step that reads its result, in
+// one launch: g_prev = J_t^T g_next with x_{t-1} = F(x) formed on chip and
+// never stored (x = x_{t-2}); no limiter and no constants' gradients.
+// ac_fuses_forward_adjoint tells whether the shape takes it.
+hipError_t ac_launch_forward_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
+                                     hipStream_t st);
+bool ac_fuses_forward_adjoint(const StepShape& s);
+
 // Temporal blocking: the most steps one launch may take (1 = none). The
 // fused adjoint is for state-free adjoints only.
 constexpr int32_t kJacMaxFuse = 6;

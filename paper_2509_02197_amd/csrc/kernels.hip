@@ -21,53 +21,11 @@
 #include <type_traits>
 
 #include "adst.h"
+#include "device_common.h"
 #include "kernels.h"
 
 namespace adst {
 namespace {
-
-constexpr int kBX = 64;  // one wavefront along x
-constexpr int kBY = 4;   // four wavefronts per block
-constexpr int kThreads = kBX * kBY;
-
-// Launches cover their tiles in an XCD-aware order. Consecutive workgroup
-// ids go to the 8 XCDs in turn, and each XCD has its own L2; renumbering so
-// that XCD k works on the k-th contiguous eighth of the tiles keeps a tile's
-// x- and y-neighbours (whose cache lines its halo shares) in the same L2.
-// The grid is rounded up to a multiple of 8; surplus workgroups exit at once.
-__device__ inline int xcd_tile(int ntiles) {
-  const int per = (ntiles + 7) / 8;
-  return (int)(blockIdx.x % 8) * per + (int)(blockIdx.x / 8);
-}
-
-inline unsigned xcd_grid(int64_t ntiles) { return (unsigned)(8 * ((ntiles + 7) / 8)); }
-
-// Streaming stores. When a state is at least kStreamBytes, the states a
-// launch reads and writes exceed the 256 MB Infinity Cache and nothing reads
-// a written value again within the launch, so the Allen-Cahn and
-// variable-coefficient kernels store (and the Allen-Cahn adjoint reads its
-// once-read x) with non-temporal hints: written lines
-// then stop evicting the halo lines that neighbouring tiles read from L2
-// (measured at 512^3 f64: 4.7 -> 5.25 TB/s adjoint, 2393 -> 2193 ms for the
-// 1024^3 call). Below it, the written state is the next launch's input and
-// should stay in the Infinity Cache. The choice is a template argument: a
-// run-time branch between the two stores is merged by the compiler into one
-// store without the hint.
-constexpr int64_t kStreamBytes = int64_t(256) << 20;
-template <bool NT, class R>
-__device__ inline void put(R* p, R v) {
-  if constexpr (NT)
-    __builtin_nontemporal_store(v, p);
-  else
-    *p = v;
-}
-template <bool NT, class R>
-__device__ inline R take(const R* p) {
-  if constexpr (NT)
-    return __builtin_nontemporal_load(p);
-  else
-    return *p;
-}
 
 // ------------------------------------------------------- 2-D LDS tiles
 // A workgroup owns a tile of the output: one thread per column, several
@@ -104,55 +62,6 @@ __device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int
         dst[e] = (c >= 0 && c < nx) ? a[jj * nx + c] : R(0);
       }
     }
-  }
-}
-
-// ------------------------------------------------------- block reductions
-// Sum over the 256 threads of a block: a wave64 butterfly, then the four
-// wave sums in a fixed order. Valid in thread 0.
-__device__ inline double block_sum(double v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  __shared__ double wave_sum[kThreads / 64];
-  const int tid = threadIdx.y * kBX + threadIdx.x;
-  if ((tid & 63) == 0) wave_sum[tid >> 6] = v;
-  __syncthreads();
-  return ((wave_sum[0] + wave_sum[1]) + wave_sum[2]) + wave_sum[3];
-}
-
-// Block sums of two values, each over the 256 threads in a fixed order.
-__device__ inline void block_sum2(double& a, double& b) {
-  a = block_sum(a);
-  __syncthreads();  // block_sum's wave sums are reused
-  b = block_sum(b);
-}
-
-// Gradients of the step constants, fused into the adjoint kernels: one
-// adjoint step's share of dL/dp is the sum over points of g_t[c] times the
-// step's partial dF_c/dp at x_{t-1} (a constant read by every point of every
-// step is a multiply-read input whose gradient accumulates, Sec. II). The
-// partials are the sub-expressions the forward step forms, in its order:
-//   Jacobi               dF/dw  = (((x[c]+x[W])+x[E])+x[S])+x[N] on interior points
-//   Allen-Cahn           dF/dD  = lap,   dF/dC = -((x[c]*x[c])*x[c])
-//   variable coefficient dF/ddt = acc
-// Products and sums are in double. Each workgroup (one tile of the adjoint
-// launch, whose tiling depends only on the grid) sums its points in a fixed
-// order and adds the result into its own slot, step after step in the
-// adjoint order t = T..1 (first: the step t = T overwrites), so the result
-// does not depend on the schedule. part holds nslots slots per constant.
-struct DpOut {
-  double* part;
-  int nslots, first;
-};
-
-// All threads of the block call this (it synchronises).
-__device__ inline void dp_commit(DpOut dp, int slot, double a0, double a1) {
-  block_sum2(a0, a1);
-  if (threadIdx.x == 0 && threadIdx.y == 0) {
-    double* p0 = dp.part + slot;
-    double* p1 = dp.part + dp.nslots + slot;
-    *p0 = dp.first ? a0 : *p0 + a0;
-    *p1 = dp.first ? a1 : *p1 + a1;
   }
 }
 
@@ -242,17 +151,6 @@ __device__ inline R vardiff_fwd_at(const R* sx, const R* sk, int q, int i, int j
     }
   }
   return xc + dt * acc;
-}
-
-// The limiter: a new value below lo becomes lo, above hi becomes hi (the
-// branch the step takes at each point; NaN passes through unchanged).
-template <class R>
-struct Limit {
-  R lo, hi;
-};
-template <class R>
-__device__ inline R limited(R y, Limit<R> l) {
-  return y < l.lo ? l.lo : (y > l.hi ? l.hi : y);
 }
 
 // Single-step tiles: TW columns x TR rows, halo one cell (staged as one
@@ -406,531 +304,6 @@ __global__ __launch_bounds__(kX2Threads) void adj_jacobi2d5_x2(const R* __restri
                                                                int tiles_x, int ntiles, int vec,
                                                                R w) {
   jacobi_tile_x2<R, true>(g, gp, nx, ny, tiles_x, ntiles, vec, w);
-}
-
-// ------------------------------------------------------- Allen-Cahn 3-D
-// 2.5-D blocking: a workgroup of 64 x 4 threads owns a 64 x 8 column of the
-// grid over kAcZC planes (two rows per thread) and marches in z. The plane
-// being updated is staged in LDS with a one-cell xy halo; the planes below
-// and above live in registers, so every input plane is read from HBM once
-// per tile.
-constexpr int kAcTX = 64, kAcTY = 8, kAcZC = 32;
-
-struct AcTile {
-  int b, i, ja, jb, by, bx, z0, z1;
-};
-
-__device__ inline bool ac_tile(int nx, int ny, int nz, int tiles_x, int tiles_y, int ntiles,
-                               AcTile* t) {
-  int b = xcd_tile(ntiles);
-  if (b >= ntiles) return false;
-  t->b = b;
-  t->bx = b % tiles_x;
-  b /= tiles_x;
-  t->by = b % tiles_y;
-  const int bz = b / tiles_y;
-  t->i = t->bx * kAcTX + (int)threadIdx.x;
-  t->ja = t->by * kAcTY + (int)threadIdx.y;
-  t->jb = t->ja + 4;
-  t->z0 = bz * kAcZC;
-  t->z1 = min(t->z0 + kAcZC, nz);
-  return true;
-}
-
-// Halo cell this thread stages (at most one; 2*64 + 2*8 = 144 < 256).
-__device__ inline void ac_halo_cell(int tid, int* ly, int* lx) {
-  constexpr int LY = kAcTY + 2, LX = kAcTX + 2;
-  const int h = tid;
-  if (h < kAcTX) {
-    *ly = 0;
-    *lx = h + 1;
-  } else if (h < 2 * kAcTX) {
-    *ly = LY - 1;
-    *lx = h - kAcTX + 1;
-  } else if (h < 2 * kAcTX + kAcTY) {
-    *ly = h - 2 * kAcTX + 1;
-    *lx = 0;
-  } else if (h < 2 * kAcTX + 2 * kAcTY) {
-    *ly = h - 2 * kAcTX - kAcTY + 1;
-    *lx = LX - 1;
-  } else {
-    *ly = -1;
-    *lx = 0;
-  }
-}
-
-// Forward, zero ghost values:
-//   lap = (((((x[-x]+x[+x])+x[-y])+x[+y])+x[-z])+x[+z]) - 6*a
-//   x'  = (a + D*lap) - C*((a*a)*a)
-// Single-step and fused kernels evaluate every point through this function.
-template <class R>
-__device__ inline R allencahn_point(R a, R xm, R xp, R ym, R yp, R zm, R zp, R D, R C) {
-  R lap = xm + xp;
-  lap += ym;
-  lap += yp;
-  lap += zm;
-  lap += zp;
-  lap = lap - R(6) * a;
-  return (a + D * lap) - C * ((a * a) * a);
-}
-
-template <class R, bool LIM, bool NT>
-__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict__ x,
-                                                             R* __restrict__ y, int nx, int ny,
-                                                             int nz, int tiles_x, int tiles_y,
-                                                             int ntiles, R D, R C, Limit<R> lim) {
-  auto out = [&](R v) { return LIM ? limited(v, lim) : v; };
-  __shared__ R tile[kAcTY + 2][kAcTX + 2];
-  AcTile t;
-  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;
-  const int plane = nx * ny;
-  auto ld = [&](int k, int j, int i) -> R {
-    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? x[k * plane + j * nx + i]
-                                                                      : R(0);
-  };
-  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
-  int hly, hlx;
-  ac_halo_cell(tid, &hly, &hlx);
-  const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
-  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
-  R belowA = ld(t.z0 - 1, t.ja, t.i), belowB = ld(t.z0 - 1, t.jb, t.i);
-  R curA = ld(t.z0, t.ja, t.i), curB = ld(t.z0, t.jb, t.i);
-  R halo = hly >= 0 ? ld(t.z0, hj, hi) : R(0);
-  for (int k = t.z0; k < t.z1; ++k) {
-    // the next plane's cells are requested before this plane is computed
-    const R aboveA = ld(k + 1, t.ja, t.i), aboveB = ld(k + 1, t.jb, t.i);
-    const R haloN = hly >= 0 ? ld(k + 1, hj, hi) : R(0);
-    __syncthreads();
-    tile[ty + 1][tx + 1] = curA;
-    tile[ty + 5][tx + 1] = curB;
-    if (hly >= 0) tile[hly][hlx] = halo;
-    __syncthreads();
-    if (va)
-      put<NT>(&y[k * plane + t.ja * nx + t.i],
-              out(allencahn_point(curA, tile[ty + 1][tx], tile[ty + 1][tx + 2], tile[ty][tx + 1],
-                                  tile[ty + 2][tx + 1], belowA, aboveA, D, C)));
-    if (vb)
-      put<NT>(&y[k * plane + t.jb * nx + t.i],
-              out(allencahn_point(curB, tile[ty + 5][tx], tile[ty + 5][tx + 2], tile[ty + 4][tx + 1],
-                                  tile[ty + 6][tx + 1], belowB, aboveB, D, C)));
-    belowA = curA;
-    belowB = curB;
-    curA = aboveA;
-    curB = aboveB;
-    halo = haloN;
-  }
-}
-
-// K forward steps in one launch (temporal blocking in 2.5-D).
-// A workgroup of 64 x 4 threads owns a region of 64 columns x SY = 4 RPT
-// rows of each plane (RPT rows per thread, four apart) and marches in z. At
-// iteration p it evaluates step 1 at plane p from x(p-1..p+1), and step l at
-// plane p-l+1 from step l-1's planes p-l..p-l+2. Every step is evaluated on
-// the whole region but is valid only on its inner (64 - 2(l-1)) x (SY -
-// 2(l-1)) cells, because its xy neighbours come from the step before it on
-// the same region; the last step's valid cells are the output tile. x(p)
-// (with a one-cell ring) and each intermediate step's latest plane are
-// staged in LDS for the xy neighbours, the planes below and above stay in
-// registers. Intermediate values are 0 outside the grid, which is the zero
-// ghost value the next step reads; every point evaluates the single-step
-// expression, so any split of the steps into launches gives the same bits.
-// Measured at 1024^3 f64, three steps per launch (64 x 16 regions, 64
-// planes) beat two (the launches of a recomputation run drop by a third);
-// four, with 24-row regions, needed 178 VGPRs and with 16-row regions
-// evaluated 7 points per output point, and both were slower.
-template <int K, int RPT, int NZ>
-struct AcN {
-  static constexpr int SX = kBX, SY = kBY * RPT;
-  static constexpr int OX = SX - 2 * (K - 1), OY = SY - 2 * (K - 1);  // output tile
-  static constexpr int ZC = NZ;                                     // output planes
-};
-
-// ST: the intermediate states are stored too, step l's into mid[l-1], each
-// point by the workgroup whose output tile holds it (a run of steps whose
-// every state is kept moves 8 + 8n bytes per point for n steps instead of
-// 16n). They are stored without the non-temporal hint: the reverse sweep
-// reads them back soon after (measured at 512^3: 58.9 -> 58.5 ms per call).
-template <class R, int K, int RPT, int NZ, bool NT, bool ST>
-__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restrict__ x,
-                                                               R* __restrict__ y,
-                                                               R* __restrict__ mid0,
-                                                               R* __restrict__ mid1, int nx,
-                                                               int ny, int nz, int tiles_x,
-                                                               int tiles_y, int ntiles, R D,
-                                                               R C) {
-  using A = AcN<K, RPT, NZ>;
-  constexpr int SX = A::SX, SY = A::SY, LX = SX + 2, LY = SY + 2, H = K - 1;
-  static_assert(K >= 2 && 2 * LX + 2 * SY <= kThreads, "ring cells: one per thread");
-  static_assert(!ST || K <= 3, "intermediate states go to mid0 (step 1) and mid1 (step 2)");
-  __shared__ R xt[LY][LX];
-  __shared__ R yt[K - 1][SY][SX];  // steps 1 .. K-1
-  int b = xcd_tile(ntiles);
-  if (b >= ntiles) return;
-  const int bx = b % tiles_x;
-  b /= tiles_x;
-  const int by = b % tiles_y;
-  const int bz = b / tiles_y;
-  const int i0 = bx * A::OX, j0 = by * A::OY;
-  const int z0 = bz * A::ZC, z1 = min(z0 + A::ZC, nz);
-  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
-  const int ic = i0 - H + tx;  // column of this thread
-  const int plane = nx * ny;
-  auto inxy = [&](int j, int i) { return i >= 0 && i < nx && j >= 0 && j < ny; };
-  auto ld = [&](int k, int j, int i) -> R {
-    return (k >= 0 && k < nz && inxy(j, i)) ? x[k * plane + j * nx + i] : R(0);
-  };
-  auto row = [&](int q) { return ty + kBY * q; };  // region row of the thread's q-th cell
-  // one cell of the LDS ring around the region
-  int hly = -1, hlx = 0;
-  if (tid < LX) {
-    hly = 0;
-    hlx = tid;
-  } else if (tid < 2 * LX) {
-    hly = LY - 1;
-    hlx = tid - LX;
-  } else if (tid < 2 * LX + SY) {
-    hly = tid - 2 * LX + 1;
-    hlx = 0;
-  } else if (tid < 2 * LX + 2 * SY) {
-    hly = tid - 2 * LX - SY + 1;
-    hlx = LX - 1;
-  }
-  const int hj = j0 - H - 1 + hly, hi = i0 - H - 1 + hlx;
-  // x at planes p-1, p, p+1; step l (index l-1) at planes p-l, p-l+1 and the
-  // one evaluated in this iteration
-  R xp[RPT], xc[RPT], xn[RPT];
-  R sb[K - 1][RPT], sc[K - 1][RPT], sn[K - 1][RPT];
-  const int pfirst = z0 - K + 1, plast = z1 + K - 2;
-  // this thread's column lies in the output tile (rows are checked per cell)
-  const bool tile_col = tx >= H && tx < SX - H;
-#pragma unroll
-  for (int q = 0; q < RPT; ++q) {
-    const int j = j0 - H + row(q);
-    xp[q] = ld(pfirst - 1, j, ic);
-    xc[q] = ld(pfirst, j, ic);
-#pragma unroll
-    for (int l = 0; l < K - 1; ++l) sb[l][q] = sc[l][q] = R(0);
-  }
-  R hv = hly >= 0 ? ld(pfirst, hj, hi) : R(0);
-  for (int p = pfirst; p <= plast; ++p) {
-    // the next plane's cells are requested before this plane is computed
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) xn[q] = ld(p + 1, j0 - H + row(q), ic);
-    const R hvn = hly >= 0 ? ld(p + 1, hj, hi) : R(0);
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) xt[row(q) + 1][tx + 1] = xc[q];
-    if (hly >= 0) xt[hly][hlx] = hv;
-    __syncthreads();
-    {  // step 1 at plane p, on every cell of the region
-      const bool pin = p >= 0 && p < nz;
-#pragma unroll
-      for (int q = 0; q < RPT; ++q) {
-        const int r = row(q);
-        const bool cin = pin && inxy(j0 - H + r, ic);
-        sn[0][q] = cin ? allencahn_point(xc[q], xt[r + 1][tx], xt[r + 1][tx + 2], xt[r][tx + 1],
-                                         xt[r + 2][tx + 1], xp[q], xn[q], D, C)
-                       : R(0);
-        if constexpr (ST) {
-          if (cin && tile_col && r >= H && r < SY - H && p >= z0 && p < z1)
-            put<false>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
-        }
-      }
-    }
-#pragma unroll
-    for (int l = 2; l <= K; ++l) {  // step l at plane p - l + 1
-      const int pl = p - l + 1;
-      const bool pin = pl >= 0 && pl < nz;
-      const bool xin = tx >= l - 1 && tx <= SX - l;
-#pragma unroll
-      for (int q = 0; q < RPT; ++q) {
-        const int r = row(q);
-        const int j = j0 - H + r;
-        const bool ok = pin && xin && r >= l - 1 && r <= SY - l && inxy(j, ic);
-        const R(*t)[SX] = yt[l - 2];
-        const R v = ok ? allencahn_point(sc[l - 2][q], t[r][tx - 1], t[r][tx + 1], t[r - 1][tx],
-                                         t[r + 1][tx], sb[l - 2][q], sn[l - 2][q], D, C)
-                       : R(0);
-        if (l < K) {
-          sn[l - 1][q] = v;
-          if constexpr (ST) {
-            if (ok && tile_col && r >= H && r < SY - H && pl >= z0 && pl < z1)
-              put<false>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
-          }
-        } else if (ok && pl >= z0 && pl < z1) {
-          put<NT>(&y[pl * plane + j * nx + ic], v);
-        }
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int l = 0; l < K - 1; ++l)
-#pragma unroll
-      for (int q = 0; q < RPT; ++q) yt[l][row(q)][tx] = sn[l][q];
-#pragma unroll
-    for (int q = 0; q < RPT; ++q) {
-      xp[q] = xc[q];
-      xc[q] = xn[q];
-#pragma unroll
-      for (int l = 0; l < K - 1; ++l) {
-        sb[l][q] = sc[l][q];
-        sc[l][q] = sn[l][q];
-      }
-    }
-    hv = hvn;
-  }
-}
-
-// Adjoint: dx'[m]/dx[m] = (1 - 6D) - 3C x[m]^2 (the nonlinear term's adjoint,
-// fused), dx'[c]/dx[m] = D for each in-grid face neighbour c of m. The
-// Laplacian with zero ghosts is symmetric, so the gather reads g at m's own
-// neighbours:  g'[m] = (k0 - k1*x[m]^2) * g[m] + D * sum_nbr g.
-// DP: also this step's share of dL/dD and dL/dC (see DpOut), from x_{t-1}
-// staged the same way as g (its plane in LDS, the planes below and above in
-// registers).
-template <class R, bool DP, bool NT>
-__global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict__ x,
-                                                             const R* __restrict__ g,
-                                                             R* __restrict__ gp, int nx, int ny,
-                                                             int nz, int tiles_x, int tiles_y,
-                                                             int ntiles, R D, R k0, R k1,
-                                                             DpOut dp) {
-  __shared__ R tile[kAcTY + 2][kAcTX + 2];
-  __shared__ R tilex[DP ? kAcTY + 2 : 1][DP ? kAcTX + 2 : 1];
-  AcTile t;
-  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;  // the whole block
-  const int plane = nx * ny;
-  auto ld = [&](const R* a, int k, int j, int i) -> R {
-    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? a[k * plane + j * nx + i]
-                                                                      : R(0);
-  };
-  // without the constants' gradients x is read once per point (streamed)
-  auto ldnt = [&](const R* a, int k, int j, int i) -> R {
-    return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx)
-               ? take<NT>(&a[k * plane + j * nx + i])
-               : R(0);
-  };
-  auto ldg = [&](int k, int j, int i) -> R { return ld(g, k, j, i); };
-  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
-  int hly, hlx;
-  ac_halo_cell(tid, &hly, &hlx);
-  const int hj = t.by * kAcTY + hly - 1, hi = t.bx * kAcTX + hlx - 1;
-  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
-  // Every value a plane needs (g and x at the thread's cells, the halo cell)
-  // is requested one plane ahead, before the current plane is computed.
-  R belowA = ldg(t.z0 - 1, t.ja, t.i), belowB = ldg(t.z0 - 1, t.jb, t.i);
-  R curA = ldg(t.z0, t.ja, t.i), curB = ldg(t.z0, t.jb, t.i);
-  R halo = hly >= 0 ? ldg(t.z0, hj, hi) : R(0);
-  R xbelowA = R(0), xbelowB = R(0);
-  R xcurA = ld(x, t.z0, t.ja, t.i), xcurB = ld(x, t.z0, t.jb, t.i);
-  R xhalo = R(0);
-  if (DP) {
-    xbelowA = ld(x, t.z0 - 1, t.ja, t.i);
-    xbelowB = ld(x, t.z0 - 1, t.jb, t.i);
-    xhalo = hly >= 0 ? ld(x, t.z0, hj, hi) : R(0);
-  }
-  double a0 = 0.0, a1 = 0.0;
-  for (int k = t.z0; k < t.z1; ++k) {
-    const R aboveA = ldg(k + 1, t.ja, t.i), aboveB = ldg(k + 1, t.jb, t.i);
-    const R haloN = hly >= 0 ? ldg(k + 1, hj, hi) : R(0);
-    const R xaboveA = DP ? ld(x, k + 1, t.ja, t.i) : ldnt(x, k + 1, t.ja, t.i);
-    const R xaboveB = DP ? ld(x, k + 1, t.jb, t.i) : ldnt(x, k + 1, t.jb, t.i);
-    const R xhaloN = DP && hly >= 0 ? ld(x, k + 1, hj, hi) : R(0);
-    const R xa = xcurA, xb = xcurB;
-    __syncthreads();
-    tile[ty + 1][tx + 1] = curA;
-    tile[ty + 5][tx + 1] = curB;
-    if (hly >= 0) tile[hly][hlx] = halo;
-    if (DP) {
-      tilex[ty + 1][tx + 1] = xcurA;
-      tilex[ty + 5][tx + 1] = xcurB;
-      if (hly >= 0) tilex[hly][hlx] = xhalo;
-    }
-    __syncthreads();
-    // lap of x at row r of this thread (r = 1: A, r = 5: B), the forward's order
-    auto lapx = [&](int r, R xzm, R xzp, R a) {
-      R lap = tilex[ty + r][tx] + tilex[ty + r][tx + 2];
-      lap += tilex[ty + r - 1][tx + 1];
-      lap += tilex[ty + r + 1][tx + 1];
-      lap += xzm;
-      lap += xzp;
-      return lap - R(6) * a;
-    };
-    if (va) {
-      R s = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
-      s += tile[ty][tx + 1];
-      s += tile[ty + 2][tx + 1];
-      s += belowA;
-      s += aboveA;
-      put<NT>(&gp[k * plane + t.ja * nx + t.i], (k0 - k1 * (xa * xa)) * curA + D * s);
-      if (DP) {
-        a0 += (double)curA * (double)lapx(1, xbelowA, xaboveA, xa);
-        a1 += (double)curA * (double)(-((xa * xa) * xa));
-      }
-    }
-    if (vb) {
-      R s = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
-      s += tile[ty + 4][tx + 1];
-      s += tile[ty + 6][tx + 1];
-      s += belowB;
-      s += aboveB;
-      put<NT>(&gp[k * plane + t.jb * nx + t.i], (k0 - k1 * (xb * xb)) * curB + D * s);
-      if (DP) {
-        a0 += (double)curB * (double)lapx(5, xbelowB, xaboveB, xb);
-        a1 += (double)curB * (double)(-((xb * xb) * xb));
-      }
-    }
-    belowA = curA;
-    belowB = curB;
-    curA = aboveA;
-    curB = aboveB;
-    halo = haloN;
-    xbelowA = xcurA;
-    xbelowB = xcurB;
-    xcurA = xaboveA;
-    xcurB = xaboveB;
-    xhalo = xhaloN;
-  }
-  if (DP) {
-    __syncthreads();
-    dp_commit(dp, t.b, a0, a1);
-  }
-}
-
-// The limiter's adjoint, g'[m] = (k0 - k1*x[m]^2) * gm[m] + D * sum_nbr gm,
-// with gm = g where the step's unlimited value (re-evaluated from x =
-// x_{t-1} with the forward's expression) lies in [lo, hi] and 0 elsewhere.
-// The masked plane k+1 is formed in iteration k: x(k+1) is staged in LDS
-// with a two-cell ring (the masks of g's one-cell ring need their own xy
-// neighbours), x(k) and x(k+2) at the thread's cells and ring cell stay in
-// registers, so every mask is evaluated from on-chip values and x is read
-// from HBM about once per point.
-template <class R, bool NT>
-__global__ __launch_bounds__(kThreads) void adj_allencahn3d7_lim(const R* __restrict__ x,
-                                                                 const R* __restrict__ g,
-                                                                 R* __restrict__ gp, int nx,
-                                                                 int ny, int nz, int tiles_x,
-                                                                 int tiles_y, int ntiles, R D,
-                                                                 R k0, R k1, R C, Limit<R> lim) {
-  constexpr int LY = kAcTY + 2, LX = kAcTX + 2;          // g: one-cell ring
-  constexpr int XY = kAcTY + 4, XX = kAcTX + 4;          // x: two-cell ring
-  __shared__ R tile[LY][LX];
-  __shared__ R xt[XY][XX];
-  AcTile t;
-  if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;  // the whole block
-  const int plane = nx * ny;
-  auto in = [&](int k, int j, int i) {
-    return k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx;
-  };
-  auto ld = [&](const R* a, int k, int j, int i) -> R {
-    return in(k, j, i) ? a[k * plane + j * nx + i] : R(0);
-  };
-  auto keep = [&](R y) { return !(y < lim.lo || y > lim.hi); };
-  // g at a cell masked from global memory (the first planes only)
-  auto ldg = [&](int k, int j, int i) -> R {
-    if (!in(k, j, i)) return R(0);
-    const int q = k * plane + j * nx + i;
-    const R y = allencahn_point(x[q], i > 0 ? x[q - 1] : R(0), i < nx - 1 ? x[q + 1] : R(0),
-                                j > 0 ? x[q - nx] : R(0), j < ny - 1 ? x[q + nx] : R(0),
-                                k > 0 ? x[q - plane] : R(0), k < nz - 1 ? x[q + plane] : R(0),
-                                D, C);
-    return keep(y) ? g[q] : R(0);
-  };
-  const int tx = threadIdx.x, ty = threadIdx.y, tid = ty * kBX + tx;
-  const int i0 = t.bx * kAcTX, j0 = t.by * kAcTY;
-  // this thread's cell of g's ring (tile coordinates hly-1, hlx-1), if any
-  int hly, hlx;
-  ac_halo_cell(tid, &hly, &hlx);
-  const bool hr = hly >= 0;
-  const int hj = j0 + hly - 1, hi = i0 + hlx - 1;
-  // this thread's cell of x's outer ring, or one of the four corners of
-  // g's ring (which g's ring cells need as x neighbours), in x-tile
-  // coordinates, if any: 2*68 + 2*10 + 4 = 160 cells
-  int oy = -1, ox = 0;
-  if (tid < XX) {
-    oy = 0;
-    ox = tid;
-  } else if (tid < 2 * XX) {
-    oy = XY - 1;
-    ox = tid - XX;
-  } else if (tid < 2 * XX + LY) {
-    oy = tid - 2 * XX + 1;
-    ox = 0;
-  } else if (tid < 2 * XX + 2 * LY) {
-    oy = tid - 2 * XX - LY + 1;
-    ox = XX - 1;
-  } else if (tid < 2 * XX + 2 * LY + 4) {
-    const int c = tid - 2 * XX - 2 * LY;
-    oy = (c & 2) ? XY - 2 : 1;
-    ox = (c & 1) ? XX - 2 : 1;
-  }
-  const bool orr = oy >= 0;
-  const int oj = j0 + oy - 2, oi = i0 + ox - 2;
-  const bool va = t.i < nx && t.ja < ny, vb = t.i < nx && t.jb < ny;
-  // masked g: planes k-1, k at the thread's cells, plane k at its ring cell
-  R belowA = ldg(t.z0 - 1, t.ja, t.i), belowB = ldg(t.z0 - 1, t.jb, t.i);
-  R curA = ldg(t.z0, t.ja, t.i), curB = ldg(t.z0, t.jb, t.i);
-  R halo = hr ? ldg(t.z0, hj, hi) : R(0);
-  // x at planes k, k+1 (the thread's cells and ring cell), outer ring at k+1
-  R xA0 = ld(x, t.z0, t.ja, t.i), xB0 = ld(x, t.z0, t.jb, t.i);
-  R xA1 = ld(x, t.z0 + 1, t.ja, t.i), xB1 = ld(x, t.z0 + 1, t.jb, t.i);
-  R xr0 = hr ? ld(x, t.z0, hj, hi) : R(0), xr1 = hr ? ld(x, t.z0 + 1, hj, hi) : R(0);
-  R xo1 = orr ? ld(x, t.z0 + 1, oj, oi) : R(0);
-  for (int k = t.z0; k < t.z1; ++k) {
-    // plane k+1's g, plane k+2's x and the outer ring of plane k+2 (for the
-    // next iteration) are requested before this plane is computed
-    const R gA = ld(g, k + 1, t.ja, t.i), gB = ld(g, k + 1, t.jb, t.i);
-    const R gr = hr ? ld(g, k + 1, hj, hi) : R(0);
-    const R xA2 = ld(x, k + 2, t.ja, t.i), xB2 = ld(x, k + 2, t.jb, t.i);
-    const R xr2 = hr ? ld(x, k + 2, hj, hi) : R(0);
-    const R xo2 = orr ? ld(x, k + 2, oj, oi) : R(0);
-    __syncthreads();
-    tile[ty + 1][tx + 1] = curA;
-    tile[ty + 5][tx + 1] = curB;
-    if (hr) tile[hly][hlx] = halo;
-    xt[ty + 2][tx + 2] = xA1;
-    xt[ty + 6][tx + 2] = xB1;
-    if (hr) xt[hly + 1][hlx + 1] = xr1;
-    if (orr) xt[oy][ox] = xo1;
-    __syncthreads();
-    // the masks of plane k+1 (x-tile position r, c; x(k) and x(k+2) there)
-    auto masked = [&](int r, int c, R xb, R xa, R gv) {
-      const R y = allencahn_point(xt[r][c], xt[r][c - 1], xt[r][c + 1], xt[r - 1][c],
-                                  xt[r + 1][c], xb, xa, D, C);
-      return keep(y) ? gv : R(0);
-    };
-    const R aboveA = masked(ty + 2, tx + 2, xA0, xA2, gA);
-    const R aboveB = masked(ty + 6, tx + 2, xB0, xB2, gB);
-    const R halon = hr ? masked(hly + 1, hlx + 1, xr0, xr2, gr) : R(0);
-    if (va) {
-      R s = tile[ty + 1][tx] + tile[ty + 1][tx + 2];
-      s += tile[ty][tx + 1];
-      s += tile[ty + 2][tx + 1];
-      s += belowA;
-      s += aboveA;
-      put<NT>(&gp[k * plane + t.ja * nx + t.i], (k0 - k1 * (xA0 * xA0)) * curA + D * s);
-    }
-    if (vb) {
-      R s = tile[ty + 5][tx] + tile[ty + 5][tx + 2];
-      s += tile[ty + 4][tx + 1];
-      s += tile[ty + 6][tx + 1];
-      s += belowB;
-      s += aboveB;
-      put<NT>(&gp[k * plane + t.jb * nx + t.i], (k0 - k1 * (xB0 * xB0)) * curB + D * s);
-    }
-    belowA = curA;
-    belowB = curB;
-    curA = aboveA;
-    curB = aboveB;
-    halo = halon;
-    xA0 = xA1;
-    xB0 = xB1;
-    xA1 = xA2;
-    xB1 = xB2;
-    xr0 = xr1;
-    xr1 = xr2;
-    xo1 = xo2;
-  }
 }
 
 // ------------------------------------------ variable-coefficient diffusion 2-D
@@ -1383,47 +756,6 @@ inline int streams(const StepShape& s) {
   return bytes >= kStreamBytes ? 1 : 0;
 }
 
-// mids (nullable): the intermediate states' buffers, step l's at mids[l-1].
-template <class R, int K, int RPT, int NZ>
-hipError_t ac_forward_n(const StepShape& s, const R* x, R* y, R* const* mids, hipStream_t st) {
-  using A = AcN<K, RPT, NZ>;
-  const int tx = cdiv(s.nx, A::OX), ty = cdiv(s.ny, A::OY);
-  const int nt = tx * ty * cdiv(s.nz, A::ZC);
-  const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
-  R* m0 = mids ? mids[0] : nullptr;
-  R* m1 = (mids && K >= 3) ? mids[1] : nullptr;
-  const bool str = streams(s) != 0;
-  if (mids && str)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, true, true><<<grid, block, 0, st>>>(
-        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
-  else if (mids)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, false, true><<<grid, block, 0, st>>>(
-        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
-  else if (str)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, true, false><<<grid, block, 0, st>>>(
-        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
-  else
-    fwd_allencahn3d7_n<R, K, RPT, NZ, false, false><<<grid, block, 0, st>>>(
-        x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
-  return hipGetLastError();
-}
-
-// Allen-Cahn, n fused forward steps (2 <= n <= kAcMaxFuse); mids as above.
-template <class R>
-hipError_t ac_forward_steps(const StepShape& s, const void* xv, void* yv, void* const* mids,
-                            int32_t n, hipStream_t st) {
-  const R* x = static_cast<const R*>(xv);
-  R* y = static_cast<R*>(yv);
-  R* const* m = reinterpret_cast<R* const*>(mids);
-  switch (n) {
-    case 2:
-      return ac_forward_n<R, 2, 4, 32>(s, x, y, m, st);
-    case 3:
-      return ac_forward_n<R, 3, 4, 64>(s, x, y, m, st);
-  }
-  return hipErrorInvalidValue;
-}
-
 template <class R>
 hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* yv, bool two,
                      hipStream_t st, void* midv = nullptr) {
@@ -1450,29 +782,9 @@ hipError_t forward_t(const StepShape& s, const void* xv, const void* Kv, void* y
       }
       break;
     }
-    case ADST_ALLENCAHN3D7: {
-      if (two) {
-        return ac_forward_n<R, 2, 4, 32>(s, x, y, nullptr, st);
-      } else {
-        const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
-        const int nt = tx * ty * cdiv(s.nz, kAcZC);
-        const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
-        const bool str = streams(s) != 0;
-        if (s.limit && str)
-          fwd_allencahn3d7<R, true, true><<<grid, block, 0, st>>>(
-              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
-        else if (s.limit)
-          fwd_allencahn3d7<R, true, false><<<grid, block, 0, st>>>(
-              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
-        else if (str)
-          fwd_allencahn3d7<R, false, true><<<grid, block, 0, st>>>(
-              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
-        else
-          fwd_allencahn3d7<R, false, false><<<grid, block, 0, st>>>(
-              x, y, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1), lim);
-      }
-      break;
-    }
+    case ADST_ALLENCAHN3D7:
+      return two ? ac_launch_forward_steps(s, x, y, nullptr, 2, st)
+                 : ac_launch_forward(s, x, y, st);
     case ADST_VARDIFF2D9: {
       const bool str = streams(s) != 0;
       const int vec = vec_ok<R>(s.nx, x, K);
@@ -1556,36 +868,8 @@ hipError_t adjoint_t(const StepShape& s, const void* xv, const void* Kv, const v
           g, gp, s.nx, s.ny, tx, nt, vec_ok<R>(s.nx, g), R(s.p0));
       break;
     }
-    case ADST_ALLENCAHN3D7: {
-      const R D = R(s.p0), C = R(s.p1);
-      const R k0 = R(1) + D * R(-6), k1 = R(3) * C;
-      const int tx = cdiv(s.nx, kAcTX), ty = cdiv(s.ny, kAcTY);
-      const int nt = tx * ty * cdiv(s.nz, kAcZC);
-      const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
-      const bool str = streams(s) != 0, lm = adjoint_applies_limit(s, dp_part != nullptr);
-      const Limit<R> lim{R(s.lo), R(s.hi)};
-#define ADST_AC_ADJ(DPV, NTV)                                                        \
-  adj_allencahn3d7<R, DPV, NTV><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, \
-                                                         D, k0, k1, dp)
-#define ADST_AC_LIM(NTV)                                                             \
-  adj_allencahn3d7_lim<R, NTV><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, \
-                                                        D, k0, k1, C, lim)
-      if (dp_part && str)
-        ADST_AC_ADJ(true, true);
-      else if (dp_part)
-        ADST_AC_ADJ(true, false);
-      else if (lm && str)
-        ADST_AC_LIM(true);
-      else if (lm)
-        ADST_AC_LIM(false);
-      else if (str)
-        ADST_AC_ADJ(false, true);
-      else
-        ADST_AC_ADJ(false, false);
-#undef ADST_AC_ADJ
-#undef ADST_AC_LIM
-      break;
-    }
+    case ADST_ALLENCAHN3D7:
+      return ac_launch_adjoint(s, x, g, gp, dp_part, dp_first, st);
     case ADST_VARDIFF2D9: {
       const int tx = cdiv(s.nx, kVdTW);
       const R dt = R(s.p0), ca = R(1) / R(3), cd = R(1) / R(12);
@@ -1673,9 +957,7 @@ int32_t max_stored_forward(int32_t kind) {
 hipError_t launch_forward_store(const StepShape& s, const void* x, const void* K, void* const* ys,
                                 int32_t n, hipStream_t stream) {
   if (n < 2 || n > max_stored_forward(s.kind) || s.limit) return hipErrorInvalidValue;
-  if (s.kind == ADST_ALLENCAHN3D7)
-    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, ys[n - 1], ys, n, stream)
-                               : ac_forward_steps<float>(s, x, ys[n - 1], ys, n, stream);
+  if (s.kind == ADST_ALLENCAHN3D7) return ac_launch_forward_steps(s, x, ys[n - 1], ys, n, stream);
   return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, ys[1], true, stream, ys[0])
                              : forward_t<float>(s, x, K, ys[1], true, stream, ys[0]);
 }
@@ -1701,9 +983,7 @@ int32_t max_fused_adjoint(int32_t kind, int64_t nx) {
 hipError_t launch_forward_n(const StepShape& s, const void* x, const void* K, void* y, int32_t n,
                             hipStream_t stream) {
   if (n < 2 || n > max_fused_forward(s.kind)) return hipErrorInvalidValue;
-  if (s.kind == ADST_ALLENCAHN3D7)
-    return s.dtype == ADST_F64 ? ac_forward_steps<double>(s, x, y, nullptr, n, stream)
-                               : ac_forward_steps<float>(s, x, y, nullptr, n, stream);
+  if (s.kind == ADST_ALLENCAHN3D7) return ac_launch_forward_steps(s, x, y, nullptr, n, stream);
   if (n == 2)
     return s.dtype == ADST_F64 ? forward_t<double>(s, x, K, y, true, stream)
                                : forward_t<float>(s, x, K, y, true, stream);
@@ -1786,8 +1066,7 @@ hipError_t launch_limit_mask(const StepShape& s, const void* x, const void* K, v
 int64_t dparam_slots(const StepShape& s) {
   switch (s.kind) {
     case ADST_JACOBI2D5: return jacobi_x_adjoint_slots(s);
-    case ADST_ALLENCAHN3D7:
-      return int64_t(cdiv(s.nx, kAcTX)) * cdiv(s.ny, kAcTY) * cdiv(s.nz, kAcZC);
+    case ADST_ALLENCAHN3D7: return ac_dparam_slots(s);
     case ADST_VARDIFF2D9: return int64_t(cdiv(s.nx, kVdTW)) * cdiv(s.ny, kVdAdjTR);
     default: return 0;
   }

@@ -1,10 +1,10 @@
 """Temporal blocking of the Allen-Cahn kind, up to three forward steps per
 launch, against one launch per step and against the oracle (needs an MI355X).
 
-A launch of n steps has each 64 x 4-thread workgroup evaluate the n steps on
-a 64 x 16 region of each plane while marching in z (32 output planes for
-n = 2, 64 for n = 3); the output tile is the region less n - 1 cells on
-each side (62 x 14, 60 x 12). The shapes put grids narrower than one tile,
+A launch of n steps has each workgroup (64 lanes by four waves of four
+rows) evaluate the n steps on a 64 x 16 region of each plane while marching
+in z over 64-plane chunks; the output tile is the region less n - 1 cells
+on each side (62 x 14, 60 x 12). The shapes put grids narrower than one tile,
 exact tiles, tiles plus one and ragged tails against these sizes in every
 axis, and runs of 1 to 3 planes. Step counts cover one launch of each depth
 and runs that split into full launches and a shorter remainder.

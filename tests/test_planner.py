@@ -188,6 +188,32 @@ def test_budget_counts_whole_slots_only():
     assert adst.adst_plan(p, 50, 3 * S, adst.ADST_SCHED_BINOMIAL).slots == 3
 
 
+def fused_forward_adjoint_pairs(acts, indices=False):
+    """Forward steps the library runs inside the next adjoint launch: a
+    single step whose output is the next adjoint step's x_{t-1} and that no
+    later action reads before it is written again (their count, or their
+    indices)."""
+    FWD, ADJ, SEED = adst.ADST_OP_FWD, adst.ADST_OP_ADJ, adst.ADST_OP_SEED
+    reads_ops = (FWD, adst.ADST_OP_FWD2, adst.ADST_OP_FWDW, ADJ, SEED)
+    writes_ops = (FWD, adst.ADST_OP_FWD2, adst.ADST_OP_FWDW)
+    found = []
+    for i in range(len(acts) - 1):
+        f, g = acts[i], acts[i + 1]
+        if not (f[0] == FWD and f[4] == 1 and g[0] == ADJ and g[2] == f[3] and g[1] == f[1] + 1
+                and f[3] != f[2]):
+            continue
+        ok = True
+        for a in acts[i + 2:]:
+            if a[0] in reads_ops and a[2] == f[3]:
+                ok = False
+                break
+            if a[0] in writes_ops and a[3] == f[3]:
+                break
+        if ok:
+            found.append(i)
+    return found if indices else len(found)
+
+
 def test_workspace_and_bytes():
     p = prob(dims=(100, 30, 7))
     S = 100 * 30 * 7 * 8
@@ -198,11 +224,21 @@ def test_workspace_and_bytes():
     assert info.fwd_workspace_bytes == S
     # Allen-Cahn: 8 B per point per forward launch read and 8 per state it
     # writes (a fused run writes one, a store-through run each of its
-    # states), 24 per adjoint, 16 for the seed
+    # states), 24 per adjoint, 16 for the seed; a recomputed step whose
+    # state only the next adjoint step reads runs inside that adjoint launch
+    # and moves nothing of its own
     n = 100 * 30 * 7
-    assert info.fwd_kernels < info.fwd_launches
-    assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels + 8 * info.fwd_launches)
+    acts = adst.adst_plan_actions(p, 12, 4 * S, adst.ADST_SCHED_BINOMIAL)
+    fused = fused_forward_adjoint_pairs(acts)
+    assert fused > 0
+    assert info.fwd_kernels < info.fwd_launches - fused
+    assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels + 8 * (info.fwd_launches - fused))
     assert info.alg_bytes == info.fwd_alg_bytes + n * (24 * 12 + 16)
+    # without fusion every forward action moves its own bytes
+    pn = prob(dims=(100, 30, 7), flags=adst.ADST_NO_FUSE)
+    info = adst.adst_plan(pn, 12, 4 * S, adst.ADST_SCHED_BINOMIAL)
+    assert info.fwd_kernels == info.fwd_launches == info.fwd_steps_total
+    assert info.fwd_alg_bytes == n * 16 * info.fwd_steps_total
     assert adst.adst_plan(p, 0, 0, 0).workspace_bytes == 16384
 
 
@@ -236,9 +272,13 @@ def test_store_through_runs_counted_like_the_executor():
     for T, slots in ((8, 3), (13, 4), (23, 5), (40, 6)):
         acts = adst.adst_plan_actions(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
         info = adst.adst_plan(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
+        fused = set(fused_forward_adjoint_pairs(acts, indices=True))
         kernels, i = 0, 0
         while i < len(acts):
             a = acts[i]
+            if i in fused:  # runs inside the next adjoint launch
+                i += 1
+                continue
             if a[0] in (adst.ADST_OP_FWD, adst.ADST_OP_FWD2):
                 kernels += 1
             r = 1
@@ -246,6 +286,8 @@ def test_store_through_runs_counted_like_the_executor():
                 while r < 3 and i + r < len(acts):
                     b, prev = acts[i + r], acts[i + r - 1]
                     if b[0] != adst.ADST_OP_FWD or b[2] != prev[3] or b[1] != prev[1] + 1:
+                        break
+                    if i + r in fused:
                         break
                     if b[3] == a[2] or any(acts[i + k][3] == b[3] for k in range(r)):
                         break
