@@ -112,10 +112,10 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   return ADST_OK;
 }
 
-// A forward step whose result only the next action, the adjoint step that
-// reads it as x_{t-1}, uses: the two run as one launch (ac_launch_forward_
-// adjoint), x_{t-1} formed on chip and never written. True when acts[i] is
-// that forward step: the kind's adjoint reads x_{t-1} only pointwise
+// A forward action (one step, or a fused run of up to three) whose result
+// only the next action, the adjoint step that reads it as x_{t-1}, uses: the
+// two run as one launch (ac_launch_forward_adjoint), x_{t-1} formed on chip
+// and never written. True when acts[i] is that forward action: the kind's adjoint reads x_{t-1} only pointwise
 // (Allen-Cahn without the limiter or the constants' gradients), and no later
 // action reads the buffer before it is written again.
 bool fused_fwd_adj(const Checked& c, const std::vector<adst_action>& acts, size_t i) {
@@ -124,8 +124,9 @@ bool fused_fwd_adj(const Checked& c, const std::vector<adst_action>& acts, size_
   if (i + 1 >= acts.size()) return false;
   const adst_action& f = acts[i];
   const adst_action& g = acts[i + 1];
-  if (f.op != ADST_OP_FWD || f.n != 1 || g.op != ADST_OP_ADJ || g.src != f.dst ||
-      g.t != f.t + 1 || f.dst == f.src)
+  const bool fwd = (f.op == ADST_OP_FWD && f.n == 1) ||
+                   (f.op == ADST_OP_FWD2 && f.n >= 2 && f.n <= kAcMaxFuse);
+  if (!fwd || g.op != ADST_OP_ADJ || g.src != f.dst || g.t != f.t + 1 || f.dst == f.src)
     return false;
   for (size_t k = i + 2; k < acts.size(); ++k) {
     const adst_action& a = acts[k];
@@ -315,6 +316,7 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
         break;
       }
       case ADST_OP_FWD2:
+        if (fused_fwd_adj(c, plan.acts, i)) break;  // moves the adjoint's bytes only
         fwd_per_point += fb;
         break;
       case ADST_OP_FWDW:
@@ -624,6 +626,18 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
     if (r == hipSuccess) r = tr.end(stream);
     return r;
   };
+  // a recomputed forward action and the adjoint step after it, in one launch
+  auto fused_launch = [&](const adst_action& f) -> hipError_t {
+    const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
+    const hipError_t r = traced(Tracer::ADJ, "ac_march<fwd" + std::to_string(f.n) + "+adj>",
+                                bytes, [&] {
+                                  return ac_launch_forward_adjoint(c.shape, buffer(f.src), gcur,
+                                                                   gnext, f.n, stream);
+                                });
+    std::swap(gcur, gnext);
+    first_adj = false;
+    return r;
+  };
   for (size_t ai = 0; ai < plan.acts.size(); ++ai) {
     const adst_action& a = plan.acts[ai];
     const bool fwd_op = a.op == ADST_OP_FWD || a.op == ADST_OP_FWD2 || a.op == ADST_OP_FWDW;
@@ -647,13 +661,7 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
     switch (a.op) {
       case ADST_OP_FWD: {
         if (fused_fwd_adj(c, plan.acts, ai)) {
-          // this recomputed step and the adjoint step after it in one launch
-          const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
-          e = traced(Tracer::ADJ, "ac_march<fwd1+adj>", bytes, [&] {
-            return ac_launch_forward_adjoint(c.shape, buffer(a.src), gcur, gnext, stream);
-          });
-          std::swap(gcur, gnext);
-          first_adj = false;
+          e = fused_launch(a);
           ++ai;
           break;
         }
@@ -674,6 +682,11 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
         break;
       }
       case ADST_OP_FWD2:
+        if (fused_fwd_adj(c, plan.acts, ai)) {
+          e = fused_launch(a);
+          ++ai;
+          break;
+        }
         e = traced(cat, kernel_label(c, a, 1, false), npts * double(pp.fwd), [&] {
           return launch_forward_n(c.shape, buffer(a.src), coeff, buffer(a.dst), a.n, stream);
         });

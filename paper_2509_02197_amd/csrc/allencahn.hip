@@ -1096,16 +1096,26 @@ hipError_t ac_launch_adjoint(const StepShape& s, const void* x, const void* g, v
                                static_cast<float*>(gp), dp_part, dp_first, st);
 }
 
+template <class R>
+hipError_t forward_adjoint(const StepShape& s, const R* x, const R* g, R* gp, int32_t n,
+                           hipStream_t st) {
+  switch (n) {
+    case 1: return march<R, 1, true, false>(s, x, g, gp, nullptr, nullptr, st);
+    case 2: return march<R, 2, true, false>(s, x, g, gp, nullptr, nullptr, st);
+    case 3: return march<R, 3, true, false>(s, x, g, gp, nullptr, nullptr, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 hipError_t ac_launch_forward_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
-                                     hipStream_t st) {
+                                     int32_t n, hipStream_t st) {
   if (s.limit || !march_fits(s)) return hipErrorInvalidValue;
   return s.dtype == ADST_F64
-             ? march<double, 1, true, false>(s, static_cast<const double*>(x),
-                                             static_cast<const double*>(g),
-                                             static_cast<double*>(gp), nullptr, nullptr, st)
-             : march<float, 1, true, false>(s, static_cast<const float*>(x),
-                                            static_cast<const float*>(g), static_cast<float*>(gp),
-                                            nullptr, nullptr, st);
+             ? forward_adjoint<double>(s, static_cast<const double*>(x),
+                                       static_cast<const double*>(g), static_cast<double*>(gp), n,
+                                       st)
+             : forward_adjoint<float>(s, static_cast<const float*>(x),
+                                      static_cast<const float*>(g), static_cast<float*>(gp), n, st);
 }
 
 bool ac_fuses_forward_adjoint(const StepShape& s) { return !s.limit && march_fits(s); }

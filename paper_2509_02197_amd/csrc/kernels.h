@@ -32,12 +32,13 @@ hipError_t ac_launch_forward_steps(const StepShape& s, const void* x, void* y, v
 hipError_t ac_launch_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
                              double* dp_part, bool dp_first, hipStream_t st);
 int64_t ac_dparam_slots(const StepShape& s);
-// One recomputed forward step and the adjoint step that reads its result, in
-// one launch: g_prev = J_t^T g_next with x_{t-1} = F(x) formed on chip and
-// never stored (x = x_{t-2}); no limiter and no constants' gradients.
-// ac_fuses_forward_adjoint tells whether the shape takes it.
+// n = 1 .. kAcMaxFuse recomputed forward steps and the adjoint step that
+// reads their result, in one launch: g_prev = J_t^T g_next with x_{t-1} =
+// F^n(x) formed on chip and never stored (x = x_{t-1-n}); no limiter and no
+// constants' gradients. ac_fuses_forward_adjoint tells whether the shape
+// takes it.
 hipError_t ac_launch_forward_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
-                                     hipStream_t st);
+                                     int32_t n, hipStream_t st);
 bool ac_fuses_forward_adjoint(const StepShape& s);
 
 // Temporal blocking: the most steps one launch may take (1 = none). The

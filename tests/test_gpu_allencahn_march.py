@@ -1,7 +1,7 @@
-"""The Allen-Cahn z-march kernels: a recomputed forward step run inside the
-adjoint launch that reads its result (x_{t-1} formed on chip, never
-stored), against one launch per step and against the oracle (needs an
-MI355X).
+"""The Allen-Cahn z-march kernels: recomputed forward steps (one, or a
+fused run of two or three) run inside the adjoint launch that reads their
+result (x_{t-1} formed on chip, never stored), against one launch per step
+and against the oracle (needs an MI355X).
 
 The single-step and plain adjoint launches own a 64 x 16 region of every
 plane (64 lanes by four waves of four rows) over 64-plane chunks; the fused
@@ -43,7 +43,7 @@ def _gpu():
 
 
 @pytest.mark.parametrize("dtype,shape", SHAPES)
-@pytest.mark.parametrize("T,slots", [(9, 2), (23, 3)])
+@pytest.mark.parametrize("T,slots", [(9, 2), (23, 3), (30, 2)])
 def test_forward_adjoint_launch(dtype, shape, T, slots):
     r = np.random.Generator(np.random.PCG64(44))
     inp = {"x0": r.uniform(-1.0, 1.0, shape).astype(NP_DTYPE[dtype]),
@@ -53,7 +53,12 @@ def test_forward_adjoint_launch(dtype, shape, T, slots):
     a = gpu_vjp(AC, inp, T, adst.ADST_LOSS_DOT_W, budget, adst.ADST_SCHED_BINOMIAL,
                 flags=adst.ADST_TRACE)
     names = {k["name"]: k["launches"] for k in adst.adst_trace_kernels()}
-    assert names.get("ac_march<fwd1+adj>", 0) > 0, names
+    fused = {n: names.get(f"ac_march<fwd{n}+adj>", 0) for n in (1, 2, 3)}
+    assert fused[1] > 0, names
+    if T >= 23:
+        assert fused[2] > 0, names  # fused runs of two steps before an adjoint step
+    if T >= 30:
+        assert fused[3] > 0, names
     assert a["info"]["adj_kernels"] == T
     b = gpu_vjp(AC, inp, T, adst.ADST_LOSS_DOT_W, budget, adst.ADST_SCHED_BINOMIAL,
                 flags=adst.ADST_NO_FUSE)
@@ -63,5 +68,5 @@ def test_forward_adjoint_launch(dtype, shape, T, slots):
                                aux=inp["aux"])
     assert np.array_equal(a["xT"], xT)
     e = rel(a["dx0"], dx0)
-    say(f"  dx0 rel L2 {e:.3e}; fused launches {names['ac_march<fwd1+adj>']}")
+    say(f"  dx0 rel L2 {e:.3e}; fused launches {fused}")
     assert e <= TOL[dtype]

@@ -189,18 +189,18 @@ def test_budget_counts_whole_slots_only():
 
 
 def fused_forward_adjoint_pairs(acts, indices=False):
-    """Forward steps the library runs inside the next adjoint launch: a
-    single step whose output is the next adjoint step's x_{t-1} and that no
-    later action reads before it is written again (their count, or their
-    indices)."""
+    """Forward actions the library runs inside the next adjoint launch: a
+    single step or a fused run of up to three whose output is the next
+    adjoint step's x_{t-1} and that no later action reads before it is
+    written again (their count, or their indices)."""
     FWD, ADJ, SEED = adst.ADST_OP_FWD, adst.ADST_OP_ADJ, adst.ADST_OP_SEED
     reads_ops = (FWD, adst.ADST_OP_FWD2, adst.ADST_OP_FWDW, ADJ, SEED)
     writes_ops = (FWD, adst.ADST_OP_FWD2, adst.ADST_OP_FWDW)
     found = []
     for i in range(len(acts) - 1):
         f, g = acts[i], acts[i + 1]
-        if not (f[0] == FWD and f[4] == 1 and g[0] == ADJ and g[2] == f[3] and g[1] == f[1] + 1
-                and f[3] != f[2]):
+        fwd = (f[0] == FWD and f[4] == 1) or (f[0] == adst.ADST_OP_FWD2 and 2 <= f[4] <= 3)
+        if not (fwd and g[0] == ADJ and g[2] == f[3] and g[1] == f[1] + 1 and f[3] != f[2]):
             continue
         ok = True
         for a in acts[i + 2:]:
