@@ -133,11 +133,21 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
 // planes) beat two (the launches of a recomputation run drop by a third);
 // four, with 24-row regions, needed 178 VGPRs and with 16-row regions
 // evaluated 7 points per output point, and both were slower.
+// Output tiles narrower than the region allows: non-temporal stores into a
+// 64-byte segment that two workgroups share were measured to cost a third
+// of a single step's time (3.26 -> 4.48 ms for a 1024^3 step whose tiles
+// were shifted by one column), so a fused launch's tile is a whole number of
+// 64-byte segments wide where that pays: two steps on 56-column tiles,
+// 4.93 -> 3.79 ms at 1024^3. Three steps keep 60 columns (56: no faster,
+// and more of the region evaluated for nothing).
+template <int K>
+constexpr int ac_out_width() { return K == 2 ? 56 : kBX - 2 * (K - 1); }
 template <int K, int RPT, int NZ>
 struct AcN {
   static constexpr int SX = kBX, SY = kBY * RPT;
-  static constexpr int OX = SX - 2 * (K - 1), OY = SY - 2 * (K - 1);  // output tile
-  static constexpr int ZC = NZ;                                     // output planes
+  static constexpr int OX = ac_out_width<K>(), OY = SY - 2 * (K - 1);  // output tile
+  static constexpr int ZC = NZ;                               // output planes
+  static_assert(OX + 2 * (K - 1) <= SX, "the output tile and its halo fit the region");
 };
 
 // ST: the intermediate states are stored too, step l's into mid[l-1], each
@@ -197,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
   R sb[K - 1][RPT], sc[K - 1][RPT], sn[K - 1][RPT];
   const int pfirst = z0 - K + 1, plast = z1 + K - 2;
   // this thread's column lies in the output tile (rows are checked per cell)
-  const bool tile_col = tx >= H && tx < SX - H;
+  const bool tile_col = tx >= H && tx < H + A::OX;
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
     const int j = j0 - H + row(q);
@@ -252,7 +262,7 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
             if (ok && tile_col && r >= H && r < SY - H && pl >= z0 && pl < z1)
               put<false>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
           }
-        } else if (ok && pl >= z0 && pl < z1) {
+        } else if (ok && tile_col && pl >= z0 && pl < z1) {
           put<NT>(&y[pl * plane + j * nx + ic], v);
         }
       }
@@ -570,7 +580,11 @@ template <int NF, int RR, int ZC>
 struct AcMarch {
   static constexpr int SX = kBX, SY = kMW * RR;
   static constexpr int H = NF > 1 ? NF - 1 : 0;  // cells per side the last level loses
-  static constexpr int OX = SX - 2 * H, OY = SY - 2 * H;
+  // output tile: 64 columns (aligned) for the plain adjoint; 56 (a whole
+  // number of 64-byte segments) with two forward levels (6.92 -> 6.84 ms
+  // at 1024^3); 60 with three (56 was slower: 8.09 -> 8.50 ms)
+  static constexpr int OX = H == 1 ? 56 : SX - 2 * H, OY = SY - 2 * H;
+  static_assert(OX + 2 * H <= SX, "the output tile and its halo fit the region");
 };
 
 template <class R>
@@ -725,8 +739,8 @@ __global__ __launch_bounds__(kBX * kMW) void ac_march(AcMarchArgs<R> a) {
     in[i] = cin && j >= 0 && j < ny;
     off[i] = in[i] ? uint32_t(j * nx + c) * sizeof(R) : kOob;
     offx[i] = (crin && j >= 0 && j < ny) ? uint32_t(j * nx + cr) * sizeof(R) : kOob;
-    // output tile: lanes H .. 63-H, region rows H .. SY-1-H
-    offo[i] = (in[i] && lane >= H && lane < kBX - H && r >= H && r < SY - H) ? off[i] : kOob;
+    // output tile: lanes H .. H+OX-1, region rows H .. SY-1-H
+    offo[i] = (in[i] && lane >= H && lane < H + M::OX && r >= H && r < SY - H) ? off[i] : kOob;
   }
   const uint32_t offy = jrin ? uint32_t(jr * nx + c) * sizeof(R) : kOob;
 
