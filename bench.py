@@ -463,10 +463,10 @@ def rocprof_label(name):
         return "jacobi_lim_adjoint<dp>" if t(2) else "jacobi_lim_adjoint"
     if base == "gs_wave":              # <R, ADJ, VEC>
         return "gs_wave<adj>" if t(1) else "gs_wave<fwd>"
-    if base == "ac_march":             # <R, NF, ADJ, RR, ZC, ST, NT>
+    if base == "ac_march":             # <R, NF, ADJ, RR, ZC, DA, ST, NT>
         if t(2):
             return "ac_march<adj>" if targs[1] == "0" else f"ac_march<fwd{targs[1]}+adj>"
-        return f"ac_march<fwd,{targs[1]}" + (",store>" if t(5) else ">")
+        return f"ac_march<fwd,{targs[1]}" + (",store>" if t(6) else ">")
     if base == "adj_allencahn3d7":     # <R, DP, NT>
         return "adj_allencahn3d7<dp>" if t(1) else "adj_allencahn3d7"
     if base == "adj_vardiff2d9":       # <R, WANT_DK, TR, DP, NT>

@@ -76,12 +76,13 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
   if (p->kind != ADST_ALLENCAHN3D7 && p->n[2] != 1)
     return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
   // Every launch covers the grid with workgroups of 256 work-items: tiles of
-  // 252 or 256 columns by 4 or 8 rows for the 2-D kinds, columns of 62 or 64
-  // by 14 or 8 points over 32 planes for the 3-D kind. The work-item count must fit the 32-bit dispatch grid.
+  // 240 to 256 columns by 4 or 8 rows for the 2-D kinds, columns of 56 to 64
+  // by 8 to 16 points over 32 or 64 planes for the 3-D kind. The work-item
+  // count of the smallest tiles must fit the 32-bit dispatch grid.
   const int64_t tiles =
       p->kind == ADST_ALLENCAHN3D7
-          ? ((p->n[0] + 61) / 62) * ((p->n[1] + 7) / 8) * ((p->n[2] + 31) / 32)
-          : ((p->n[0] + 251) / 252) * ((p->n[1] + 3) / 4);
+          ? ((p->n[0] + 55) / 56) * ((p->n[1] + 7) / 8) * ((p->n[2] + 31) / 32)
+          : ((p->n[0] + 239) / 240) * ((p->n[1] + 3) / 4);
   if ((tiles + 8) * 256 >= (int64_t(1) << 32))
     return fail(ADST_ERR_UNSUPPORTED, "grid too thin in x/y for the tile shape");
   if (grads & ~(ADST_GRAD_COEFF | ADST_GRAD_PARAMS))

@@ -60,13 +60,13 @@ def test_median_interval_empirical_coverage():
     ("void adst::(anonymous namespace)::gs_wave<double, true, true>(double*)", "gs_wave<adj>"),
     ("void adst::(anonymous namespace)::seed_loss<double, 1>(double const*)", "seed_loss"),
     ("__amd_rocclr_copyBuffer", "hipMemcpyAsync copy"),
-    ("void adst::(anonymous namespace)::ac_march<double, 3, false, 4, 64, true, false>(adst::("
+    ("void adst::(anonymous namespace)::ac_march<double, 3, false, 4, 64, 0, true, false>(adst::("
      "anonymous namespace)::AcMarchArgs<double>)", "ac_march<fwd,3,store>"),
-    ("void adst::(anonymous namespace)::ac_march<double, 0, true, 4, 64, false, true>(x)",
+    ("void adst::(anonymous namespace)::ac_march<double, 0, true, 4, 64, 1, false, true>(x)",
      "ac_march<adj>"),
-    ("void adst::(anonymous namespace)::ac_march<double, 1, true, 4, 64, false, true>(x)",
+    ("void adst::(anonymous namespace)::ac_march<double, 1, true, 4, 64, 1, false, true>(x)",
      "ac_march<fwd1+adj>"),
-    ("void adst::(anonymous namespace)::ac_march<double, 1, false, 4, 64, false, true>(x)",
+    ("void adst::(anonymous namespace)::ac_march<double, 1, false, 4, 64, 0, false, true>(x)",
      "ac_march<fwd,1>"),
 ])
 def test_rocprof_names_map_to_library_labels(name, label):
