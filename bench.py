@@ -18,9 +18,11 @@ calls each and are reported under "workloads".
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--sched S]
                     [--force-tape] [--no-fuse] [--dparams] [--limit LO HI]
                     [--no-extras] [--no-cpu-baseline]
+    python bench.py --sweep [--workload NAME] [--steps K] ...
     python bench.py --rocprof-summary KT_DIR [--fetch DIR --write DIR] ...
 
-The second form turns rocprofv3 output (kernel stats, FETCH_SIZE and
+The second form times the Allen-Cahn workloads across schedules and
+budgets (SWEEP below). The third form turns rocprofv3 output (kernel stats, FETCH_SIZE and
 WRITE_SIZE counter runs) into the markdown tables kept under profiles/,
 with the kernels named as this file and the library name them.
 """
@@ -58,6 +60,20 @@ EXTRAS = [
     ("gaussseidel2d5_f64_400x400_T100", {}),
     ("gaussseidel2d5_f64_4096x4096_T100", {}),
 ]
+# The budget/schedule sweep (--sweep) of the two Allen-Cahn workloads:
+# store-all where the tape fits, two or three binomial budgets and the
+# uniform schedule at the workloads' own budget (state: 1 GiB at 512^3,
+# 8.6 GB at 1024^3).
+SWEEP = [
+    ("allencahn3d7_f64_512cube_T50", "store_all", 64 << 30),
+    ("allencahn3d7_f64_512cube_T50", "binomial", 3 << 30),
+    ("allencahn3d7_f64_512cube_T50", "binomial", 8 << 30),
+    ("allencahn3d7_f64_512cube_T50", "uniform", 8 << 30),
+    ("allencahn3d7_f64_1024cube_T200", "binomial", 26_000_000_000),
+    ("allencahn3d7_f64_1024cube_T200", "binomial", 64_000_000_000),
+    ("allencahn3d7_f64_1024cube_T200", "binomial", 130_000_000_000),
+    ("allencahn3d7_f64_1024cube_T200", "uniform", 64_000_000_000),
+]
 # The oracle's sample for the headline: the same kind, precision, step count,
 # loss and per-point work on a 128^3 grid (a store-all tape of the full grid,
 # 1.7 TB, cannot be held).
@@ -82,6 +98,9 @@ def parse():
     ap.add_argument("--traced-calls", type=int, default=2,
                     help="calls with per-launch HIP events, for the kernels' average durations")
     ap.add_argument("--no-extras", action="store_true", help="only the chosen workload")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only the budget/schedule sweep of the Allen-Cahn workloads (one JSON "
+                         "line, each entry with its phases' kernels)")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -185,10 +204,11 @@ def _roof(workload, k, npts):
     }
 
 
-def run_workload(adst, torch, w, opts, steps, warmup, traced_calls, say):
+def run_workload(adst, torch, w, opts, steps, warmup, traced_calls, say, inp=None):
     """Time `steps` adst_vjp calls of workload w (inputs resident in HBM),
     then `traced_calls` more with per-launch events. Returns the result dict
-    and the host inputs (for the oracle)."""
+    and the host inputs (for the oracle; pass them back in to skip drawing
+    them again)."""
     from paper_2509_02197_amd.workloads import dims_of, make_inputs
     sched = opts.get("sched", w.sched)
     budget = opts.get("budget", w.budget_bytes)
@@ -197,7 +217,8 @@ def run_workload(adst, torch, w, opts, steps, warmup, traced_calls, say):
     lim = opts.get("limit")
     want_dp = bool(opts.get("dparams"))
     say(f"# workload {w.name} sched={SCHED_NAMES[sched]} budget={budget} flags={flags}")
-    inp = make_inputs(w)
+    if inp is None:
+        inp = make_inputs(w)
     dev = torch.device("cuda:0")
     x0 = torch.from_numpy(inp["x0"]).to(dev)
     K = torch.from_numpy(inp["K"]).to(dev) if inp["K"] is not None else None
@@ -364,6 +385,40 @@ def cpu_baseline(w, target_s, lim=None, want_dp=False):
             "host_cpu": _cpu_model(), "host_nproc": os.cpu_count()}
 
 
+def sweep(args):
+    """The budget/schedule sweep: one JSON line, one entry per (workload,
+    schedule, budget) with the median call and every kernel's average launch
+    duration and achieved bandwidth from the library's per-launch events."""
+    import torch
+    import paper_2509_02197_amd as adst
+    from paper_2509_02197_amd.workloads import WORKLOADS
+
+    def say(m):
+        print(m, file=sys.stderr, flush=True)
+
+    ids = {v: k for k, v in SCHED_NAMES.items()}
+    entries, inputs = [], {}
+    for name, sched, budget in SWEEP:
+        if args.workload and name != args.workload:
+            continue
+        w = WORKLOADS[name]
+        r, inputs[name] = run_workload(adst, torch, w, {"sched": ids[sched], "budget": budget},
+                                       args.steps, args.warmup, args.traced_calls, say,
+                                       inputs.get(name))
+        say(f"# {name} {r['schedule']} slots={r['slots']}: median {r['ms_median']} ms")
+        entries.append({k: r[k] for k in ("workload", "schedule", "budget_bytes", "slots",
+                                          "fwd_steps", "recompute_steps", "fwd_kernels",
+                                          "adj_kernels", "ms_median", "ms_ci95",
+                                          "pt_steps_per_s", "phase_ms", "fwd_gbps",
+                                          "adj_gbps", "kernels")})
+        for k in entries[-1]["kernels"]:
+            k["frac"] = round(k["gbps"] / HBM_PEAK_GBPS, 4)
+        for name_ in [n for n in inputs if n != name]:
+            del inputs[name_]
+    print(json.dumps({"sweep": entries, "steps": args.steps, "warmup": args.warmup,
+                      "traced_calls": args.traced_calls}), flush=True)
+
+
 def main_bench(args):
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
@@ -484,13 +539,31 @@ def _csv(d, suffix):
     return list(csv.DictReader(open(sorted(hits)[0])))
 
 
+def _kernel_rows(d):
+    """Per-kernel rows (Name, Calls, TotalDurationNs, MinNs, MaxNs,
+    Percentage) from a rocprofv3 --stats CSV, or from the kernel dispatches
+    of its SQLite output (*_results.db) when it was not written as CSV."""
+    if glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True):
+        return _csv(d, "kernel_stats.csv")
+    import sqlite3
+    hits = glob.glob(os.path.join(d, "**", "*_results.db"), recursive=True)
+    if not hits:
+        raise SystemExit(f"no *kernel_stats.csv or *_results.db under {d}")
+    con = sqlite3.connect(sorted(hits)[0])
+    agg = con.execute("SELECT name, COUNT(*), SUM(duration), MIN(duration), MAX(duration) "
+                      "FROM kernels GROUP BY name").fetchall()
+    total = sum(r[2] for r in agg) or 1
+    return [{"Name": n, "Calls": c, "TotalDurationNs": t, "MinNs": lo, "MaxNs": hi,
+             "Percentage": 100.0 * t / total} for n, c, t, lo, hi in agg]
+
+
 def rocprof_summary(args):
     """Markdown of kernel times (and HBM bytes with --fetch/--write) from
     rocprofv3 CSV output, kernels named by the library's labels; HBM bytes
     are FETCH_SIZE and WRITE_SIZE scaled so that the last plain copy of the
     run (a 1 GiB hipMemcpyAsync from --copy-probe-mib 1024) counts its bytes
     exactly; the per-launch figures also go to profiles/traffic.json."""
-    rows = _csv(args.rocprof_summary, "kernel_stats.csv")
+    rows = _kernel_rows(args.rocprof_summary)
     out = [f"# Kernel time: {args.title}", "",
            "Command (from the repository root on the GPU box, after "
            "`cd /tmp && export TMPDIR=/tmp`):", "", "```", args.command, "```", "",
@@ -557,8 +630,15 @@ def rocprof_summary(args):
 
 def main():
     args = parse()
+    if args.gpus != 1 and not args.rocprof_summary:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              f"multi-GPU path", file=sys.stderr)
+        sys.exit(2)
     if args.rocprof_summary:
         rocprof_summary(args)
+        return
+    if args.sweep:
+        sweep(args)
         return
     main_bench(args)
 

@@ -71,3 +71,27 @@ def test_median_interval_empirical_coverage():
 ])
 def test_rocprof_names_map_to_library_labels(name, label):
     assert bench.rocprof_label(name) == label
+
+
+def test_kernel_rows_from_rocpd_database(tmp_path):
+    # rocprofv3 writes SQLite when no CSV format is asked for: the summary
+    # aggregates its kernel dispatches per name
+    import sqlite3
+    d = tmp_path / "kt" / "host"
+    d.mkdir(parents=True)
+    con = sqlite3.connect(str(d / "run_results.db"))
+    con.execute("CREATE TABLE kernels (name TEXT, duration INTEGER)")
+    con.executemany("INSERT INTO kernels VALUES (?, ?)",
+                    [("a", 10), ("a", 30), ("b", 60)])
+    con.commit()
+    con.close()
+    rows = {r["Name"]: r for r in bench._kernel_rows(str(tmp_path / "kt"))}
+    assert rows["a"]["Calls"] == 2 and rows["a"]["TotalDurationNs"] == 40
+    assert rows["a"]["MinNs"] == 10 and rows["a"]["MaxNs"] == 30
+    assert abs(rows["b"]["Percentage"] - 60.0) < 1e-12
+
+
+def test_sweep_lists_known_workloads_and_schedules():
+    from paper_2509_02197_amd.workloads import WORKLOADS
+    for name, sched, budget in bench.SWEEP:
+        assert name in WORKLOADS and sched in bench.SCHED_NAMES.values() and budget > 0
