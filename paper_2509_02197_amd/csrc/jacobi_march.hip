@@ -56,11 +56,9 @@ namespace adst {
 namespace {
 
 constexpr int kLanes = 64;
-constexpr int kRows = 48;      // rows per chunk of an interior strip
-constexpr int kAdjRows = 42;   // the same for the marching adjoint: 4086 waves
-                               // at 4096^2, about one per wave slot of the chip
-                               // (54.0 against 55.1 us per 6-step launch; the
-                               // forward is faster with 48)
+constexpr int kRows = 48;      // rows per chunk of an interior strip (42 for the
+                               // adjoint measured the same: 56.3 against 56.1 us
+                               // per 6-step launch at 4096^2, one rocprofv3 job)
 constexpr int kEdgeRows = 12;  // rows per chunk of the first and last strip
 constexpr int kEndRows = 6;    // rows of a strip's first and last chunk, whose
                                // blocks near the grid's top and bottom edge
@@ -70,8 +68,6 @@ constexpr int kUnroll = 6;     // input rows per straight-line block
 constexpr int kXcds = 8;       // workgroup i runs on XCD i mod 8
 static_assert(kUnroll % kAhead == 0 && kUnroll % 3 == 0, "register slots must stay static");
 static_assert(2 * kEndRows <= kRows && kEdgeRows <= kRows && kRows <= 64, "chunk sizes");
-static_assert(2 * kEndRows <= kAdjRows && kEdgeRows <= kAdjRows && kAdjRows <= kRows,
-              "chunk sizes");
 
 // Whole-wave lane shifts: lane i receives lane i-1's value (lane 0: 0) or
 // lane i+1's (lane 63: 0).
@@ -446,7 +442,7 @@ hipError_t march_launch(const StepShape& s, const R* x, R* y, hipStream_t st) {
   if (ADJ && s.nx <= G::V) return hipErrorInvalidValue;  // a lane would hold both ring columns
   MarchGrid g;
   int64_t blocks;
-  if (!make_grid(s.nx, s.ny, G::OW, &g, &blocks, ADJ ? kAdjRows : kRows))
+  if (!make_grid(s.nx, s.ny, G::OW, &g, &blocks))
     return hipErrorInvalidValue;
   const bool vec = s.nx % G::V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(y) & 15u) == 0;

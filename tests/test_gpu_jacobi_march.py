@@ -6,9 +6,12 @@ time levels in registers; strips overlap by whole 16-byte vectors of halo
 and each chunk of rows recomputes n rows above and below itself. The shapes
 put strip edges, chunk edges and the vector width against the grid's fixed
 ring: widths around one strip (120 or 116 output columns in fp64, 248 or 240
-in fp32, for 3-4 and 5-6 steps), heights around the row chunks (12 rows in
-the first and last strip, 48 in the others), widths that are not a multiple
-of the vector (element loads and stores) and grids narrower than the halo.
+in fp32, for 3-4 and 5-6 steps), heights around the row chunks (6 rows at
+each end of a strip; between them 12-row chunks in the first and last strip
+and 48-row chunks in the others, so heights 60/61 over three or more strips
+put a chunk edge on the last rows, and 54/55 one 12-row edge-strip chunk
+boundary), widths that are not a multiple of the vector (element loads and
+stores) and grids narrower than the halo.
 Step counts cover one launch of each depth and runs that split into several
 launches with a shorter remainder.
 
@@ -35,6 +38,7 @@ SHAPES = [
     (F64, (50, 120)), (F64, (49, 121)), (F64, (12, 116)), (F64, (13, 117)),
     (F64, (48, 128)), (F64, (60, 236)), (F64, (97, 240)), (F64, (25, 241)),
     (F64, (3, 1000)), (F64, (1000, 3)), (F64, (130, 4)), (F64, (61, 350)),
+    (F64, (54, 370)), (F64, (55, 361)), (F64, (60, 370)), (F64, (61, 365)),
     (F32, (50, 248)), (F32, (11, 249)), (F32, (49, 240)), (F32, (24, 496)),
     (F32, (4, 4)), (F32, (7, 5)), (F32, (37, 1021)), (F32, (100, 250)),
 ]
