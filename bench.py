@@ -148,7 +148,7 @@ def kernel_source(kernel):
         return "jacobi_march.hip"
     if kernel.startswith("gs_wave"):
         return "gauss_seidel.hip"
-    if "allencahn" in kernel and os.path.exists(
+    if ("allencahn" in kernel or kernel.startswith("ac_march")) and os.path.exists(
             os.path.join(ROOT, "paper_2509_02197_amd", "csrc", "allencahn.hip")):
         return "allencahn.hip"
     return "kernels.hip"

@@ -566,13 +566,14 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7_lim(const R* __rest
 // every lane's offset within a plane is fixed for the whole launch (an
 // offset beyond the descriptor's range for cells outside the grid, and a
 // range of 0 for planes outside it, so those reads return 0 without a
-// branch). Writes are masked by the lanes' exec bits instead: stores with
-// out-of-range lanes were measured to write up to 1.8x the bytes they keep. Planes are held in rings of 4
-// slots, plane q in slot (q - pfirst) mod 4, and the iteration body is
-// unrolled 4 times so every slot index is a compile-time constant. Each
-// input plane is requested two iterations before its first use. One barrier
-// per iteration: rows published at iteration p (into LDS half
-// (p - pfirst + 1) mod 2) are read at iteration p + 1.
+// branch). Stores are issued only by the lanes whose cell lies in the
+// output tile (exec-masked), never to an out-of-range offset. Planes are
+// held in rings of 4 slots, plane q in slot (q - pfirst) mod 4, and the
+// iteration body is unrolled 4 times so every slot index is a compile-time
+// constant. The input planes are requested DA planes ahead of the plane
+// being evaluated (the side columns two). One barrier per iteration: rows
+// published at iteration p (into LDS half (p - pfirst + 1) mod 2) are read
+// at iteration p + 1.
 constexpr int kMW = 4;
 constexpr uint32_t kOob = 0xFFFFFF00u;  // a buffer offset beyond any plane
 

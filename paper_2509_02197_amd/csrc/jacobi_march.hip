@@ -59,6 +59,11 @@ constexpr int kLanes = 64;
 constexpr int kRows = 48;      // rows per chunk of an interior strip (42 for the
                                // adjoint measured the same: 56.3 against 56.1 us
                                // per 6-step launch at 4096^2, one rocprofv3 job)
+constexpr int kLimRows = 192;  // rows per chunk of the limiter's one-step adjoint:
+                               // with two arrays in flight, fewer and longer
+                               // waves were faster (48 / 64 / 128 / 192 / 256
+                               // rows: 99.5 / 93.5 / 92.7 / 90.4 / 102.9 us
+                               // per launch at 4096^2 f64)
 constexpr int kEdgeRows = 12;  // rows per chunk of the first and last strip
 constexpr int kEndRows = 6;    // rows of a strip's first and last chunk, whose
                                // blocks near the grid's top and bottom edge
@@ -664,7 +669,7 @@ hipError_t lim_adjoint_launch(const StepShape& s, const R* x, const R* g, R* gp,
   constexpr int V = 16 / sizeof(R), OW = kLanes * V - 2 * V;
   MarchGrid grid;
   int64_t blocks;
-  if (!make_grid(s.nx, s.ny, OW, &grid, &blocks)) return hipErrorInvalidValue;
+  if (!make_grid(s.nx, s.ny, OW, &grid, &blocks, kLimRows)) return hipErrorInvalidValue;
   const bool vec = s.nx % V == 0 && (reinterpret_cast<uintptr_t>(x) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(g) & 15u) == 0 &&
                    (reinterpret_cast<uintptr_t>(gp) & 15u) == 0;
@@ -727,7 +732,7 @@ int64_t jacobi_x_adjoint_slots(const StepShape& s) {
   const int V = s.dtype == ADST_F64 ? 2 : 4, OW = kLanes * V - 2 * V;  // as lim_adjoint_launch
   MarchGrid g;
   int64_t blocks;
-  if (!make_grid(s.nx, s.ny, OW, &g, &blocks)) return 0;
+  if (!make_grid(s.nx, s.ny, OW, &g, &blocks, kLimRows)) return 0;
   return int64_t(g.nedge) * g.ce + int64_t(g.ns - g.nedge) * g.ci;
 }
 

@@ -118,12 +118,14 @@ def test_infinite_bounds_give_the_unlimited_bits(kind, dtype, shape, T, loss):
 # register-marching pass; asking for the constants' gradients as well takes
 # the separate mask pass and the tiled adjoint. Both must give the same
 # dx0 bits. Shapes put the column strips (124 output columns in fp64, 248
-# in fp32), the row chunks and the element path (odd widths) against the
-# ring, plus grids narrower than a strip and a few rows tall.
+# in fp32), the row chunks (6 rows at each end of a strip, 12 between them
+# in the first and last strip and 192 in the others: heights 204/205 over
+# three or more strips) and the element path (odd widths) against the ring,
+# plus grids narrower than a strip and a few rows tall.
 FUSED_LIM_SHAPES = [
     (F64, (50, 124)), (F64, (49, 125)), (F64, (97, 248)), (F64, (3, 300)), (F64, (300, 3)),
     (F64, (5, 4)), (F64, (61, 351)), (F32, (50, 248)), (F32, (13, 249)), (F32, (100, 497)),
-    (F32, (7, 5)),
+    (F32, (7, 5)), (F64, (204, 380)), (F64, (205, 373)), (F64, (410, 130)), (F32, (211, 750)),
 ]
 
 
@@ -161,6 +163,7 @@ def test_fused_limiter_adjoint_full_grid():
 FUSED_LIM_AC_SHAPES = [
     (F64, (39, 45, 67)), (F64, (33, 9, 65)), (F64, (1, 20, 70)), (F64, (40, 1, 3)),
     (F64, (3, 4, 5)), (F32, (17, 33, 65)), (F32, (64, 16, 128)),
+    (F64, (64, 28, 112)), (F64, (65, 29, 113)), (F64, (130, 15, 57)), (F32, (129, 14, 56)),
 ]
 
 
