@@ -968,13 +968,24 @@ inline bool march_fits(const StepShape& s) {
   return int64_t(s.nx) * s.ny * (s.dtype == ADST_F64 ? 8 : 4) < (int64_t(1) << 31);
 }
 
-// Rows per wave and planes per chunk of the z-march launches.
-constexpr int kMarchRows = 4, kMarchPlanes = 64, kMarchAhead = 1;
+// Rows per wave and planes per chunk of the z-march launches. The plain
+// adjoint (no forward level: few values live per row) takes eight rows per
+// wave, a 64 x 32 region, where a plane is kTallPlaneBytes or more: its
+// row-beyond reads and LDS exchanges halve per point (1024^3 step 4.79 ->
+// 4.62 ms, in one process against four rows; two rows: 4.98 ms; 128-plane
+// chunks no faster). At 512^3 (2 MiB planes) four rows stay faster (0.568
+// against 0.586 ms).
+constexpr int kMarchRows = 4, kAdjMarchRows = 8, kMarchPlanes = 64, kMarchAhead = 1;
+constexpr int64_t kTallPlaneBytes = int64_t(4) << 20;
 
-template <class R, int NF, bool ADJ, bool ST>
+template <class R, int NF, bool ADJ, bool ST, int RR = kMarchRows>
 hipError_t march(const StepShape& s, const R* x, const R* g, R* y, R* m0, R* m1,
                  hipStream_t st) {
-  using M = AcMarch<NF, kMarchRows, kMarchPlanes>;
+  if constexpr (NF == 0 && RR != kAdjMarchRows) {
+    if (int64_t(s.nx) * s.ny * int64_t(sizeof(R)) >= kTallPlaneBytes)
+      return march<R, NF, ADJ, ST, kAdjMarchRows>(s, x, g, y, m0, m1, st);
+  }
+  using M = AcMarch<NF, RR, kMarchPlanes>;
   const int tx = cdiv(s.nx, M::OX), ty = cdiv(s.ny, M::OY);
   const int nt = tx * ty * cdiv(s.nz, kMarchPlanes);
   const R D = R(s.p0), C = R(s.p1);
@@ -982,9 +993,9 @@ hipError_t march(const StepShape& s, const R* x, const R* g, R* y, R* m0, R* m1,
                          D, C, R(1) + D * R(-6), R(3) * C};
   const dim3 grid(xcd_grid(nt)), block(kBX, kMW);
   if (streams(s))
-    ac_march<R, NF, ADJ, kMarchRows, kMarchPlanes, kMarchAhead, ST, true><<<grid, block, 0, st>>>(a);
+    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, true><<<grid, block, 0, st>>>(a);
   else
-    ac_march<R, NF, ADJ, kMarchRows, kMarchPlanes, kMarchAhead, ST, false><<<grid, block, 0, st>>>(a);
+    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, false><<<grid, block, 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -3,12 +3,15 @@ fused run of two or three) run inside the adjoint launch that reads their
 result (x_{t-1} formed on chip, never stored), against one launch per step
 and against the oracle (needs an MI355X).
 
-The single-step and plain adjoint launches own a 64 x 16 region of every
-plane (64 lanes by four waves of four rows) over 64-plane chunks; the fused
-forward-adjoint launch has the same output tile (the forward step's
-neighbours come from a one-cell ring read with the region). The shapes put
+The plain adjoint launch owns a 64 x 16 region of every plane (64 lanes by
+four waves of four rows; 64 x 32, eight rows per wave, where a plane holds
+4 MiB or more), the fused forward-adjoint launches a 64 x 16 region (the
+output tile is the region less n-1 cells per side for n forward levels,
+56 columns wide for two), all over 64-plane chunks; the forward steps'
+neighbours come from a one-cell ring read with the region. The shapes put
 grids narrower than one tile, exact tiles, tiles plus one and ragged tails
-against these sizes in every axis, with one to three planes.
+against these sizes in every axis, with one to three planes, and two grids
+with planes of over 4 MiB.
 
 Bars: gradients of binomial plans (whose adjoint steps read states a
 single recomputed step produced) bit-identical to one launch per step and
@@ -31,6 +34,8 @@ SHAPES = [
     (F64, (1, 1, 1)), (F64, (2, 3, 70)), (F64, (3, 16, 64)), (F64, (65, 17, 65)),
     (F64, (64, 16, 128)), (F64, (9, 33, 129)), (F64, (20, 15, 63)), (F64, (5, 1, 200)),
     (F64, (7, 50, 1)), (F32, (17, 31, 97)), (F32, (66, 16, 64)),
+    (F64, (4, 32, 64)), (F64, (70, 65, 66)), (F32, (3, 96, 130)),
+    (F64, (3, 515, 1030)), (F32, (2, 1057, 1100)),
 ]
 
 
