@@ -117,8 +117,8 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
 }
 
 // K forward steps in one launch (temporal blocking in 2.5-D).
-// A workgroup of 64 x 4 threads owns a region of 64 columns x SY = 4 RPT
-// rows of each plane (RPT rows per thread, four apart) and marches in z. At
+// A workgroup of 64 x BY threads owns a region of 64 columns x SY = BY * RPT
+// rows of each plane (RPT rows per thread, BY apart) and marches in z. At
 // iteration p it evaluates step 1 at plane p from x(p-1..p+1), and step l at
 // plane p-l+1 from step l-1's planes p-l..p-l+2. Every step is evaluated on
 // the whole region but is valid only on its inner (64 - 2(l-1)) x (SY -
@@ -129,10 +129,15 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
 // registers. Intermediate values are 0 outside the grid, which is the zero
 // ghost value the next step reads; every point evaluates the single-step
 // expression, so any split of the steps into launches gives the same bits.
-// Measured at 1024^3 f64, three steps per launch (64 x 16 regions, 64
-// planes) beat two (the launches of a recomputation run drop by a third);
-// four, with 24-row regions, needed 178 VGPRs and with 16-row regions
-// evaluated 7 points per output point, and both were slower.
+// Measured at 1024^3 f64, three steps per launch (64-plane chunks) beat two
+// (the launches of a recomputation run drop by a third); four, with 24-row
+// regions, needed 178 VGPRs and with 16-row regions evaluated 7 points per
+// output point, and both were slower. Three steps run on 64 x 32 regions of
+// sixteen waves of two rows (a region point per output point and step
+// 1.42 -> 1.22; 1024^3 launch 4.84 -> 4.49 ms, in one process; four waves
+// of four rows had been the shape before, eight waves of three or four
+// rows and sixteen of three or four were slower), two steps on 64 x 16
+// regions of four waves of four rows (no other shape was faster).
 // Output tiles narrower than the region allows: non-temporal stores into a
 // 64-byte segment that two workgroups share were measured to cost a third
 // of a single step's time (3.26 -> 4.48 ms for a 1024^3 step whose tiles
@@ -142,9 +147,9 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7(const R* __restrict
 // and more of the region evaluated for nothing).
 template <int K>
 constexpr int ac_out_width() { return K == 2 ? 56 : kBX - 2 * (K - 1); }
-template <int K, int RPT, int NZ>
+template <int K, int RPT, int NZ, int BY>
 struct AcN {
-  static constexpr int SX = kBX, SY = kBY * RPT;
+  static constexpr int SX = kBX, SY = BY * RPT;
   static constexpr int OX = ac_out_width<K>(), OY = SY - 2 * (K - 1);  // output tile
   static constexpr int ZC = NZ;                               // output planes
   static_assert(OX + 2 * (K - 1) <= SX, "the output tile and its halo fit the region");
@@ -155,17 +160,17 @@ struct AcN {
 // every state is kept moves 8 + 8n bytes per point for n steps instead of
 // 16n). They are stored without the non-temporal hint: the reverse sweep
 // reads them back soon after (measured at 512^3: 58.9 -> 58.5 ms per call).
-template <class R, int K, int RPT, int NZ, bool NT, bool ST>
-__global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restrict__ x,
+template <class R, int K, int RPT, int NZ, bool NT, bool ST, int BY>
+__global__ __launch_bounds__(kBX * BY) void fwd_allencahn3d7_n(const R* __restrict__ x,
                                                                R* __restrict__ y,
                                                                R* __restrict__ mid0,
                                                                R* __restrict__ mid1, int nx,
                                                                int ny, int nz, int tiles_x,
                                                                int tiles_y, int ntiles, R D,
                                                                R C) {
-  using A = AcN<K, RPT, NZ>;
+  using A = AcN<K, RPT, NZ, BY>;
   constexpr int SX = A::SX, SY = A::SY, LX = SX + 2, LY = SY + 2, H = K - 1;
-  static_assert(K >= 2 && 2 * LX + 2 * SY <= kThreads, "ring cells: one per thread");
+  static_assert(K >= 2 && 2 * LX + 2 * SY <= kBX * BY, "ring cells: one per thread");
   static_assert(!ST || K <= 3, "intermediate states go to mid0 (step 1) and mid1 (step 2)");
   __shared__ R xt[LY][LX];
   __shared__ R yt[K - 1][SY][SX];  // steps 1 .. K-1
@@ -184,7 +189,7 @@ __global__ __launch_bounds__(kThreads) void fwd_allencahn3d7_n(const R* __restri
   auto ld = [&](int k, int j, int i) -> R {
     return (k >= 0 && k < nz && inxy(j, i)) ? x[k * plane + j * nx + i] : R(0);
   };
-  auto row = [&](int q) { return ty + kBY * q; };  // region row of the thread's q-th cell
+  auto row = [&](int q) { return ty + BY * q; };  // region row of the thread's q-th cell
   // one cell of the LDS ring around the region
   int hly = -1, hlx = 0;
   if (tid < LX) {
@@ -1000,26 +1005,26 @@ hipError_t march(const StepShape& s, const R* x, const R* g, R* y, R* m0, R* m1,
 }
 
 // mids (nullable): the intermediate states' buffers, step l's at mids[l-1].
-template <class R, int K, int RPT, int NZ>
+template <class R, int K, int RPT, int NZ, int BY>
 hipError_t ac_forward_n(const StepShape& s, const R* x, R* y, R* const* mids, hipStream_t st) {
-  using A = AcN<K, RPT, NZ>;
+  using A = AcN<K, RPT, NZ, BY>;
   const int tx = cdiv(s.nx, A::OX), ty = cdiv(s.ny, A::OY);
   const int nt = tx * ty * cdiv(s.nz, A::ZC);
-  const dim3 grid(xcd_grid(nt)), block(kBX, kBY);
+  const dim3 grid(xcd_grid(nt)), block(kBX, BY);
   R* m0 = mids ? mids[0] : nullptr;
   R* m1 = (mids && K >= 3) ? mids[1] : nullptr;
   const bool str = streams(s) != 0;
   if (mids && str)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, true, true><<<grid, block, 0, st>>>(
+    fwd_allencahn3d7_n<R, K, RPT, NZ, true, true, BY><<<grid, block, 0, st>>>(
         x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   else if (mids)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, false, true><<<grid, block, 0, st>>>(
+    fwd_allencahn3d7_n<R, K, RPT, NZ, false, true, BY><<<grid, block, 0, st>>>(
         x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   else if (str)
-    fwd_allencahn3d7_n<R, K, RPT, NZ, true, false><<<grid, block, 0, st>>>(
+    fwd_allencahn3d7_n<R, K, RPT, NZ, true, false, BY><<<grid, block, 0, st>>>(
         x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   else
-    fwd_allencahn3d7_n<R, K, RPT, NZ, false, false><<<grid, block, 0, st>>>(
+    fwd_allencahn3d7_n<R, K, RPT, NZ, false, false, BY><<<grid, block, 0, st>>>(
         x, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt, R(s.p0), R(s.p1));
   return hipGetLastError();
 }
@@ -1033,9 +1038,9 @@ hipError_t ac_forward_steps(const StepShape& s, const void* xv, void* yv, void* 
   R* const* m = reinterpret_cast<R* const*>(mids);
   switch (n) {
     case 2:
-      return ac_forward_n<R, 2, 4, 32>(s, x, y, m, st);
+      return ac_forward_n<R, 2, 4, 32, kBY>(s, x, y, m, st);
     case 3:
-      return ac_forward_n<R, 3, 4, 64>(s, x, y, m, st);
+      return ac_forward_n<R, 3, 2, 64, 16>(s, x, y, m, st);
   }
   return hipErrorInvalidValue;
 }

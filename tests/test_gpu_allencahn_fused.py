@@ -1,10 +1,11 @@
 """Temporal blocking of the Allen-Cahn kind, up to three forward steps per
 launch, against one launch per step and against the oracle (needs an MI355X).
 
-A launch of n steps has each workgroup (64 lanes by four waves of four
-rows) evaluate the n steps on a 64 x 16 region of each plane while marching
-in z over 64-plane chunks; the output tile is the region less n - 1 cells
-on each side (62 x 14, 60 x 12). The shapes put grids narrower than one tile,
+A launch of n steps has each workgroup evaluate the n steps on a region of
+each plane while marching in z: two steps on 64 x 16 regions (four waves of
+four rows) over 32-plane chunks with 56 x 14 output tiles, three steps on
+64 x 32 regions (sixteen waves of two rows) over 64-plane chunks with
+60 x 28 output tiles. The shapes put grids narrower than one tile,
 exact tiles, tiles plus one and ragged tails against these sizes in every
 axis, and runs of 1 to 3 planes. Step counts cover one launch of each depth
 and runs that split into full launches and a shorter remainder.
@@ -33,6 +34,7 @@ SHAPES = [
     (F64, (32, 18, 58)), (F64, (33, 19, 59)), (F64, (65, 14, 62)), (F64, (40, 37, 130)),
     (F64, (70, 15, 63)), (F64, (5, 40, 200)), (F64, (64, 13, 61)),
     (F32, (17, 33, 130)), (F32, (33, 19, 117)), (F32, (4, 4, 4)),
+    (F64, (65, 28, 60)), (F64, (64, 29, 121)), (F64, (9, 57, 120)), (F32, (66, 56, 61)),
 ]
 
 

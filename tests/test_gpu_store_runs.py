@@ -5,8 +5,8 @@ writes each state of the run, up to three steps (Allen-Cahn) or two
 (variable coefficients) per launch.
 
 The shapes put grids narrower than one tile, exact tiles, tiles plus one and
-ragged tails against the fused kernels' output tiles (Allen-Cahn 62 x 14 over
-32 planes and 60 x 12 over 64 planes; variable coefficients 252 x 8), and
+ragged tails against the fused kernels' output tiles (Allen-Cahn 56 x 14 over
+32 planes and 60 x 28 over 64 planes; variable coefficients 252 x 8), and
 one-plane and one-row grids. Plans: store-all (one chain through every
 step) and binomial plans whose budgets leave store-all runs of several
 lengths.
@@ -31,6 +31,7 @@ F64, F32 = adst.ADST_F64, adst.ADST_F32
 CASES = [
     (AC, F64, (1, 1, 1)), (AC, F64, (3, 15, 63)), (AC, F64, (33, 14, 62)),
     (AC, F64, (65, 13, 61)), (AC, F64, (40, 29, 125)), (AC, F32, (17, 33, 130)),
+    (AC, F64, (64, 28, 60)), (AC, F64, (66, 57, 113)),
     (VD, F32, (1, 7)), (VD, F32, (9, 253)), (VD, F32, (17, 504)), (VD, F32, (33, 1000)),
     (VD, F64, (25, 505)), (VD, F64, (12, 3)),
 ]
