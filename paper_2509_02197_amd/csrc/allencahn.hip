@@ -158,8 +158,9 @@ struct AcN {
 // ST: the intermediate states are stored too, step l's into mid[l-1], each
 // point by the workgroup whose output tile holds it (a run of steps whose
 // every state is kept moves 8 + 8n bytes per point for n steps instead of
-// 16n). They are stored without the non-temporal hint: the reverse sweep
-// reads them back soon after (measured at 512^3: 58.9 -> 58.5 ms per call).
+// 16n). They take the non-temporal hint with the output where states are
+// large (1024^3 call 1890 -> 1875 ms, in one process; 512^3 unchanged): the
+// reverse sweep reads them back, but only after many other launches.
 template <class R, int K, int RPT, int NZ, bool NT, bool ST, int BY>
 __global__ __launch_bounds__(kBX * BY) void fwd_allencahn3d7_n(const R* __restrict__ x,
                                                                R* __restrict__ y,
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(kBX * BY) void fwd_allencahn3d7_n(const R* __restri
                        : R(0);
         if constexpr (ST) {
           if (cin && tile_col && r >= H && r < SY - H && p >= z0 && p < z1)
-            put<false>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
+            put<NT>(&mid0[p * plane + (j0 - H + r) * nx + ic], sn[0][q]);
         }
       }
     }
@@ -265,7 +266,7 @@ __global__ __launch_bounds__(kBX * BY) void fwd_allencahn3d7_n(const R* __restri
           sn[l - 1][q] = v;
           if constexpr (ST) {
             if (ok && tile_col && r >= H && r < SY - H && pl >= z0 && pl < z1)
-              put<false>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
+              put<NT>(&(l == 2 ? mid1 : mid0)[pl * plane + j * nx + ic], v);
           }
         } else if (ok && tile_col && pl >= z0 && pl < z1) {
           put<NT>(&y[pl * plane + j * nx + ic], v);
