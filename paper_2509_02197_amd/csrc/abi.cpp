@@ -251,7 +251,7 @@ std::string kernel_label(const Checked& c, const adst_action& a, int32_t stored,
       return k == ADST_ALLENCAHN3D7
                  ? "fwd_allencahn3d7_n<" + std::to_string(stored) + ",store>"
                  : std::string(kFwd[k]) + "_x2<store>";
-    if (a.n <= 1) return kFwd[k];
+    if (a.n <= 1) return c.shape.limit ? std::string(kFwd[k]) + "<lim>" : std::string(kFwd[k]);
     if (k == ADST_ALLENCAHN3D7) return "fwd_allencahn3d7_n<" + std::to_string(a.n) + ">";
     if (a.n == 2) return std::string(kFwd[k]) + "_x2";
     return "jacobi_march<fwd," + std::to_string(a.n) + ">";
@@ -695,7 +695,12 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
       case ADST_OP_SEED: {
         const void* xsrc = buffer(a.src);
         void* xcopy = (steps == 0 && xT) ? xT : nullptr;
-        e = traced(cat, "seed_loss", npts * double(pp.seed), [&] {
+        // the half square with x_T already in g_T's buffer only reads it
+        const double seed_bytes =
+            (loss == ADST_LOSS_HALF_SQ && xsrc == g_T ? double(itemsize(c.shape.dtype))
+                                                      : double(pp.seed)) +
+            (xcopy ? double(itemsize(c.shape.dtype)) : 0.0);
+        e = traced(cat, "seed_loss", npts * seed_bytes, [&] {
           return launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, g_T, xcopy, partials,
                              stream);
         });
