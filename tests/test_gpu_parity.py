@@ -158,14 +158,16 @@ def test_zero_steps(kind, dtype, shape, dK):
 
 
 def test_trace_fills_phase_times():
+    # 23 steps in two slots: recomputation runs of their own remain beside
+    # the steps that run inside adjoint launches
     inp = inputs(AC, F64, (16, 32, 64), 6)
-    g = gpu_vjp(AC, inp, 9, DOT_W, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL,
+    g = gpu_vjp(AC, inp, 23, DOT_W, 2 * inp["x0"].nbytes, adst.ADST_SCHED_BINOMIAL,
                 flags=adst.ADST_TRACE)
     info = g["info"]
     assert info["ms_fwd_sweep"] > 0 and info["ms_adj"] > 0 and info["ms_seed"] > 0
     assert info["ms_fwd_recompute"] > 0
     assert info["ms_total"] >= info["ms_adj"]
-    check_against_oracle(AC, F64, inp, 9, DOT_W, False, g)
+    check_against_oracle(AC, F64, inp, 23, DOT_W, False, g)
 
 
 def test_workspace_reuse_between_calls():
