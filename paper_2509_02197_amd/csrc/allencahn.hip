@@ -608,9 +608,9 @@ __global__ __launch_bounds__(kBX * TW) void adj_allencahn3d7_lim(const R* __rest
 constexpr int kMW = 4;
 constexpr uint32_t kOob = 0xFFFFFF00u;  // a buffer offset beyond any plane
 
-template <int NF, int RR, int ZC>
+template <int NF, int RR, int ZC, int MW = kMW>
 struct AcMarch {
-  static constexpr int SX = kBX, SY = kMW * RR;
+  static constexpr int SX = kBX, SY = MW * RR;
   static constexpr int H = NF > 1 ? NF - 1 : 0;  // cells per side the last level loses
   // output tile: 64 columns (aligned) for the plain adjoint; 56 (a whole
   // number of 64-byte segments) with two forward levels (6.92 -> 6.84 ms
@@ -730,9 +730,9 @@ __device__ inline float zero_outside(float v, uint64_t m) {
 template <int N>
 using IC = std::integral_constant<int, N>;
 
-template <class R, int NF, bool ADJ, int RR, int ZC, int DA, bool ST, bool NT>
-__global__ __launch_bounds__(kBX * kMW) void ac_march(AcMarchArgs<R> a) {
-  using M = AcMarch<NF, RR, ZC>;
+template <class R, int NF, bool ADJ, int RR, int ZC, int DA, bool ST, bool NT, int MW>
+__global__ __launch_bounds__(kBX * MW) void ac_march(AcMarchArgs<R> a) {
+  using M = AcMarch<NF, RR, ZC, MW>;
   constexpr int H = M::H, SY = M::SY;
   constexpr int NL = NF > 0 ? NF : 1;   // levels kept in rings: 0 .. NL-1
   constexpr int NE = (NF > 0 ? NF : 0) + (ADJ ? 1 : 0);  // exchanged fields
@@ -741,7 +741,7 @@ __global__ __launch_bounds__(kBX * kMW) void ac_march(AcMarchArgs<R> a) {
   static_assert(!ST || NF >= 2, "stored states are intermediate forward levels");
   // rows published for the neighbours: [half][field][0: a wave's last row
   // (read by the wave below it), 1: its first row (read by the wave above)]
-  __shared__ R pub[2][NE][2][kMW][kBX];
+  __shared__ R pub[2][NE][2][MW][kBX];
   int b = xcd_tile(a.ntiles);
   if (b >= a.ntiles) return;
   const int bx = b % a.tiles_x;
@@ -761,7 +761,7 @@ __global__ __launch_bounds__(kBX * kMW) void ac_march(AcMarchArgs<R> a) {
   const int cr = lane == 0 ? c - 1 : c + 1;
   const bool crin = (lane == 0 || lane == kBX - 1) && cr >= 0 && cr < nx;
   const int jr = w == 0 ? jw - 1 : jw + RR;
-  const bool jrin = (w == 0 || w == kMW - 1) && jr >= 0 && jr < ny && cin;
+  const bool jrin = (w == 0 || w == MW - 1) && jr >= 0 && jr < ny && cin;
   // byte offsets within a plane (kOob where the cell is not read or written)
   uint32_t off[RR], offx[RR], offo[RR];
   bool in[RR];
@@ -846,14 +846,14 @@ __global__ __launch_bounds__(kBX * kMW) void ac_march(AcMarchArgs<R> a) {
   // last wave for w = 3), [1][w] wave w's first row (the row above the first
   // wave for w = 0). A wave's first row reads its y-1 neighbours from the
   // slot above it, its last row its y+1 neighbours from the slot below.
-  const int up_slot = w > 0 ? w - 1 : kMW;                  // [0][w-1], or [1][0]
-  const int dn_slot = w < kMW - 1 ? kMW + w + 1 : kMW - 1;  // [1][w+1], or [0][3]
+  const int up_slot = w > 0 ? w - 1 : MW;                 // [0][w-1], or [1][0]
+  const int dn_slot = w < MW - 1 ? MW + w + 1 : MW - 1;   // [1][w+1], or [0][MW-1]
   auto lds = [&](int hh, int f, int slot) -> R& {
     return (&pub[hh][f][0][0][0])[slot * kBX + lane];
   };
   auto publish = [&](int hh, int f, const R (&v)[RR], R beyond) {
-    lds(hh, f, w) = w == kMW - 1 ? beyond : v[RR - 1];
-    lds(hh, f, kMW + w) = w == 0 ? beyond : v[0];
+    lds(hh, f, w) = w == MW - 1 ? beyond : v[RR - 1];
+    lds(hh, f, MW + w) = w == 0 ? beyond : v[0];
   };
   // the stencil's neighbour sum at row i, in the forward's order
   //   ((((x-1 + x+1) + y-1) + y+1) + z-1) + z+1
@@ -1009,24 +1009,24 @@ inline bool march_fits(const StepShape& s) {
 constexpr int kMarchRows = 4, kAdjMarchRows = 8, kMarchPlanes = 64, kMarchAhead = 1;
 constexpr int64_t kTallPlaneBytes = int64_t(4) << 20;
 
-template <class R, int NF, bool ADJ, bool ST, int RR = kMarchRows>
+template <class R, int NF, bool ADJ, bool ST, int RR = kMarchRows, int MW = kMW>
 hipError_t march(const StepShape& s, const R* x, const R* g, R* y, R* m0, R* m1,
                  hipStream_t st) {
   if constexpr (NF == 0 && RR != kAdjMarchRows) {
     if (int64_t(s.nx) * s.ny * int64_t(sizeof(R)) >= kTallPlaneBytes)
-      return march<R, NF, ADJ, ST, kAdjMarchRows>(s, x, g, y, m0, m1, st);
+      return march<R, NF, ADJ, ST, kAdjMarchRows, MW>(s, x, g, y, m0, m1, st);
   }
-  using M = AcMarch<NF, RR, kMarchPlanes>;
+  using M = AcMarch<NF, RR, kMarchPlanes, MW>;
   const int tx = cdiv(s.nx, M::OX), ty = cdiv(s.ny, M::OY);
   const int nt = tx * ty * cdiv(s.nz, kMarchPlanes);
   const R D = R(s.p0), C = R(s.p1);
   const AcMarchArgs<R> a{x, g, y, m0, m1, s.nx, s.ny, s.nz, tx, ty, nt,
                          D, C, R(1) + D * R(-6), R(3) * C};
-  const dim3 grid(xcd_grid(nt)), block(kBX, kMW);
+  const dim3 grid(xcd_grid(nt)), block(kBX, MW);
   if (streams(s))
-    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, true><<<grid, block, 0, st>>>(a);
+    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, true, MW><<<grid, block, 0, st>>>(a);
   else
-    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, false><<<grid, block, 0, st>>>(a);
+    ac_march<R, NF, ADJ, RR, kMarchPlanes, kMarchAhead, ST, false, MW><<<grid, block, 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -1157,18 +1157,27 @@ hipError_t ac_launch_adjoint(const StepShape& s, const void* x, const void* g, v
                                static_cast<float*>(gp), dp_part, dp_first, st);
 }
 
+// Three recomputed levels take eight waves (a 64 x 32 region: 1.42 -> 1.22
+// region points per output point and level; 1024^3 launch with two kept
+// states 11.21 -> 10.93 ms, in one process and one placement of the
+// buffers); one or two keep four (eight measured no faster for two).
+constexpr int kFused3Waves = 8;
+
 template <class R>
 hipError_t forward_adjoint(const StepShape& s, const R* x, const R* g, R* gp, int32_t n,
                            R* m0, R* m1, hipStream_t st) {
   if (m0) {  // the first n - 1 levels are stored too
     if (n == 2 && !m1) return march<R, 2, true, true>(s, x, g, gp, m0, nullptr, st);
-    if (n == 3 && m1) return march<R, 3, true, true>(s, x, g, gp, m0, m1, st);
+    if (n == 3 && m1)
+      return march<R, 3, true, true, kMarchRows, kFused3Waves>(s, x, g, gp, m0, m1, st);
     return hipErrorInvalidValue;
   }
   switch (n) {
     case 1: return march<R, 1, true, false>(s, x, g, gp, nullptr, nullptr, st);
     case 2: return march<R, 2, true, false>(s, x, g, gp, nullptr, nullptr, st);
-    case 3: return march<R, 3, true, false>(s, x, g, gp, nullptr, nullptr, st);
+    case 3:
+      return march<R, 3, true, false, kMarchRows, kFused3Waves>(s, x, g, gp, nullptr, nullptr,
+                                                                st);
   }
   return hipErrorInvalidValue;
 }

@@ -5,15 +5,17 @@ and against the oracle (needs an MI355X).
 
 Chains of one or two single steps whose states a later adjoint step reads,
 ending in a fused step, run in one launch that also writes the kept states
-(where a plane holds 4 MiB or more). The plain adjoint launch owns a 64 x 16 region of every plane (64 lanes by
-four waves of four rows; 64 x 32, eight rows per wave, where a plane holds
-4 MiB or more), the fused forward-adjoint launches a 64 x 16 region (the
-output tile is the region less n-1 cells per side for n forward levels,
-56 columns wide for two), all over 64-plane chunks; the forward steps'
-neighbours come from a one-cell ring read with the region. The shapes put
-grids narrower than one tile, exact tiles, tiles plus one and ragged tails
-against these sizes in every axis, with one to three planes, and two grids
-with planes of over 4 MiB.
+(where a plane holds 4 MiB or more). The plain adjoint launch owns a 64 x 16
+region of every plane (64 lanes by four waves of four rows; 64 x 32, eight
+rows per wave, where a plane holds 4 MiB or more); the fused
+forward-adjoint launches own a 64 x 16 region (one or two levels) or a
+64 x 32 region of eight waves (three levels), and their output tile is the
+region less n-1 cells per side for n forward levels (56 columns wide for
+two); all march over 64-plane chunks, and the forward steps' neighbours come
+from a one-cell ring read with the region. The shapes put grids narrower
+than one tile, exact tiles, tiles plus one and ragged tails against these
+sizes in every axis, with one to three planes, and two grids with planes of
+over 4 MiB.
 
 Bars: gradients of binomial plans (whose adjoint steps read states a
 single recomputed step produced) bit-identical to one launch per step and
@@ -38,7 +40,7 @@ SHAPES = [
     (F64, (64, 16, 128)), (F64, (9, 33, 129)), (F64, (20, 15, 63)), (F64, (5, 1, 200)),
     (F64, (7, 50, 1)), (F32, (17, 31, 97)), (F32, (66, 16, 64)),
     (F64, (4, 32, 64)), (F64, (70, 65, 66)), (F32, (3, 96, 130)),
-    (F64, (3, 515, 1030)), (F32, (2, 1057, 1100)),
+    (F64, (3, 515, 1030)), (F32, (2, 1057, 1100)), (F64, (5, 28, 60)), (F64, (66, 29, 61)),
 ]
 
 
