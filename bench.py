@@ -520,8 +520,7 @@ def rocprof_label(name):
         return "gs_wave<adj>" if t(1) else "gs_wave<fwd>"
     if base == "ac_march":             # <R, NF, ADJ, RR, ZC, DA, ST, NT>
         if t(2):
-            st = ",store" if t(6) else ""
-            return "ac_march<adj>" if targs[1] == "0" else f"ac_march<fwd{targs[1]}+adj{st}>"
+            return "ac_march<adj>" if targs[1] == "0" else f"ac_march<fwd{targs[1]}+adj>"
         return f"ac_march<fwd,{targs[1]}" + (",store>" if t(6) else ">")
     if base == "adj_allencahn3d7":     # <R, DP, NT>
         return "adj_allencahn3d7<dp>" if t(1) else "adj_allencahn3d7"

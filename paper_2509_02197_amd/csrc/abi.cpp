@@ -141,38 +141,6 @@ bool fused_fwd_adj(const Checked& c, const std::vector<adst_action>& acts, size_
   return true;
 }
 
-// A chain of single forward steps whose states a later adjoint step reads,
-// ending in a step fused with the adjoint after it: the fused launch also
-// writes the chain's kept states (2: one kept step before the fused one, 3:
-// two; 0: no such chain at acts[i]). The kept states go to buffers distinct
-// from each other and from the chain's input. Taken where a plane holds 4
-// MiB or more: at 1024^3 f64 the headline call went 1894 -> 1879 ms (one
-// process), at 512^3 the separate launches stayed faster (53.2 against
-// 54.0 ms).
-int32_t fused_store_levels(const Checked& c, const std::vector<adst_action>& acts, size_t i) {
-  if (c.shape.kind != ADST_ALLENCAHN3D7 || c.want_dp || c.shape.limit || !c.fuse_adj_fwd)
-    return 0;
-  if (int64_t(c.shape.nx) * c.shape.ny * int64_t(itemsize(c.shape.dtype)) < (int64_t(4) << 20))
-    return 0;
-  for (int32_t nf = 2; nf <= kAcMaxFuse && i + nf < acts.size(); ++nf) {
-    for (int32_t k = 0; k < nf; ++k) {
-      const adst_action& a = acts[i + k];
-      if (a.op != ADST_OP_FWD || a.n != 1) return 0;
-      if (k > 0 && (a.src != acts[i + k - 1].dst || a.t != acts[i + k - 1].t + 1)) return 0;
-    }
-    for (int32_t k = 0; k + 1 < nf; ++k)
-      if (fused_fwd_adj(c, acts, i + k)) return 0;
-    if (!fused_fwd_adj(c, acts, i + nf - 1)) continue;  // a longer chain, perhaps
-    for (int32_t k = 0; k + 1 < nf; ++k) {
-      if (acts[i + k].dst == acts[i].src) return 0;
-      for (int32_t m = k + 1; m < nf; ++m)
-        if (acts[i + k].dst == acts[i + m].dst) return 0;
-    }
-    return nf;
-  }
-  return 0;
-}
-
 // Length of the run of single forward steps starting at acts[i] that one
 // store-through launch takes (1: none): each action reads the state the one
 // before it wrote, and the states go to buffers that differ from each other
@@ -180,15 +148,13 @@ int32_t fused_store_levels(const Checked& c, const std::vector<adst_action>& act
 // A step fused with the adjoint after it ends the run before it.
 int32_t stored_run(const Checked& c, const std::vector<adst_action>& acts, size_t i) {
   const int32_t depth = c.store_fwd;
-  if (depth < 2 || acts[i].op != ADST_OP_FWD || fused_fwd_adj(c, acts, i) ||
-      fused_store_levels(c, acts, i))
-    return 1;
+  if (depth < 2 || acts[i].op != ADST_OP_FWD || fused_fwd_adj(c, acts, i)) return 1;
   int32_t n = 1;
   while (n < depth && i + n < acts.size()) {
     const adst_action& a = acts[i + n];
     const adst_action& p = acts[i + n - 1];
     if (a.op != ADST_OP_FWD || a.src != p.dst || a.t != p.t + 1) break;
-    if (fused_fwd_adj(c, acts, i + n) || fused_store_levels(c, acts, i + n)) break;
+    if (fused_fwd_adj(c, acts, i + n)) break;
     bool clash = a.dst == acts[i].src;
     for (int32_t k = 0; k < n; ++k) clash = clash || acts[i + k].dst == a.dst;
     if (clash) break;
@@ -325,10 +291,6 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
     const bool adj_op = a.op == ADST_OP_ADJ || a.op == ADST_OP_ADJ2 || a.op == ADST_OP_ADJW;
     if (!fwd_op && !adj_op) continue;
     if (fused_fwd_adj(c, plan.acts, i)) continue;  // counted with its adjoint
-    if (const int32_t nf = fused_store_levels(c, plan.acts, i)) {
-      i += nf - 2;  // the kept steps: counted with the adjoint
-      continue;
-    }
     const int64_t k = c.in_place ? gs_kernel_launches(c.shape, adj_op, a.n) : 1;
     (fwd_op ? info->fwd_kernels : info->adj_kernels) += k;
     i += stored_run(c, plan.acts, i) - 1;
@@ -349,11 +311,6 @@ void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk
     switch (a.op) {
       case ADST_OP_FWD: {
         if (fused_fwd_adj(c, plan.acts, i)) break;  // moves the adjoint's bytes only
-        if (const int32_t nf = fused_store_levels(c, plan.acts, i)) {
-          per_point += uint64_t(nf - 1) * itemsize(c.shape.dtype);  // the kept states
-          i += nf - 2;
-          break;
-        }
         const int32_t r = stored_run(c, plan.acts, i);
         fwd_per_point += fb + uint64_t(r - 1) * itemsize(c.shape.dtype);
         i += r - 1;
@@ -671,20 +628,13 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
     return r;
   };
   // a recomputed forward action and the adjoint step after it, in one launch
-  auto fused_launch = [&](const adst_action& f, int32_t n = 0, void* mid0 = nullptr,
-                          void* mid1 = nullptr) -> hipError_t {
-    if (n == 0) n = f.n;
-    const int32_t kept = mid0 ? n - 1 : 0;  // states written besides g_{t-1}
-    const double bytes =
-        npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra +
-                      uint64_t(kept) * itemsize(c.shape.dtype));
-    const hipError_t r =
-        traced(Tracer::ADJ,
-               "ac_march<fwd" + std::to_string(n) + "+adj" + (kept ? ",store>" : ">"), bytes,
-               [&] {
-                 return ac_launch_forward_adjoint(c.shape, buffer(f.src), gcur, gnext, n, stream,
-                                                  mid0, mid1);
-               });
+  auto fused_launch = [&](const adst_action& f) -> hipError_t {
+    const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
+    const hipError_t r = traced(Tracer::ADJ, "ac_march<fwd" + std::to_string(f.n) + "+adj>",
+                                bytes, [&] {
+                                  return ac_launch_forward_adjoint(c.shape, buffer(f.src), gcur,
+                                                                   gnext, f.n, stream);
+                                });
     std::swap(gcur, gnext);
     first_adj = false;
     return r;
@@ -714,12 +664,6 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
         if (fused_fwd_adj(c, plan.acts, ai)) {
           e = fused_launch(a);
           ++ai;
-          break;
-        }
-        if (const int32_t nf = fused_store_levels(c, plan.acts, ai)) {
-          e = fused_launch(a, nf, buffer(a.dst),
-                           nf == 3 ? buffer(plan.acts[ai + 1].dst) : nullptr);
-          ai += nf;  // the chain and its adjoint step
           break;
         }
         const int32_t r = stored_run(c, plan.acts, ai);

@@ -738,7 +738,7 @@ __global__ __launch_bounds__(kBX * MW) void ac_march(AcMarchArgs<R> a) {
   constexpr int NE = (NF > 0 ? NF : 0) + (ADJ ? 1 : 0);  // exchanged fields
   constexpr int GF = NE - 1;            // exchange field of g
   static_assert(NF >= 0 && NF <= 3 && (NF > 0 || ADJ), "levels");
-  static_assert(!ST || NF >= 2, "stored states are intermediate forward levels");
+  static_assert(!ST || (NF >= 2 && !ADJ), "store-through runs are forward runs");
   // rows published for the neighbours: [half][field][0: a wave's last row
   // (read by the wave below it), 1: its first row (read by the wave above)]
   __shared__ R pub[2][NE][2][MW][kBX];
@@ -915,7 +915,7 @@ __global__ __launch_bounds__(kBX * MW) void ac_march(AcMarchArgs<R> a) {
         const R o = zero_outside(v, qin ? rowmask[i] : 0);
         if constexpr (NF > 1) L[1][B0][i] = o; else last[i] = o;
         if constexpr (ST) {
-          if (offo[i] != kOob) bstore<R, NT ? kAuxNT : 0>(rm, offo[i], o);
+          if (offo[i] != kOob) bstore<R, 0>(rm, offo[i], o);
         }
       }
     }
@@ -935,7 +935,7 @@ __global__ __launch_bounds__(kBX * MW) void ac_march(AcMarchArgs<R> a) {
         const R o = zero_outside(v, qin ? rowmask[i] : 0);
         if constexpr (l < NF) L[l][sc][i] = o; else last[i] = o;
         if constexpr (ST && l == 2 && NF == 3) {
-          if (offo[i] != kOob) bstore<R, NT ? kAuxNT : 0>(rm, offo[i], o);
+          if (offo[i] != kOob) bstore<R, 0>(rm, offo[i], o);
         }
       }
     };
@@ -1158,20 +1158,15 @@ hipError_t ac_launch_adjoint(const StepShape& s, const void* x, const void* g, v
 }
 
 // Three recomputed levels take eight waves (a 64 x 32 region: 1.42 -> 1.22
-// region points per output point and level; 1024^3 launch with two kept
-// states 11.21 -> 10.93 ms, in one process and one placement of the
-// buffers); one or two keep four (eight measured no faster for two).
+// region points per output point and level; at 1024^3, 11.21 -> 10.93 ms
+// for a launch that also wrote two intermediate states, in one process and
+// one placement of the buffers); one or two keep four (eight measured no
+// faster for two).
 constexpr int kFused3Waves = 8;
 
 template <class R>
 hipError_t forward_adjoint(const StepShape& s, const R* x, const R* g, R* gp, int32_t n,
-                           R* m0, R* m1, hipStream_t st) {
-  if (m0) {  // the first n - 1 levels are stored too
-    if (n == 2 && !m1) return march<R, 2, true, true>(s, x, g, gp, m0, nullptr, st);
-    if (n == 3 && m1)
-      return march<R, 3, true, true, kMarchRows, kFused3Waves>(s, x, g, gp, m0, m1, st);
-    return hipErrorInvalidValue;
-  }
+                           hipStream_t st) {
   switch (n) {
     case 1: return march<R, 1, true, false>(s, x, g, gp, nullptr, nullptr, st);
     case 2: return march<R, 2, true, false>(s, x, g, gp, nullptr, nullptr, st);
@@ -1183,15 +1178,14 @@ hipError_t forward_adjoint(const StepShape& s, const R* x, const R* g, R* gp, in
 }
 
 hipError_t ac_launch_forward_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
-                                     int32_t n, hipStream_t st, void* mid0, void* mid1) {
+                                     int32_t n, hipStream_t st) {
   if (s.limit || !march_fits(s)) return hipErrorInvalidValue;
   return s.dtype == ADST_F64
              ? forward_adjoint<double>(s, static_cast<const double*>(x),
                                        static_cast<const double*>(g), static_cast<double*>(gp), n,
-                                       static_cast<double*>(mid0), static_cast<double*>(mid1), st)
+                                       st)
              : forward_adjoint<float>(s, static_cast<const float*>(x),
-                                      static_cast<const float*>(g), static_cast<float*>(gp), n,
-                                      static_cast<float*>(mid0), static_cast<float*>(mid1), st);
+                                      static_cast<const float*>(g), static_cast<float*>(gp), n, st);
 }
 
 bool ac_fuses_forward_adjoint(const StepShape& s) { return !s.limit && march_fits(s); }

@@ -35,13 +35,10 @@ int64_t ac_dparam_slots(const StepShape& s);
 // n = 1 .. kAcMaxFuse recomputed forward steps and the adjoint step that
 // reads their result, in one launch: g_prev = J_t^T g_next with x_{t-1} =
 // F^n(x) formed on chip and never stored (x = x_{t-1-n}); no limiter and no
-// constants' gradients. With mid0 (n = 2) or mid0 and mid1 (n = 3) the
-// states of the first n - 1 steps are also written there (steps whose
-// states a later adjoint step reads). ac_fuses_forward_adjoint tells
-// whether the shape takes it.
+// constants' gradients. ac_fuses_forward_adjoint tells whether the shape
+// takes it.
 hipError_t ac_launch_forward_adjoint(const StepShape& s, const void* x, const void* g, void* gp,
-                                     int32_t n, hipStream_t st, void* mid0 = nullptr,
-                                     void* mid1 = nullptr);
+                                     int32_t n, hipStream_t st);
 bool ac_fuses_forward_adjoint(const StepShape& s);
 
 // Temporal blocking: the most steps one launch may take (1 = none). The

@@ -66,8 +66,6 @@ def test_median_interval_empirical_coverage():
      "ac_march<adj>"),
     ("void adst::(anonymous namespace)::ac_march<double, 1, true, 4, 64, 1, false, true>(x)",
      "ac_march<fwd1+adj>"),
-    ("void adst::(anonymous namespace)::ac_march<double, 2, true, 4, 64, 1, true, true>(x)",
-     "ac_march<fwd2+adj,store>"),
     ("void adst::(anonymous namespace)::ac_march<double, 1, false, 4, 64, 0, false, true>(x)",
      "ac_march<fwd,1>"),
 ])

@@ -214,45 +214,6 @@ def fused_forward_adjoint_pairs(acts, indices=False):
     return found if indices else len(found)
 
 
-def kept_chains(acts, plane_bytes):
-    """Single forward steps whose states a later adjoint step reads, run in
-    the fused launch of the step after them (which runs inside the next
-    adjoint launch): chains of one or two such steps, each reading the state
-    the one before wrote, into buffers distinct from each other and from the
-    chain's input; only where a plane holds 4 MiB or more. Returns the kept
-    steps' indices."""
-    if plane_bytes < 4 << 20:
-        return []
-    FWD = adst.ADST_OP_FWD
-    fused = set(fused_forward_adjoint_pairs(acts, indices=True))
-    kept, i = [], 0
-    while i < len(acts):
-        take = 0
-        for nf in (2, 3):
-            if i + nf >= len(acts):
-                break
-            chain = acts[i:i + nf]
-            if any(a[0] != FWD or a[4] != 1 for a in chain):
-                break
-            if any(chain[k][2] != chain[k - 1][3] or chain[k][1] != chain[k - 1][1] + 1
-                   for k in range(1, nf)):
-                break
-            if any(i + k in fused for k in range(nf - 1)):
-                break
-            if i + nf - 1 not in fused:
-                continue
-            dsts = [a[3] for a in chain[:-1]]
-            if len(set(dsts)) == len(dsts) and chain[0][2] not in dsts:
-                take = nf
-            break
-        if take:
-            kept += list(range(i, i + take - 1))
-            i += take
-        else:
-            i += 1
-    return kept
-
-
 def test_workspace_and_bytes():
     p = prob(dims=(100, 30, 7))
     S = 100 * 30 * 7 * 8
@@ -269,13 +230,10 @@ def test_workspace_and_bytes():
     n = 100 * 30 * 7
     acts = adst.adst_plan_actions(p, 12, 4 * S, adst.ADST_SCHED_BINOMIAL)
     fused = fused_forward_adjoint_pairs(acts)
-    kept = len(kept_chains(acts, 100 * 30 * 8))
     assert fused > 0
-    assert info.fwd_kernels < info.fwd_launches - fused - kept
-    assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels +
-                                      8 * (info.fwd_launches - fused - kept))
-    # a kept step's state is written by the adjoint launch it runs in
-    assert info.alg_bytes == info.fwd_alg_bytes + n * (24 * 12 + 16 + 8 * kept)
+    assert info.fwd_kernels < info.fwd_launches - fused
+    assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels + 8 * (info.fwd_launches - fused))
+    assert info.alg_bytes == info.fwd_alg_bytes + n * (24 * 12 + 16)
     # without fusion every forward action moves its own bytes
     pn = prob(dims=(100, 30, 7), flags=adst.ADST_NO_FUSE)
     info = adst.adst_plan(pn, 12, 4 * S, adst.ADST_SCHED_BINOMIAL)
@@ -308,19 +266,17 @@ def test_store_through_runs(kind, dtype, dims, grads, depth, bytes_in):
 def test_store_through_runs_counted_like_the_executor():
     # binomial plans: the launches fwd_kernels counts are the runs of chained
     # single steps (up to three, into buffers other than the run's input)
-    # and the fused actions; steps run inside an adjoint launch (fused with
-    # it, or kept by a chain that ends in such a step) count with it
+    # and the fused actions
     p = adst.make_problem(adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (10, 9, 8))
     S = 10 * 9 * 8 * 8
     for T, slots in ((8, 3), (13, 4), (23, 5), (40, 6)):
         acts = adst.adst_plan_actions(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
         info = adst.adst_plan(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
         fused = set(fused_forward_adjoint_pairs(acts, indices=True))
-        inside = fused | set(kept_chains(acts, 10 * 9 * 8))
         kernels, i = 0, 0
         while i < len(acts):
             a = acts[i]
-            if i in inside:  # runs inside the next adjoint launch
+            if i in fused:  # runs inside the next adjoint launch
                 i += 1
                 continue
             if a[0] in (adst.ADST_OP_FWD, adst.ADST_OP_FWD2):
@@ -331,32 +287,13 @@ def test_store_through_runs_counted_like_the_executor():
                     b, prev = acts[i + r], acts[i + r - 1]
                     if b[0] != adst.ADST_OP_FWD or b[2] != prev[3] or b[1] != prev[1] + 1:
                         break
-                    if i + r in inside:
+                    if i + r in fused:
                         break
                     if b[3] == a[2] or any(acts[i + k][3] == b[3] for k in range(r)):
                         break
                     r += 1
             i += r
         assert info.fwd_kernels == kernels
-
-
-def test_kept_chains_counted_like_the_executor():
-    # planes of 4 MiB or more: chains of kept single steps ending in a step
-    # fused with the adjoint run in that adjoint launch, which also writes
-    # the kept states (8 B per point each); smaller planes keep them apart
-    for nx, ny in ((1024, 512), (1024, 511)):
-        p = adst.make_problem(adst.ADST_ALLENCAHN3D7, adst.ADST_F64, (nx, ny, 3))
-        S = nx * ny * 3 * 8
-        n = nx * ny * 3
-        for T, slots in ((23, 3), (40, 4)):
-            acts = adst.adst_plan_actions(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
-            info = adst.adst_plan(p, T, slots * S, adst.ADST_SCHED_BINOMIAL)
-            kept = kept_chains(acts, nx * ny * 8)
-            assert bool(kept) == (nx * ny * 8 >= 4 << 20), (nx, ny, T)
-            fused = fused_forward_adjoint_pairs(acts)
-            assert info.fwd_alg_bytes == n * (8 * info.fwd_kernels +
-                                              8 * (info.fwd_launches - fused - len(kept)))
-            assert info.alg_bytes == info.fwd_alg_bytes + n * (24 * T + 16 + 8 * len(kept))
 
 
 def test_zero_steps_plan():
