@@ -520,8 +520,8 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   if (XS) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
   const int i = i0 + (int)threadIdx.x;
   // the accumulated dK of the thread's cells, requested with the staged
-  // rows (where the row loop is unrolled, so the registers stay static)
-  constexpr bool PRE = WANT_DK && !DP;
+  // rows (the row loop is unrolled, so the registers stay static)
+  constexpr bool PRE = WANT_DK;
   R dk0[PRE ? TR : 1];
   if (PRE) {
 #pragma unroll
@@ -551,9 +551,11 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
     const bool all_in = i0 >= 1 && i0 + kVdTW <= nx - 1 && j0 >= 1 && j0 + TR <= ny - 1;
     auto rows = [&](auto all_in_t) {
     constexpr bool ALL_IN = decltype(all_in_t)::value;
-    // rolled with both dK and the constants' sums, to keep four waves per SIMD
-    constexpr int kRowUnroll = (WANT_DK && DP) ? 1 : TR;
-#pragma unroll kRowUnroll
+    // unrolled also with both dK and the constants' sums: with the dK
+    // requests moved ahead of the loop, 389 -> 377 us per 8192^2 f32 step
+    // (a rolled loop had kept four waves per SIMD; unrolled without the
+    // early requests it took 508 us)
+#pragma unroll
     for (int r = 0; r < TR; ++r) {
       const int j = j0 + r;
       if (!ALL_IN && j >= ny) break;
