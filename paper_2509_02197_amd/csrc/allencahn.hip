@@ -310,6 +310,8 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   __shared__ R tilex[DP ? kAcTY + 2 : 1][DP ? kAcTX + 2 : 1];
   AcTile t;
   if (!ac_tile(nx, ny, nz, tiles_x, tiles_y, ntiles, &t)) return;  // the whole block
+  DpPrev prev;
+  if (DP) prev = dp_prev<2>(dp, t.b);
   const int plane = nx * ny;
   auto ld = [&](const R* a, int k, int j, int i) -> R {
     return (k >= 0 && k < nz && j >= 0 && j < ny && i >= 0 && i < nx) ? a[k * plane + j * nx + i]
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
   }
   if (DP) {
     __syncthreads();
-    dp_commit(dp, t.b, a0, a1);
+    dp_commit<2>(dp, t.b, prev, a0, a1);
   }
 }
 
@@ -1000,21 +1002,23 @@ inline bool march_fits(const StepShape& s) {
 }
 
 // Rows per wave and planes per chunk of the z-march launches. The plain
-// adjoint (no forward level: few values live per row) takes eight rows per
-// wave, a 64 x 32 region, where a plane is kTallPlaneBytes or more: its
-// row-beyond reads and LDS exchanges halve per point (1024^3 step 4.79 ->
-// 4.62 ms, in one process against four rows; two rows: 4.98 ms; 128-plane
-// chunks no faster). At 512^3 (2 MiB planes) four rows stay faster (0.568
-// against 0.586 ms).
-constexpr int kMarchRows = 4, kAdjMarchRows = 8, kMarchPlanes = 64, kMarchAhead = 1;
+// adjoint (no forward level: few values live per row) runs a 64 x 32 region,
+// as eight waves of four rows, where a plane is kTallPlaneBytes or more: its
+// row-beyond reads halve per point and eight waves hide more of the LDS
+// exchange (1024^3 step 4.76 -> 4.68 ms and 4.67 -> 4.55 ms in the two
+// buffer placements against a 64 x 16 region; four waves of eight rows:
+// 4.62 ms in the faster placement, sixteen waves of two rows: 5.24 ms;
+// 128-plane chunks no faster). At 512^3 (2 MiB planes) the 64 x 16 region
+// stays faster (0.568 against 0.586 ms).
+constexpr int kMarchRows = 4, kMarchPlanes = 64, kMarchAhead = 1, kTallAdjWaves = 8;
 constexpr int64_t kTallPlaneBytes = int64_t(4) << 20;
 
 template <class R, int NF, bool ADJ, bool ST, int RR = kMarchRows, int MW = kMW>
 hipError_t march(const StepShape& s, const R* x, const R* g, R* y, R* m0, R* m1,
                  hipStream_t st) {
-  if constexpr (NF == 0 && RR != kAdjMarchRows) {
+  if constexpr (NF == 0 && MW == kMW) {
     if (int64_t(s.nx) * s.ny * int64_t(sizeof(R)) >= kTallPlaneBytes)
-      return march<R, NF, ADJ, ST, kAdjMarchRows, MW>(s, x, g, y, m0, m1, st);
+      return march<R, NF, ADJ, ST, RR, kTallAdjWaves>(s, x, g, y, m0, m1, st);
   }
   using M = AcMarch<NF, RR, kMarchPlanes, MW>;
   const int tx = cdiv(s.nx, M::OX), ty = cdiv(s.ny, M::OY);

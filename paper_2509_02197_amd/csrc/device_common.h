@@ -92,14 +92,33 @@ struct DpOut {
   int nslots, first;
 };
 
-// All threads of the block call this (it synchronises).
-__device__ inline void dp_commit(DpOut dp, int slot, double a0, double a1) {
-  block_sum2(a0, a1);
+// The slot's sums of the steps before, requested when the workgroup starts
+// so that the read's latency passes while it works (none on the first step,
+// which overwrites). NC: the constants of the kind (1 or 2).
+struct DpPrev {
+  double p0 = 0.0, p1 = 0.0;
+};
+template <int NC>
+__device__ inline DpPrev dp_prev(DpOut dp, int slot) {
+  DpPrev r;
+  if (!dp.first && threadIdx.x == 0 && threadIdx.y == 0) {
+    r.p0 = dp.part[slot];
+    if (NC == 2) r.p1 = dp.part[dp.nslots + slot];
+  }
+  return r;
+}
+
+// All threads of the block call this (it synchronises). With one constant
+// the second slots hold +0.
+template <int NC>
+__device__ inline void dp_commit(DpOut dp, int slot, DpPrev prev, double a0, double a1) {
+  if (NC == 2)
+    block_sum2(a0, a1);
+  else
+    a0 = block_sum(a0);
   if (threadIdx.x == 0 && threadIdx.y == 0) {
-    double* p0 = dp.part + slot;
-    double* p1 = dp.part + dp.nslots + slot;
-    *p0 = dp.first ? a0 : *p0 + a0;
-    *p1 = dp.first ? a1 : *p1 + a1;
+    dp.part[slot] = dp.first ? a0 : prev.p0 + a0;
+    dp.part[dp.nslots + slot] = NC == 2 ? (dp.first ? a1 : prev.p1 + a1) : 0.0;
   }
 }
 

@@ -515,6 +515,8 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   const int b = xcd_tile(ntiles);
   if (b >= ntiles) return;  // the whole block
   const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * TR;
+  DpPrev prev;
+  if (DP) prev = dp_prev<1>(dp, b);
   stage_rows<R, kVdTW, G::LR, LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
   stage_rows<R, kVdTW, G::LR, LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
   if (XS) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
@@ -600,7 +602,7 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
     else
       rows(std::false_type{});
   }
-  if (DP) dp_commit(dp, b, a0, 0.0);
+  if (DP) dp_commit<1>(dp, b, prev, a0, 0.0);
 }
 
 template <class R, int LOSS>

@@ -55,9 +55,9 @@ int64_t best_split(int64_t l, int64_t c) {
 
 class Builder {
  public:
-  Builder(int32_t T, bool needs_state, int32_t fuse_fwd, int32_t fuse_adj)
+  Builder(int32_t T, bool needs_state, int32_t fuse_fwd, int32_t fuse_adj, bool pair_tail)
       : T_(T), needs_state_(needs_state), fuse_fwd_(std::max(fuse_fwd, 1)),
-        fuse_adj_(std::max(fuse_adj, 1)) {}
+        fuse_adj_(std::max(fuse_adj, 1)), pair_tail_(pair_tail && fuse_fwd > 2) {}
 
   std::vector<adst_action> acts;
   int32_t slots_used = 0;
@@ -92,12 +92,19 @@ class Builder {
   // From buffer b holding x_i, compute x_{i+1}..x_j through the work buffers;
   // the last step writes final_dst instead when one is given. Returns the
   // buffer holding x_j. The intermediate states are read by nothing else, so
-  // with fusion on they are computed up to fuse_fwd_ steps per launch.
+  // with fusion on they are computed up to fuse_fwd_ steps per launch. With
+  // pair_tail_, a run into a slot whose last fuse_fwd_ + 1 steps would be a
+  // full launch and a single step takes them as two launches of about half
+  // depth. Runs into a work buffer keep the single step last: the adjoint
+  // step that reads the result may take it into its own launch, or a
+  // store-through launch the steps after it.
   int32_t advance(int32_t b, int32_t i, int32_t j, int32_t final_dst) {
     int32_t cur = b;
     int32_t t = i;
     while (t < j) {
-      const int32_t n = std::min(fuse_fwd_, j - t);
+      int32_t n = std::min(fuse_fwd_, j - t);
+      if (pair_tail_ && final_dst >= ADST_BUF_SLOT0 && j - t == fuse_fwd_ + 1)
+        n = (fuse_fwd_ + 2) / 2;
       t += n;
       const int32_t dst = (t == j && final_dst != ADST_BUF_NONE) ? final_dst : other_work(cur);
       if (n >= 2)
@@ -246,6 +253,7 @@ class Builder {
   int32_t T_;
   bool needs_state_;
   int32_t fuse_fwd_, fuse_adj_;  // most steps per launch (1 = no fusion)
+  bool pair_tail_;               // see advance()
   bool seeded_ = false;
   std::vector<int32_t> free_;
 };
@@ -268,8 +276,8 @@ constexpr int64_t kMaxActions = int64_t(1) << 24;
 }  // namespace
 
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       int32_t fuse_fwd, int32_t fuse_adj, bool pipelined, Plan* out,
-                       std::string* err) {
+                       int32_t fuse_fwd, int32_t fuse_adj, bool pair_tail, bool pipelined,
+                       Plan* out, std::string* err) {
   if (steps < 0) {
     *err = "steps must be >= 0";
     return ADST_ERR_ARG;
@@ -298,7 +306,7 @@ adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool n
     return ADST_ERR_UNSUPPORTED;
   }
 
-  Builder b(steps, needs_state, fuse_fwd, needs_state ? 1 : fuse_adj);
+  Builder b(steps, needs_state, fuse_fwd, needs_state ? 1 : fuse_adj, pair_tail);
   if (steps == 0) {
     b.zero_steps();
   } else if (!needs_state && pipelined) {

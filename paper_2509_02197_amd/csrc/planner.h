@@ -35,12 +35,15 @@ inline int64_t store_all_slots(int64_t T) { return T > 2 ? T - 2 : 0; }
 // budget allows (x0 excluded). sched may be AUTO. fuse_fwd lets up to that
 // many forward steps whose intermediate states nothing reads share one launch
 // (FWD2 with n steps; 1 = no fusion); fuse_adj does the same for state-free
-// adjoint steps (ADJ2). pipelined (the in-place kind) turns a state-free
-// plan into one pipelined forward run and one pipelined reverse run (FWDW,
-// ADJW). Returns ADST_OK or ADST_ERR_BUDGET / ADST_ERR_ARG /
-// ADST_ERR_UNSUPPORTED with *err filled.
+// adjoint steps (ADJ2). pair_tail: a run into a checkpoint slot that would
+// end with one step after a launch of fuse_fwd steps ends with two launches
+// of about half that depth instead, for kinds where those cost less (the
+// step count, the launch count and the stored states stay the same).
+// pipelined (the in-place kind) turns a state-free plan into one pipelined
+// forward run and one pipelined reverse run (FWDW, ADJW). Returns ADST_OK or
+// ADST_ERR_BUDGET / ADST_ERR_ARG / ADST_ERR_UNSUPPORTED with *err filled.
 adst_status build_plan(int32_t steps, int64_t slots_avail, int32_t sched, bool needs_state,
-                       int32_t fuse_fwd, int32_t fuse_adj, bool pipelined, Plan* out,
-                       std::string* err);
+                       int32_t fuse_fwd, int32_t fuse_adj, bool pair_tail, bool pipelined,
+                       Plan* out, std::string* err);
 
 }  // namespace adst

@@ -4,8 +4,8 @@ result (x_{t-1} formed on chip, never stored), against one launch per step
 and against the oracle (needs an MI355X).
 
 The plain adjoint launch owns a 64 x 16 region of every plane (64 lanes by
-four waves of four rows; 64 x 32, eight rows per wave, where a plane holds
-4 MiB or more); the fused
+four waves of four rows; 64 x 32, eight waves of four rows, where a plane
+holds 4 MiB or more); the fused
 forward-adjoint launches own a 64 x 16 region (one or two levels) or a
 64 x 32 region of eight waves (three levels), and their output tile is the
 region less n-1 cells per side for n forward levels (56 columns wide for

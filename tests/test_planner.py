@@ -335,6 +335,56 @@ def test_fused_plans_replay_with_the_same_step_counts(kind, flags, sched, slots)
         assert all(a[4] <= depth for a in fused if a[0] == adst.ADST_OP_ADJ2)
 
 
+def _runs_into_slots(acts):
+    """(steps per launch of each run whose last launch writes a slot)."""
+    FWD, FWD2, SLOT0 = adst.ADST_OP_FWD, adst.ADST_OP_FWD2, adst.ADST_BUF_SLOT0
+    runs, cur = [], []
+    for i, a in enumerate(acts):
+        if a[0] not in (FWD, FWD2):
+            cur = []
+            continue
+        prev = acts[i - 1] if i else None
+        chained = (cur and prev[0] in (FWD, FWD2) and prev[3] == a[2]
+                   and prev[1] == a[1] - a[4] and prev[3] < SLOT0)
+        cur = cur + [a[4]] if chained else [a[4]]
+        if a[3] >= SLOT0:
+            runs.append(cur)
+            cur = []
+    return runs
+
+
+@pytest.mark.parametrize("T,slots", [(40, 6), (64, 3), (100, 15), (200, 7), (200, 3)])
+def test_allencahn_runs_into_slots_end_in_pairs(T, slots):
+    """An Allen-Cahn run into a checkpoint slot that would end with a single
+    step after a 3-step launch ends with two 2-step launches instead (two
+    2-step launches cost less than a 3-step launch and a single step); which
+    states are computed and kept, the step count and the launch count stay
+    those of the plain split (the other kinds keep it)."""
+    p = prob(dims=(6, 5, 4))
+    b = budget_for(slots, p)
+    acts = adst.adst_plan_actions(p, T, b, adst.ADST_SCHED_BINOMIAL)
+    runs = _runs_into_slots(acts)
+    assert runs and not any(len(r) >= 2 and r[-2:] == [3, 1] for r in runs)
+    plain = [sum(r) for r in runs]
+    assert all(r == [3] * ((n - 4) // 3) + [2, 2] for r, n in zip(runs, plain) if n % 3 == 1 and n > 3)
+    assert all(r == [3] * (n // 3) + ([n % 3] if n % 3 else []) for r, n in zip(runs, plain)
+               if n % 3 != 1 or n == 1)
+    nf, _ = replay(acts, T, True, slots)
+    pn = prob(dims=(6, 5, 4), flags=adst.ADST_NO_FUSE)
+    plainacts = adst.adst_plan_actions(pn, T, b, adst.ADST_SCHED_BINOMIAL)
+    kept = lambda L: [(a[1], a[3]) for a in L if a[0] in (adst.ADST_OP_FWD, adst.ADST_OP_FWD2)
+                      and a[3] >= adst.ADST_BUF_SLOT0]
+    assert kept(acts) == kept(plainacts)
+    assert nf == cp.forward_steps_binomial(T, slots + 1)
+    if (T, slots) == (200, 7):
+        assert sum(1 for r in runs if r[-2:] == [2, 2]) == 14
+    # Jacobi with a forced tape (six steps per launch) keeps the single step
+    pj = prob(adst.ADST_JACOBI2D5, (6, 5, 1), flags=adst.ADST_FORCE_TAPE)
+    runs = _runs_into_slots(adst.adst_plan_actions(pj, T, budget_for(slots, pj),
+                                                   adst.ADST_SCHED_BINOMIAL))
+    assert all(r == [6] * (sum(r) // 6) + ([sum(r) % 6] if sum(r) % 6 else []) for r in runs)
+
+
 def test_elided_jacobi_fuses_everything():
     """Jacobi steps go up to six per launch, forward and adjoint; the
     remainder takes the last forward launch and the last adjoint launch."""
