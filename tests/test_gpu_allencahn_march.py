@@ -12,8 +12,9 @@ region less n-1 cells per side for n forward levels (56 columns wide for
 two); all march over 64-plane chunks, and the forward steps' neighbours come
 from a one-cell ring read with the region. The shapes put grids narrower
 than one tile, exact tiles, tiles plus one and ragged tails against these
-sizes in every axis, with one to three planes, and two grids with planes of
-over 4 MiB.
+sizes in every axis, with one to three planes, grids with planes of over
+4 MiB (one of a single plane), and planes of exactly 4 MiB and one row less,
+either side of the rule that picks the region.
 
 Bars: gradients of binomial plans (whose adjoint steps read states a
 single recomputed step produced) bit-identical to one launch per step and
@@ -38,6 +39,9 @@ SHAPES = [
     (F64, (7, 50, 1)), (F32, (17, 31, 97)), (F32, (66, 16, 64)),
     (F64, (4, 32, 64)), (F64, (70, 65, 66)), (F32, (3, 96, 130)),
     (F64, (3, 515, 1030)), (F32, (2, 1057, 1100)), (F64, (5, 28, 60)), (F64, (66, 29, 61)),
+    # one plane of over 4 MiB; planes of exactly 4 MiB (the taller region) and
+    # one row less (the 64 x 16 region)
+    (F64, (1, 515, 1030)), (F64, (2, 512, 1024)), (F64, (2, 511, 1024)),
 ]
 
 
