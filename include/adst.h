@@ -45,8 +45,10 @@
  * Conventions for every call:
  *   - All device memory is caller-owned; adst never allocates or frees device
  *     memory. Pointers are device addresses on the current HIP device.
- *   - Inputs (x0, coeff, loss_aux) are read-only; x0 serves as the free base
- *     checkpoint and must stay untouched until the stream reaches the call.
+ *   - Inputs (x0, coeff, loss_aux) are read-only and must stay untouched
+ *     until the call's work on the stream has run: x0 serves as the free
+ *     base checkpoint, and for DOT_W and SEED the first adjoint step reads
+ *     g_T from loss_aux itself.
  *   - Outputs are overwritten (=, never +=).
  *   - Calls that take a stream only enqueue work on it and never synchronise,
  *     except with ADST_TRACE set (see below). Argument errors are detected

@@ -272,12 +272,22 @@ std::string kernel_label(const Checked& c, const adst_action& a, int32_t stored,
   return n;
 }
 
+// For the dot-product and explicit-seed losses g_T is loss_aux itself: the
+// first adjoint launch reads it there, and the loss pass reads x_T and
+// loss_aux and writes no g_T. The in-place kind reverses in dx0 itself and
+// the limiter's separate mask pass rewrites g_t in place, so both keep the
+// copy, as does a call of zero steps (dx0 = g_T).
+bool seed_in_aux(const Checked& c, int32_t loss, int32_t steps) {
+  return (loss == ADST_LOSS_DOT_W || loss == ADST_LOSS_SEED) && steps > 0 && !c.in_place &&
+         !(c.shape.limit && !adjoint_applies_limit(c.shape, c.want_dp));
+}
+
 void fill_info(const Checked& c, const Plan& plan, uint64_t budget, bool want_dk, int32_t loss,
                adst_plan_info* info) {
   const Layout L = layout_for(c, plan);
   const PerPoint pp = per_point_bytes(c, want_dk, loss);
-  const uint64_t fb = pp.fwd, ab = pp.adj, ab1 = pp.adj_first, sb = pp.seed,
-                 db = pp.adj_extra + pp.mask;
+  const uint64_t sb = seed_in_aux(c, loss, plan.steps) ? 2 * itemsize(c.shape.dtype) : pp.seed;
+  const uint64_t fb = pp.fwd, ab = pp.adj, ab1 = pp.adj_first, db = pp.adj_extra + pp.mask;
   *info = adst_plan_info{};
   info->steps = plan.steps;
   info->sched = plan.sched;
@@ -608,6 +618,7 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
   void* gcur = (c.in_place || plan.adj_launches % 2 == 0) ? dx0 : gws;
   void* gnext = (gcur == dx0) ? gws : dx0;
   void* const g_T = gcur;
+  const bool g_T_is_aux = seed_in_aux(c, loss, steps);
   double* dp_part = reinterpret_cast<double*>(wsb + L.dp);
   auto buffer = [&](int32_t id) -> void* {
     switch (id) {
@@ -623,6 +634,8 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
   const PerPoint pp = per_point_bytes(c, want_dk, loss);
   const double npts = double(c.npoints);
   bool seeded = false, first_adj = true;
+  // the gradient the next adjoint launch reads
+  auto g_in = [&]() -> const void* { return first_adj && g_T_is_aux ? loss_aux : gcur; };
   hipError_t e = hipSuccess;
   auto traced = [&](Tracer::Cat cat, std::string label, double bytes, auto&& launch,
                     int64_t launches = 1) -> hipError_t {
@@ -636,7 +649,7 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
     const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
     const hipError_t r = traced(Tracer::ADJ, "ac_march<fwd" + std::to_string(f.n) + "+adj>",
                                 bytes, [&] {
-                                  return ac_launch_forward_adjoint(c.shape, buffer(f.src), gcur,
+                                  return ac_launch_forward_adjoint(c.shape, buffer(f.src), g_in(),
                                                                    gnext, f.n, stream);
                                 });
     std::swap(gcur, gnext);
@@ -699,14 +712,17 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
       case ADST_OP_SEED: {
         const void* xsrc = buffer(a.src);
         void* xcopy = (steps == 0 && xT) ? xT : nullptr;
-        // the half square with x_T already in g_T's buffer only reads it
+        // the half square with x_T already in g_T's buffer only reads it;
+        // with g_T read from loss_aux the pass reads x_T and loss_aux only
+        const double isz = double(itemsize(c.shape.dtype));
         const double seed_bytes =
-            (loss == ADST_LOSS_HALF_SQ && xsrc == g_T ? double(itemsize(c.shape.dtype))
+            (loss == ADST_LOSS_HALF_SQ && xsrc == g_T ? isz
+             : g_T_is_aux                             ? 2.0 * isz
                                                       : double(pp.seed)) +
-            (xcopy ? double(itemsize(c.shape.dtype)) : 0.0);
+            (xcopy ? isz : 0.0);
         e = traced(cat, "seed_loss", npts * seed_bytes, [&] {
-          return launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux, g_T, xcopy, partials,
-                             stream);
+          return launch_seed(c.shape.dtype, loss, c.npoints, xsrc, loss_aux,
+                             g_T_is_aux ? nullptr : g_T, xcopy, partials, stream);
         });
         if (e == hipSuccess)
           e = traced(cat, "finalize_loss", 8.0 * seed_partials(c.npoints), [&] {
@@ -737,7 +753,7 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
         // constants' gradients, from g_t and x_{t-1}
         const double bytes = npts * double((first_adj ? pp.adj_first : pp.adj) + pp.adj_extra);
         e = traced(cat, kernel_label(c, a, 1, dparams != nullptr), bytes, [&] {
-          return launch_adjoint(c.shape, xs, coeff, gcur, gnext, dcoeff, a.t == steps,
+          return launch_adjoint(c.shape, xs, coeff, g_in(), gnext, dcoeff, a.t == steps,
                                 dparams ? dp_part : nullptr, a.t == steps, stream);
         });
         std::swap(gcur, gnext);
@@ -746,7 +762,7 @@ adst_status vjp_impl(const adst_problem* prob, const void* x0, const void* coeff
       }
       case ADST_OP_ADJ2:
         e = traced(cat, kernel_label(c, a, 1, false), npts * double(pp.adj), [&] {
-          return launch_adjoint_n(c.shape, gcur, gnext, a.n, stream);
+          return launch_adjoint_n(c.shape, g_in(), gnext, a.n, stream);
         });
         std::swap(gcur, gnext);
         first_adj = false;
