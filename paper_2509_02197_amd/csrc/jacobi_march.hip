@@ -507,12 +507,14 @@ __global__ __launch_bounds__(kLanes) void jacobi_lim_adjoint(const R* __restrict
   }
   const bool strip_in = s0 - H >= 2 && s0 - H + kLanes * V <= nx - 2;
   const bool st_lane = lane * V >= H && lane * V < H + OW;
+  // x and g are read once per step, with the non-temporal hint (4096^2
+  // f64: 90.5 -> 83.5 us per step; the hint on x alone did nothing)
   auto load = [&](const R* a, int row, R* out) {
     const int rr = min(max(row, lo_need), hi_need);
     const R* src = a + (int64_t)rr * nx;
     if constexpr (VEC) {
       const int cc = min(max(c0, 0), nx - V);
-      const vec_t t = *reinterpret_cast<const vec_t*>(src + cc);
+      const vec_t t = __builtin_nontemporal_load(reinterpret_cast<const vec_t*>(src + cc));
 #pragma unroll
       for (int e = 0; e < V; ++e) out[e] = t[e];
     } else {
