@@ -78,7 +78,7 @@ adst_status check_problem(const adst_problem* p, int32_t grads, Checked* out) {
     return fail(ADST_ERR_UNSUPPORTED, "this kind is 2-D: n[2] must be 1");
   // Every launch covers the grid with workgroups of 256 work-items: tiles of
   // 240 to 256 columns by 4 or 8 rows for the 2-D kinds, columns of 56 to 64
-  // by 8 to 16 points over 32 or 64 planes for the 3-D kind. The work-item
+  // by 8 to 16 points over 32 to 256 planes for the 3-D kind. The work-item
   // count of the smallest tiles must fit the 32-bit dispatch grid.
   const int64_t tiles =
       p->kind == ADST_ALLENCAHN3D7

@@ -418,7 +418,7 @@ __global__ __launch_bounds__(kThreads) void adj_allencahn3d7(const R* __restrict
 // neighbours), x(k) and x(k+2) at the thread's cells and ring cell stay in
 // registers, so every mask is evaluated from on-chip values and x is read
 // from HBM about once per point.
-template <class R, bool NT, int TW>
+template <class R, bool NT, int TW, int ZC>
 __global__ __launch_bounds__(kBX * TW) void adj_allencahn3d7_lim(const R* __restrict__ x,
                                                                  const R* __restrict__ g,
                                                                  R* __restrict__ gp, int nx,
@@ -441,8 +441,8 @@ __global__ __launch_bounds__(kBX * TW) void adj_allencahn3d7_lim(const R* __rest
     t.i = t.bx * kAcTX + (int)threadIdx.x;
     t.ja = t.by * TY + (int)threadIdx.y;
     t.jb = t.ja + TW;
-    t.z0 = (b / tiles_y) * kAcZC;
-    t.z1 = min(t.z0 + kAcZC, nz);
+    t.z0 = (b / tiles_y) * ZC;
+    t.z1 = min(t.z0 + ZC, nz);
   }
   const int plane = nx * ny;
   auto in = [&](int k, int j, int i) {
@@ -1114,11 +1114,15 @@ hipError_t adjoint1(const StepShape& s, const R* x, const R* g, R* gp, double* d
   adj_allencahn3d7<R, DPV, NTV><<<grid, block, 0, st>>>(x, g, gp, s.nx, s.ny, s.nz, tx, ty, nt, \
                                                          D, k0, k1, dp)
   // waves (and rows per half-tile) of the limiter's adjoint: 64 x 16 tiles
-  // (0.703 -> 0.686 ms per 512^3 step against 64 x 8; 64 x 32 was slower)
-  constexpr int kLimTW = 8;
-  const int tyl = cdiv(s.ny, 2 * kLimTW), ntl = tx * tyl * cdiv(s.nz, kAcZC);
-#define ADST_AC_LIM(NTV)                                                                   \
-  adj_allencahn3d7_lim<R, NTV, kLimTW><<<dim3(xcd_grid(ntl)), dim3(kBX, kLimTW), 0, st>>>( \
+  // (0.703 -> 0.686 ms per 512^3 step against 64 x 8; 64 x 32 was slower),
+  // marching over 256-plane chunks (0.686 -> 0.620 ms against 32 planes;
+  // 128: 0.636). The other tiled kernels keep 32: at 128 the forward with
+  // the limiter went from 0.409 to 0.436 ms and the adjoint with the
+  // constants' partials from 0.629 to 0.653.
+  constexpr int kLimTW = 8, kLimZC = 256;
+  const int tyl = cdiv(s.ny, 2 * kLimTW), ntl = tx * tyl * cdiv(s.nz, kLimZC);
+#define ADST_AC_LIM(NTV)                                                                          \
+  adj_allencahn3d7_lim<R, NTV, kLimTW, kLimZC><<<dim3(xcd_grid(ntl)), dim3(kBX, kLimTW), 0, st>>>( \
       x, g, gp, s.nx, s.ny, s.nz, tx, tyl, ntl, D, k0, k1, C, lim)
   if (dp_part && str)
     ADST_AC_ADJ(true, true);

@@ -158,7 +158,7 @@ def test_fused_limiter_adjoint_full_grid():
 # The Allen-Cahn adjoint applies the branch mask as it reads g (the step's
 # value re-evaluated at every cell it reads: its own, the six neighbours'
 # and the LDS ring's); with the constants' gradients it keeps the separate
-# mask pass. Shapes put the edges of its 64 x 16 x 32 tiles (64 x 8 x 32
+# mask pass. Shapes put the edges of its 64 x 16 x 256 tiles (64 x 8 x 32
 # for the constants' variant), ragged tails in every axis and one-plane and
 # one-row grids against the ring.
 FUSED_LIM_AC_SHAPES = [
@@ -166,6 +166,7 @@ FUSED_LIM_AC_SHAPES = [
     (F64, (3, 4, 5)), (F32, (17, 33, 65)), (F32, (64, 16, 128)),
     (F64, (64, 28, 112)), (F64, (65, 29, 113)), (F64, (130, 15, 57)), (F32, (129, 14, 56)),
     (F64, (33, 17, 64)), (F64, (31, 32, 65)),
+    (F64, (256, 6, 64)), (F64, (258, 9, 40)), (F32, (513, 5, 33)),
 ]
 
 
