@@ -35,9 +35,8 @@ namespace {
 // no formula evaluated at an in-grid point uses them.
 
 // Stage LR x LW elements of a, starting at global row row0 and column col0
-// (col0 a multiple of the vector width), into lds (row stride LW). NTL: with
-// the non-temporal hint on the whole-vector loads.
-template <class R, int NT, int LR, int LW, bool NTL = false>
+// (col0 a multiple of the vector width), into lds (row stride LW).
+template <class R, int NT, int LR, int LW>
 __device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int row0, int nx,
                                   int ny, bool vec) {
   constexpr int V = 16 / sizeof(R);
@@ -53,8 +52,7 @@ __device__ inline void stage_rows(R* lds, const R* __restrict__ a, int col0, int
 #pragma unroll
       for (int e = 0; e < V; ++e) dst[e] = R(0);
     } else if (vec && ii >= 0 && ii + V <= nx) {
-      const vec_t* p = reinterpret_cast<const vec_t*>(a + jj * nx + ii);
-      const vec_t v = NTL ? __builtin_nontemporal_load(p) : *p;
+      const vec_t v = *reinterpret_cast<const vec_t*>(a + jj * nx + ii);
 #pragma unroll
       for (int e = 0; e < V; ++e) dst[e] = v[e];
     } else {
@@ -519,11 +517,9 @@ __global__ __launch_bounds__(kVdTW) void adj_vardiff2d9(const R* __restrict__ x,
   const int i0 = (b % tiles_x) * kVdTW, j0 = (b / tiles_x) * TR;
   DpPrev prev;
   if (DP) prev = dp_prev<1>(dp, b);
-  // with states that exceed the cache, read with the non-temporal hint too
-  // (8192^2 f32 with dK: 0.304 -> 0.295 ms per step)
-  stage_rows<R, kVdTW, G::LR, LW, NT>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
-  stage_rows<R, kVdTW, G::LR, LW, NT>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
-  if (XS) stage_rows<R, kVdTW, G::LR, LW, NT>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, LW>(sg, g, i0 - G::V, j0 - 1, nx, ny, vec);
+  stage_rows<R, kVdTW, G::LR, LW>(sk, K, i0 - G::V, j0 - 1, nx, ny, vec);
+  if (XS) stage_rows<R, kVdTW, G::LR, LW>(sx, x, i0 - G::V, j0 - 1, nx, ny, vec);
   const int i = i0 + (int)threadIdx.x;
   // the accumulated dK of the thread's cells, requested with the staged
   // rows (the row loop is unrolled, so the registers stay static)
