@@ -59,11 +59,12 @@ constexpr int kLanes = 64;
 constexpr int kRows = 48;      // rows per chunk of an interior strip (42 for the
                                // adjoint measured the same: 56.3 against 56.1 us
                                // per 6-step launch at 4096^2, one rocprofv3 job)
-constexpr int kLimRows = 192;  // rows per chunk of the limiter's one-step adjoint:
-                               // with two arrays in flight, fewer and longer
-                               // waves were faster (48 / 64 / 128 / 192 / 256
-                               // rows: 99.5 / 93.5 / 92.7 / 90.4 / 102.9 us
-                               // per launch at 4096^2 f64)
+constexpr int kLimRows = 128;  // rows per chunk of the limiter's one-step adjoint:
+                               // with x and g read non-temporally, 64 / 96 /
+                               // 128 / 160 / 192 / 256 / 384 rows took 82.0 /
+                               // 82.3 / 81.5 / 86.5 / 83.4 / 97.2 / 115.0 us
+                               // per launch at 4096^2 f64 (before the hint,
+                               // 192 was best: 90.4 against 92.7 us at 128)
 constexpr int kEdgeRows = 12;  // rows per chunk of the first and last strip
 constexpr int kEndRows = 6;    // rows of a strip's first and last chunk, whose
                                // blocks near the grid's top and bottom edge

@@ -171,16 +171,16 @@ def test_gradient_mask():
     # bytes: every adjoint step also reads x_{t-1} for the partials
     assert withp.alg_bytes - (16 * 5 + 16 * 5 + 16) * 64 == 8 * 5 * 64
     # slot counts follow the adjoint's work items: Jacobi one per column strip
-    # (124 columns in f64) and row chunk (12 rows in the two edge strips, 192
+    # (124 columns in f64) and row chunk (12 rows in the two edge strips, 128
     # in the others, 6 at each end), Allen-Cahn 64 x 8 x 32 tiles, variable
     # coefficients 256 x 4 tiles (2 doubles per item, 4 KiB aligned)
     def march_items(nx, ny):
         ns = -(-nx // 124)
         chunks = lambda mid: 2 + -(-(ny - 12) // mid) if ny > 12 else 1
         nedge = 2 if ns >= 2 else 1
-        return nedge * chunks(12) + (ns - nedge) * chunks(192)
+        return nedge * chunks(12) + (ns - nedge) * chunks(128)
     assert march_items(600, 100) == 2 * 10 + 3 * 3
-    assert march_items(4096, 4096) == 2 * 343 + 32 * 24
+    assert march_items(4096, 4096) == 2 * 343 + 32 * 34
     for kind, dims, tiles in [(adst.ADST_JACOBI2D5, (600, 100, 1), march_items(600, 100)),
                               (adst.ADST_JACOBI2D5, (4096, 4096, 1), march_items(4096, 4096)),
                               (adst.ADST_ALLENCAHN3D7, (65, 9, 33), 2 * 2 * 2),

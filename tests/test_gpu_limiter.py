@@ -119,13 +119,14 @@ def test_infinite_bounds_give_the_unlimited_bits(kind, dtype, shape, T, loss):
 # the separate mask pass and the tiled adjoint. Both must give the same
 # dx0 bits. Shapes put the column strips (124 output columns in fp64, 248
 # in fp32), the row chunks (6 rows at each end of a strip, 12 between them
-# in the first and last strip and 192 in the others: heights 204/205 over
-# three or more strips) and the element path (odd widths) against the ring,
-# plus grids narrower than a strip and a few rows tall.
+# in the first and last strip and 128 in the others: heights 140/141 and
+# 268/269 over three or more strips) and the element path (odd widths)
+# against the ring, plus grids narrower than a strip and a few rows tall.
 FUSED_LIM_SHAPES = [
     (F64, (50, 124)), (F64, (49, 125)), (F64, (97, 248)), (F64, (3, 300)), (F64, (300, 3)),
     (F64, (5, 4)), (F64, (61, 351)), (F32, (50, 248)), (F32, (13, 249)), (F32, (100, 497)),
     (F32, (7, 5)), (F64, (204, 380)), (F64, (205, 373)), (F64, (410, 130)), (F32, (211, 750)),
+    (F64, (140, 380)), (F64, (141, 373)), (F64, (268, 130)), (F32, (269, 750)),
 ]
 
 
